@@ -1,0 +1,546 @@
+"""Pins of the float64 oracle against things other than itself.
+
+The paper prints no worked example, so the oracle is pinned by
+* hand-worked examples with numbers chosen to be checkable by eye,
+* a library special case (``torch.optim.SGD`` with momentum and decay),
+* library routines for the statistics (``numpy.var``, ``numpy.mean``),
+* closed forms of the gradient-variability metric (Eq. (5)),
+* exact rational brute force of the momentum recursion over three steps,
+* invariants (identical replicas, permutations, exact rescaling, K = 1),
+* expectations of the statistics under the seeded generator.
+Each test is meant to catch a class of mistakes (a dropped term, a wrong
+sign or index, a swapped operand, an off-by-one step).
+"""
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import OracleAGS
+from paper_2603_18112_amd import layouts, synth
+
+SD = layouts.LAYER_SCALE | layouts.LAYER_DECAY
+
+
+def _coarse(x):
+    """Round to multiples of 2^-10 (|x| < 16): at most 14 significant bits,
+    so small rational multiples stay exact in fp32."""
+    return (np.round(np.clip(x, -15, 15) * 1024) / 1024).astype(np.float32)
+
+
+def _layers(numels, flags=None, pad=8):
+    lay = layouts.custom_layout(numels, flags, pad=pad)
+    return lay, lay.table()
+
+
+# --------------------------------------------------------------------------
+# hand-worked example: K = 4, one layer of two elements
+
+
+H1_W = np.array([3.0, 4.0])
+H1_G = np.array([[2.0, 0.0], [0.0, 2.0], [0.0, 0.0], [2.0, 2.0]], np.float32)
+
+
+def test_hand_example_statistics():
+    # gbar = [1, 1]; deviations are (+-1, +-1) for every replica.
+    o = OracleAGS([(0, 2, SD)], 2, 4, H1_W, lr=0.1, momentum=0.9, weight_decay=5e-4)
+    st, gl = o.stats(H1_G)
+    assert st["w_sq"][0] == 25.0
+    assert st["g_sq"][0] == 2.0
+    assert st["var"][0] == 2.0        # (1/4) * (2 + 2 + 2 + 2)
+    assert st["gsmall_sq"][0] == 4.0  # replica 0 = [2, 0]
+    assert st["noise_ratio"][0] == 1.0
+    assert gl["delta"] == math.inf and gl["sensitive"] == 1
+
+
+def test_hand_example_ags_two_steps():
+    lam, eta, mu = 5e-4, 0.1, 0.9
+    o = OracleAGS([(0, 2, SD)], 2, 4, H1_W, lr=eta, momentum=mu, weight_decay=lam,
+                  eps=1e-8, refresh_every=1, small_replica=0)
+    # Step 1: no previous norm -> sensitive, unscaled; d = gbar + lam w.
+    st, gl = o.step(H1_G)
+    assert gl["sensitive"] == 1 and st["coef_a"][0] == 1.0 and st["coef_b"][0] == lam
+    np.testing.assert_allclose(o.m, [1.0015, 1.002], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(o.w, [2.89985, 3.8998], rtol=0, atol=1e-15)
+    # UpdateGradScale: ||g_small|| / (||g_large|| + eps) = 2 / (sqrt(2) + 1e-8),
+    # below s_max = sqrt(4) = 2.
+    s = 2.0 / (math.sqrt(2.0) + 1e-8)
+    assert abs(s - 1.414213552373095) < 1e-15
+    assert abs(st["gradscale"][0] - s) < 1e-15
+    # Step 2: same gradients -> Delta = 0 < 0.5 -> scaled by s.
+    st, gl = o.step(H1_G)
+    assert gl["delta"] == 0.0 and gl["sensitive"] == 0
+    assert abs(st["coef_a"][0] - s) < 1e-15
+    np.testing.assert_allclose(o.m, [2.317013477373095, 2.317963452373095], rtol=0, atol=1e-14)
+    np.testing.assert_allclose(o.w, [2.6681486522626905, 3.6680036547626904], rtol=0, atol=1e-14)
+    assert abs(st["w_sq"][0] - (2.89985 ** 2 + 3.8998 ** 2)) < 1e-12
+
+
+def test_hand_example_lars_one_step():
+    lam, eta, tau = 5e-4, 0.1, 1e-3
+    o = OracleAGS([(0, 2, SD)], 2, 4, H1_W, mode="lars", lr=eta, momentum=0.9,
+                  weight_decay=lam, trust_coef=tau)
+    st, _ = o.step(H1_G)
+    trust = tau * 5.0 / (math.sqrt(2.0) + lam * 5.0)
+    assert abs(trust - 0.0035292949349794095) < 1e-17
+    assert abs(st["coef_a"][0] - trust) < 1e-18
+    assert abs(st["coef_b"][0] - trust * lam) < 1e-20
+    np.testing.assert_allclose(o.w, [2.999646541112262, 3.999646364647515], rtol=0, atol=1e-14)
+
+
+# --------------------------------------------------------------------------
+# library special case: momentum SGD with weight decay
+
+
+def _torch_sgd_run(w0, lay, grads_per_step, lr, mu, lam, scales=None):
+    """torch.optim.SGD on float64 CPU tensors, one param per layer.
+
+    ``grads_per_step[t]`` is [K, n_flat]; the large-batch gradient is its
+    mean over replicas (torch.mean); ``scales[t][l]`` multiplies layer l's
+    gradient before the optimizer sees it (the AGS mapping G~ = s G).
+    """
+    params, groups = [], []
+    for l, (o, n, f) in enumerate(lay.table()):
+        p = torch.tensor(np.asarray(w0[o:o + n], np.float64), requires_grad=True)
+        params.append(p)
+        groups.append({"params": [p], "weight_decay": lam if f & layouts.LAYER_DECAY else 0.0})
+    opt = torch.optim.SGD(groups, lr=lr, momentum=mu, dampening=0, nesterov=False)
+    for t, g in enumerate(grads_per_step):
+        gm = torch.mean(torch.tensor(np.asarray(g, np.float64)), dim=0)
+        for l, (o, n, f) in enumerate(lay.table()):
+            s = 1.0 if scales is None else scales[t][l]
+            params[l].grad = gm[o:o + n].clone() * s
+        opt.step()
+    w = np.zeros(lay.n_flat)
+    m = np.zeros(lay.n_flat)
+    for l, (o, n, f) in enumerate(lay.table()):
+        w[o:o + n] = params[l].detach().numpy()
+        m[o:o + n] = opt.state[params[l]]["momentum_buffer"].numpy()
+    return w, m
+
+
+@pytest.mark.parametrize("mode", ["sgd", "ags_scale_off", "ags_no_refresh"])
+def test_sgd_special_case_matches_torch(mode):
+    rng = np.random.default_rng(1)
+    flags = [SD, layouts.LAYER_SCALE, layouts.LAYER_DECAY, 0, SD]
+    lay, table = _layers([37, 64, 5, 1, 200], flags)
+    K, steps, lr, mu, lam = 3, 5, 0.1, 0.9, 5e-4
+    w0 = np.zeros(lay.n_flat, np.float32)
+    for o, n, _ in table:
+        w0[o:o + n] = rng.standard_normal(n).astype(np.float32)
+    grads = []
+    for _ in range(steps):
+        g = np.zeros((K, lay.n_flat), np.float32)
+        for o, n, _ in table:
+            g[:, o:o + n] = rng.standard_normal((K, n)).astype(np.float32)
+        grads.append(g)
+    if mode == "sgd":
+        o = OracleAGS(table, lay.n_flat, K, w0, mode="sgd", lr=lr, momentum=mu, weight_decay=lam)
+    elif mode == "ags_scale_off":
+        t2 = [(a, b, f & ~layouts.LAYER_SCALE) for a, b, f in table]
+        o = OracleAGS(t2, lay.n_flat, K, w0, mode="ags", lr=lr, momentum=mu, weight_decay=lam)
+    else:
+        o = OracleAGS(table, lay.n_flat, K, w0, mode="ags", lr=lr, momentum=mu,
+                      weight_decay=lam, refresh_every=0)
+    for g in grads:
+        o.step(g)
+    w_ref, m_ref = _torch_sgd_run(w0, lay, grads, lr, mu, lam)
+    np.testing.assert_allclose(o.w, w_ref, rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(o.m, m_ref, rtol=1e-13, atol=1e-15)
+
+
+def test_ags_decisions_match_torch_with_prescaled_gradients():
+    """AGS = momentum SGD fed with gradscale (.) G on non-sensitive steps.
+
+    Step t's replicas are c_t times a base draw, so G_t = c_t^2 G_1 and the
+    variability of Eq. (5) is |c_t^2 / c_{t-1}^2 - 1| in closed form:
+    t=1: inf (sensitive), t=2: c=1.125 -> 0.265625 (scaled), t=3: c=2 ->
+    2.16 (sensitive), t=4: c=2 -> 0 (scaled).  Base values carry few
+    mantissa bits so that c * g is exact in fp32.  The scale applied at step t is the
+    one refreshed from step t-1's statistics: min(||g_r|| / (||gbar|| + eps),
+    sqrt(K)), computed here with numpy.linalg.norm.
+    """
+    rng = np.random.default_rng(7)
+    K = 4
+    flags = [SD, SD, SD, layouts.LAYER_DECAY, SD]
+    lay, table = _layers([50, 64, 30, 16, 100], flags)
+    w0 = np.zeros(lay.n_flat, np.float32)
+    base = np.zeros((K, lay.n_flat), np.float32)
+    for i, (o, n, _) in enumerate(table):
+        w0[o:o + n] = rng.standard_normal(n)
+        x = _coarse(rng.standard_normal(n))
+        if i == 1:    # replicas nearly cancel: ratio >> sqrt(K), clipped to 2
+            base[:, o:o + n] = np.stack([x, -x, x, -x + _coarse(0.01 * x)])
+        elif i == 2:  # the small replica is weak: ratio < 1 is kept (s < 1)
+            base[:, o:o + n] = np.stack([np.float32(0.125) * x, x, x, x])
+        else:
+            base[:, o:o + n] = x + _coarse(0.5 * rng.standard_normal((K, n)))
+    cs = [1.0, 1.125, 2.0, 2.0]
+    grads = [(np.float32(c) * base).astype(np.float32) for c in cs]
+    eps = 1e-8
+    o = OracleAGS(table, lay.n_flat, K, w0, mode="ags", lr=0.05, momentum=0.9,
+                  weight_decay=5e-4, eps=eps, refresh_every=1, small_replica=0)
+    expect_sens = [1, 0, 1, 0]
+    scales_applied, prev_scale = [], np.ones(len(table))
+    for t, g in enumerate(grads):
+        st, gl = o.step(g)
+        assert gl["sensitive"] == expect_sens[t]
+        if t == 1:
+            assert abs(gl["delta"] - (1.125 ** 2 - 1.0)) < 1e-12
+        if t == 2:
+            assert abs(gl["delta"] - (4.0 / 1.265625 - 1.0)) < 1e-12
+        applied = [prev_scale[l] if (not expect_sens[t] and table[l][2] & layouts.LAYER_SCALE)
+                   else 1.0 for l in range(len(table))]
+        np.testing.assert_allclose(st["coef_a"], applied, rtol=1e-15)
+        scales_applied.append(applied)
+        g64 = g.astype(np.float64)
+        new = np.ones(len(table))
+        for l, (oo, n, f) in enumerate(table):
+            if f & layouts.LAYER_SCALE:
+                gs = np.linalg.norm(g64[0, oo:oo + n])
+                gl_ = np.linalg.norm(np.mean(g64[:, oo:oo + n], axis=0))
+                new[l] = min(gs / (gl_ + eps), math.sqrt(K))
+            else:
+                new[l] = prev_scale[l]
+        np.testing.assert_allclose(st["gradscale"], new, rtol=1e-12)
+        prev_scale = new
+    assert prev_scale[1] == 2.0               # clipped at s_max = sqrt(K)
+    assert abs(prev_scale[2] - 0.125 / 0.78125) < 1e-9   # s < 1 allowed
+    w_ref, m_ref = _torch_sgd_run(w0, lay, grads, 0.05, 0.9, 5e-4, scales_applied)
+    np.testing.assert_allclose(o.w, w_ref, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(o.m, m_ref, rtol=1e-12, atol=1e-14)
+
+
+# --------------------------------------------------------------------------
+# statistics against library routines
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("r", [0, 2, -1])
+def test_statistics_match_numpy(dtype, r):
+    rng = np.random.default_rng(3)
+    K = 5
+    lay, table = _layers([1, 7, 64, 333, 1000])
+    w0 = rng.standard_normal(lay.n_flat).astype(np.float32)
+    g32 = (rng.standard_normal((K, lay.n_flat)) * 0.01).astype(np.float32)
+    g = synth.to_bf16_bits(g32) if dtype == "bf16" else g32
+    gv = synth.bf16_bits_to_f32(g) if dtype == "bf16" else g32
+    o = OracleAGS(table, lay.n_flat, K, w0, grad_dtype=dtype, small_replica=r)
+    st, gl = o.stats(g)
+    G_tot = 0.0
+    for l, (oo, n, _) in enumerate(table):
+        x = gv[:, oo:oo + n].astype(np.float64)
+        ww = w0[oo:oo + n].astype(np.float64)
+        W = np.dot(ww, ww)
+        G = np.sum(np.mean(x, axis=0) ** 2)
+        V = np.sum(np.var(x, axis=0))           # (1/K) sum_k (x_k - mean)^2
+        S = np.sum(x[r] ** 2) if r >= 0 else np.mean(np.sum(x ** 2, axis=1))
+        np.testing.assert_allclose([st["w_sq"][l], st["g_sq"][l], st["var"][l], st["gsmall_sq"][l]],
+                                   [W, G, V, S], rtol=1e-12)
+        np.testing.assert_allclose(st["noise_ratio"][l], V / G, rtol=1e-12)
+        G_tot += G
+    np.testing.assert_allclose(gl["g_sq"], G_tot, rtol=1e-12)
+
+
+def test_statistics_ignore_padding_and_other_layers():
+    # Values outside every layer (padding, stride tail) must not leak in.
+    K = 3
+    lay, table = _layers([5, 9])
+    stride = lay.n_flat + 24
+    g = np.full((K, stride), 1e6, np.float32)
+    for oo, n, _ in table:
+        g[:, oo:oo + n] = 1.0
+    w = np.full(lay.n_flat, 1e6, np.float32)
+    for oo, n, _ in table:
+        w[oo:oo + n] = 2.0
+    o = OracleAGS(table, lay.n_flat, K, w)
+    st, gl = o.stats(g)
+    np.testing.assert_array_equal(st["g_sq"], [5.0, 9.0])
+    np.testing.assert_array_equal(st["w_sq"], [20.0, 36.0])
+    np.testing.assert_array_equal(st["var"], [0.0, 0.0])
+
+
+# --------------------------------------------------------------------------
+# Eq. (5) closed forms
+
+
+@pytest.mark.parametrize("c,expect_delta,expect_sens", [
+    (0.5, 0.75, 1), (1.0, 0.0, 0), (2.0, 3.0, 1), (1.125, 0.265625, 0),
+    (0.75, 0.4375, 0)])
+def test_delta_closed_form(c, expect_delta, expect_sens):
+    rng = np.random.default_rng(11)
+    K = 2
+    lay, table = _layers([100, 28])
+    g1 = _coarse(rng.standard_normal((K, lay.n_flat)))
+    g2 = (np.float32(c) * g1).astype(np.float32)  # exact: few mantissa bits
+    o = OracleAGS(table, lay.n_flat, K, np.ones(lay.n_flat, np.float32), delta=0.5)
+    _, gl1 = o.step(g1)
+    _, gl2 = o.step(g2)
+    assert gl1["delta"] == math.inf and gl1["sensitive"] == 1
+    assert gl2["g_sq_prev"] == gl1["g_sq"]
+    assert abs(gl2["delta"] - expect_delta) < 1e-12
+    assert gl2["sensitive"] == expect_sens
+
+
+# --------------------------------------------------------------------------
+# exact rational brute force, three steps on ten elements
+
+
+def _q(x):
+    return Fraction(float(x))
+
+
+def _sqrt_q(x: Fraction) -> Fraction:
+    n, d = x.numerator, x.denominator
+    rn, rd = math.isqrt(n), math.isqrt(d)
+    assert rn * rn == n and rd * rd == d, "brute force needs a rational square root"
+    return Fraction(rn, rd)
+
+
+def _brute(w, grads_steps, K, mode, lr, mu, lam, delta, s_max):
+    """Exact rational AGS / SGD on one scaled+decayed layer, eps = 0."""
+    w = [_q(x) for x in w]
+    m = [Fraction(0)] * len(w)
+    scale, g_prev = Fraction(1), None
+    for t, g in enumerate(grads_steps, start=1):
+        gb = [sum(_q(g[k][j]) for k in range(K)) / K for j in range(len(w))]
+        G = sum(x * x for x in gb)
+        sens = True
+        if t > 1 and g_prev > 0:
+            sens = not (abs((G - g_prev) / g_prev) < delta)
+        a = scale if (mode == "ags" and not sens) else Fraction(1)
+        for j in range(len(w)):
+            d = a * gb[j] + lam * w[j]
+            m[j] = mu * m[j] + d
+            w[j] = w[j] - lr * m[j]
+        if mode == "ags":
+            S = sum(_q(g[0][j]) ** 2 for j in range(len(w)))
+            s = _sqrt_q(S / G)   # = sqrt(S) / (sqrt(G) + eps) with eps = 0
+            scale = min(s, s_max)
+        g_prev = G
+    return w, m
+
+
+@pytest.mark.parametrize("mode", ["sgd", "ags"])
+def test_bruteforce_three_steps_exact(mode):
+    # K = 4 replicas g0 = 1.5 u, g1 = 2.5 u, g2 = g3 = 0: gbar = u and
+    # ||g0|| / ||gbar|| = 3/2 exactly.  Step 2 repeats step 1 (Delta = 0,
+    # scaled), step 3 doubles it (Delta = 3, sensitive).
+    u = np.array([1, -2, 3, 0.5, -0.25, 4, -1, 2, 0.75, -3], np.float32)
+    g = np.stack([1.5 * u, 2.5 * u, 0 * u, 0 * u]).astype(np.float32)
+    steps = [g, g, (2 * g).astype(np.float32)]
+    w0 = np.array([0.5, 1, -1, 2, 0.25, -0.5, 3, -2, 1.5, 0.125], np.float32)
+    lr, mu, lam, delta = Fraction(1, 10), Fraction(9, 10), Fraction(1, 2000), Fraction(1, 2)
+    wq, mq = _brute(w0, steps, 4, mode, lr, mu, lam, delta, Fraction(2))
+    o = OracleAGS([(0, 10, SD)], 10, 4, w0, mode=mode, lr=0.1, momentum=0.9,
+                  weight_decay=5e-4, delta=0.5, eps=0.0, refresh_every=1)
+    sens = []
+    for gs in steps:
+        _, gl = o.step(gs)
+        sens.append(gl["sensitive"])
+    if mode == "ags":
+        assert sens == [1, 0, 1]
+        assert o.gradscale[0] == 1.5
+    np.testing.assert_allclose(o.w, [float(x) for x in wq], rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(o.m, [float(x) for x in mq], rtol=1e-14, atol=1e-15)
+
+
+# --------------------------------------------------------------------------
+# invariants
+
+
+def test_identical_replicas_have_zero_variance():
+    rng = np.random.default_rng(5)
+    lay, table = _layers([17, 64, 3])
+    x = rng.standard_normal(lay.n_flat).astype(np.float32)
+    for K in (1, 2, 7):
+        g = np.tile(x, (K, 1))
+        o = OracleAGS(table, lay.n_flat, K, x)
+        st, _ = o.stats(g)
+        assert np.all(st["var"] == 0.0)
+        assert np.all(st["noise_ratio"] == 0.0)
+
+
+def test_single_replica_reduces():
+    rng = np.random.default_rng(6)
+    lay, table = _layers([40, 9])
+    g = rng.standard_normal((1, lay.n_flat)).astype(np.float32)
+    o = OracleAGS(table, lay.n_flat, 1, np.ones(lay.n_flat, np.float32), eps=1e-8)
+    st, _ = o.step(g)
+    np.testing.assert_array_equal(st["gsmall_sq"], st["g_sq"])
+    np.testing.assert_array_equal(st["var"], 0.0)
+    nrm = np.sqrt(st["g_sq"])
+    np.testing.assert_allclose(st["gradscale"], nrm / (nrm + 1e-8), rtol=1e-15)
+    assert np.all(st["gradscale"] <= 1.0)   # s_max = sqrt(1)
+
+
+def test_replica_permutation_invariance():
+    rng = np.random.default_rng(8)
+    K = 6
+    lay, table = _layers([100, 31])
+    g = rng.standard_normal((K, lay.n_flat)).astype(np.float32)
+    w = rng.standard_normal(lay.n_flat).astype(np.float32)
+    perm = rng.permutation(K)
+    a, _ = OracleAGS(table, lay.n_flat, K, w, small_replica=-1).stats(g)
+    b, _ = OracleAGS(table, lay.n_flat, K, w, small_replica=-1).stats(g[perm].copy())
+    for f in ("w_sq", "g_sq", "var", "gsmall_sq"):
+        np.testing.assert_allclose(a[f], b[f], rtol=1e-14)
+
+
+def test_exact_rescaling():
+    # Multiplying every gradient by 2^p scales G, V, S by 4^p exactly and
+    # leaves rho and (with eps = 0) the scale unchanged.
+    rng = np.random.default_rng(9)
+    K = 4
+    lay, table = _layers([64, 10])
+    g = rng.standard_normal((K, lay.n_flat)).astype(np.float32)
+    w = rng.standard_normal(lay.n_flat).astype(np.float32)
+    a, _ = OracleAGS(table, lay.n_flat, K, w, eps=0.0).step(g)
+    b, _ = OracleAGS(table, lay.n_flat, K, w, eps=0.0).step((g * np.float32(8)).astype(np.float32))
+    for f in ("g_sq", "var", "gsmall_sq"):
+        np.testing.assert_array_equal(b[f], 64.0 * a[f])
+    np.testing.assert_array_equal(a["noise_ratio"], b["noise_ratio"])
+    np.testing.assert_array_equal(a["gradscale"], b["gradscale"])
+
+
+def test_variance_identity_and_bounds():
+    # V = (1/K) sum_k ||g_k||^2 - ||gbar||^2, and 0 < s <= s_max.
+    rng = np.random.default_rng(10)
+    K = 8
+    lay, table = _layers([500, 64, 8])
+    g = (rng.standard_normal((K, lay.n_flat)) * rng.uniform(0.1, 3, lay.n_flat)).astype(np.float32)
+    o = OracleAGS(table, lay.n_flat, K, np.zeros(lay.n_flat), small_replica=-1)
+    st, _ = o.step(g)
+    np.testing.assert_allclose(st["var"], st["gsmall_sq"] - st["g_sq"], rtol=1e-10)
+    assert np.all(st["gradscale"] > 0) and np.all(st["gradscale"] <= math.sqrt(K))
+
+
+# --------------------------------------------------------------------------
+# degenerate cases
+
+
+def test_zero_gradients():
+    K = 3
+    lay, table = _layers([10, 20])
+    o = OracleAGS(table, lay.n_flat, K, np.ones(lay.n_flat), refresh_every=1)
+    z = np.zeros((K, lay.n_flat), np.float32)
+    st, gl = o.step(z)
+    np.testing.assert_array_equal(st["noise_ratio"], 0.0)
+    np.testing.assert_array_equal(st["gradscale"], 1.0)     # zero-norm fallback
+    st, gl = o.step(z)
+    assert gl["delta"] == math.inf and gl["sensitive"] == 1  # G_prev = 0
+
+
+def test_zero_mean_with_noise_gives_infinite_ratio():
+    lay, table = _layers([4])
+    g = np.zeros((2, lay.n_flat), np.float32)
+    g[0, :4], g[1, :4] = 1.0, -1.0
+    st, _ = OracleAGS(table, lay.n_flat, 2, np.ones(lay.n_flat)).stats(g)
+    assert st["g_sq"][0] == 0.0 and st["var"][0] == 4.0 and st["noise_ratio"][0] == math.inf
+
+
+def test_lars_zero_weight_trust_is_one():
+    lay, table = _layers([16])
+    g = np.ones((2, lay.n_flat), np.float32)
+    st, _ = OracleAGS(table, lay.n_flat, 2, np.zeros(lay.n_flat), mode="lars").step(g)
+    assert st["coef_a"][0] == 1.0
+
+
+def test_nonfinite_gradient_is_flagged_and_sensitive():
+    lay, table = _layers([8, 8])
+    g = np.ones((2, lay.n_flat), np.float32)
+    o = OracleAGS(table, lay.n_flat, 2, np.ones(lay.n_flat))
+    o.step(g)
+    g2 = g.copy()
+    g2[1, 3] = np.nan
+    _, gl = o.step(g2)
+    assert gl["nonfinite"] == 1 and gl["sensitive"] == 1
+
+
+# --------------------------------------------------------------------------
+# state: stats() does not mutate, checkpoint / resume is exact
+
+
+def test_stats_call_does_not_mutate():
+    rng = np.random.default_rng(12)
+    lay, table = _layers([33, 64])
+    g = rng.standard_normal((3, lay.n_flat)).astype(np.float32)
+    o = OracleAGS(table, lay.n_flat, 3, rng.standard_normal(lay.n_flat))
+    o.step(g)
+    before = (o.w.copy(), o.m.copy(), o.get_state())
+    o.stats(g * np.float32(3))
+    np.testing.assert_array_equal(o.w, before[0])
+    np.testing.assert_array_equal(o.m, before[1])
+    s = o.get_state()
+    np.testing.assert_array_equal(s[0], before[2][0])
+    assert s[1:] == before[2][1:]
+
+
+def test_checkpoint_resume_is_bitwise():
+    lay = layouts.get_layout("tiny_cnn")
+    w0 = synth.init_weights(lay, 0)
+    grads = [synth.replica_grads(lay, 4, t, 0) for t in range(4)]
+    a = OracleAGS(lay.table(), lay.n_flat, 4, w0)
+    for g in grads:
+        a.step(g)
+    b = OracleAGS(lay.table(), lay.n_flat, 4, w0)
+    for g in grads[:2]:
+        b.step(g)
+    c = OracleAGS(lay.table(), lay.n_flat, 4, b.w, b.m)
+    c.set_state(*b.get_state())
+    for g in grads[2:]:
+        c.step(g)
+    np.testing.assert_array_equal(a.w, c.w)
+    np.testing.assert_array_equal(a.m, c.m)
+    np.testing.assert_array_equal(a.gradscale, c.gradscale)
+
+
+# --------------------------------------------------------------------------
+# expectations under the generator (c = noise / sigma)
+
+
+@pytest.mark.parametrize("K,c,dtype", [(16, 0.5, "bf16"), (4, 2.0, "f32"), (8, 0.1, "f32")])
+def test_statistics_expectations_under_generator(K, c, dtype):
+    lay = layouts.custom_layout([4096, 20000, 1500], pad=64)
+    sig = synth.layer_sigmas(lay, 3)
+    g = synth.replica_grads(lay, K, 0, 3, noise=c, dtype=dtype, sigmas=sig)
+    o = OracleAGS(lay.table(), lay.n_flat, K, np.zeros(lay.n_flat), grad_dtype=dtype)
+    st, _ = o.stats(g)
+    for l in range(lay.n_layers):
+        n, s2 = float(lay.numels[l]), sig[l] ** 2
+        tol = 6.0 / math.sqrt(n)
+        assert abs(st["g_sq"][l] / (n * s2 * (1 + c * c / K)) - 1) < tol
+        assert abs(st["var"][l] / (n * s2 * c * c * (K - 1) / K) - 1) < tol
+        assert abs(st["gsmall_sq"][l] / (n * s2 * (1 + c * c)) - 1) < tol
+
+
+def test_tie_at_threshold_is_sensitive():
+    # Algorithm 1 scales only when Delta < delta; Delta == delta is a
+    # sensitive step.  ||gbar||^2 goes 2 -> 3, so Delta = 0.5 exactly.
+    g1 = np.array([[1.0, 1.0, 0.0, 0, 0, 0, 0, 0]], np.float32)
+    g2 = np.array([[1.0, 1.0, 1.0, 0, 0, 0, 0, 0]], np.float32)
+    o = OracleAGS([(0, 3, SD)], 8, 1, np.ones(8), delta=0.5)
+    o.step(g1)
+    o.set_state([0.5], o.get_state()[1], o.get_state()[2])
+    st, gl = o.step(g2)
+    assert gl["delta"] == 0.5 and gl["sensitive"] == 1 and st["coef_a"][0] == 1.0
+    o2 = OracleAGS([(0, 3, SD)], 8, 1, np.ones(8), delta=0.5 + 2 ** -20)
+    o2.step(g1)
+    o2.set_state([0.5], o2.get_state()[1], o2.get_state()[2])
+    st, gl = o2.step(g2)
+    assert gl["sensitive"] == 0 and st["coef_a"][0] == 0.5
+
+
+def test_unscaled_layer_ignores_gradscale_state():
+    # A layer without the scale flag is never scaled, even if its stored
+    # gradscale (e.g. restored from a checkpoint) differs from 1.
+    lay, table = _layers([8, 8], [SD, layouts.LAYER_DECAY])
+    g = np.ones((2, lay.n_flat), np.float32)
+    o = OracleAGS(table, lay.n_flat, 2, np.ones(lay.n_flat), refresh_every=0)
+    o.step(g)
+    o.set_state([1.5, 3.0], o.get_state()[1], o.get_state()[2])
+    st, gl = o.step(g)
+    assert gl["sensitive"] == 0
+    assert st["coef_a"][0] == 1.5 and st["coef_a"][1] == 1.0
