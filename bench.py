@@ -1,0 +1,241 @@
+"""Benchmark of the AGS step + gradient statistics on one MI355X.
+
+Workload: ResNet-50 ImageNet layout (161 tensors, 25,557,032 parameters),
+K = 16 bf16 replica gradients, fp32 weights and momentum, AGS mode.  A step
+is one full pass of the hot path: replica mean, per-layer statistics,
+decision, update (three kernels on one stream).  Inputs are seeded and
+synthetic and already resident in HBM when timing starts; the timed steps
+reuse one generated gradient set.
+
+Prints one JSON line (last line of stdout):
+  value          algorithmic GB/s of the whole step: (K*2 + 16) bytes per
+                 parameter per step (each replica read once, w and m read and
+                 written once) over the measured step time
+  roofline       the dominant kernel's algorithmic bytes per launch over its
+                 average duration (HIP events on the launch stream), against
+                 the 8 TB/s HBM peak; traffic = HBM bytes per launch from
+                 rocprofv3 FETCH_SIZE/WRITE_SIZE (committed summary), or null
+                 when the kernels changed since it was taken
+  cpu_baseline   the float64 oracle on the host on whole steps of the same
+                 workload (a reported baseline, not a target)
+
+Usage: python bench.py [--gpus 1] [--steps 200] [--warmup 20]
+                       [--no-cpu-baseline] [--copy-probe]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+WORKLOAD = "resnet50_k16_bf16"
+K = 16
+E_G = 2  # bytes per bf16 gradient element
+HYPER = dict(lr=0.1, momentum=0.9, weight_decay=5e-4, delta=0.5, eps=1e-8, s_max=0.0,
+             trust_coef=1e-3, refresh_every=1, small_replica=0)
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2603_18112_amd", "csrc", "ags_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_resnet50_k16_bf16.txt")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    for p in (KERNEL_SOURCE, os.path.join(ROOT, "paper_2603_18112_amd", "csrc", "ags_internal.h")):
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(n_params: int):
+    """Per-launch algorithmic bytes of each kernel and of the whole step."""
+    materialized = K * E_G > 8
+    stats = n_params * (K * E_G + 4 + (4 if materialized else 0))  # replicas + w (+ gbar out)
+    update = n_params * ((4 if materialized else K * E_G) + 16)   # gbar/replicas + w,m in+out
+    step = n_params * (K * E_G + 16)
+    return {"stats": stats, "finalize": 0, "update": update, "step": step}
+
+
+def read_traffic(kernel: str):
+    """HBM bytes per launch for ``kernel`` from the committed counter summary,
+    if it was taken on the current kernel source."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as f:
+            for line in f:
+                if "=" in line and not line.lstrip().startswith("#"):
+                    k, v = line.split("=", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("kernel_source_sha") != kernel_source_sha():
+            return None
+        v = kv.get(f"{kernel}_bytes_per_launch")
+        return float(v) if v else None
+    except OSError:
+        return None
+
+
+def copy_probe(torch, nbytes=1 << 30, reps=20):
+    """Device-to-device copy bandwidth (read + write bytes / time)."""
+    n = nbytes // 4
+    a = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return 2 * n * 4 / (ms * 1e-3) / 1e9
+
+
+def cpu_baseline(layout, w0, grads_np, budget_s=12.0, max_steps=8):
+    """The float64 oracle as it stands, single-threaded, on whole steps."""
+    from oracle import OracleAGS
+    o = OracleAGS(layout.table(), layout.n_flat, K, w0, grad_dtype="bf16", **HYPER)
+    times = []
+    t_start = time.time()
+    while len(times) < max_steps and (time.time() - t_start) < budget_s:
+        t0 = time.perf_counter()
+        o.step(grads_np)
+        times.append(time.perf_counter() - t0)
+    sec = sorted(times)[len(times) // 2]
+    return sec, len(times)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run the 1 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the hot path measured here is the "
+              f"single-GPU AGS step (got --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2603_18112_amd import ags, layouts, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    if args.copy_probe:
+        bw = copy_probe(torch)
+        log(f"copy probe: {bw:.1f} GB/s")
+        print(json.dumps({"copy_probe_GBps": round(bw, 1), "bytes_per_copy": 2 * (1 << 30)}))
+        return
+
+    lib = ags.load_library()
+    log(f"libags: {ags.library_path()}")
+    lay = layouts.get_layout("resnet50")
+    N = lay.n_params
+    t0 = time.time()
+    w0 = synth.init_weights(lay, 0)
+    g_np = synth.replica_grads(lay, K, 0, 0, dtype="bf16")
+    log(f"inputs generated in {time.time() - t0:.1f}s: {N} params, K={K} bf16 "
+        f"({g_np.nbytes / 1e9:.2f} GB of gradients)")
+
+    w = torch.from_numpy(w0.copy()).cuda()
+    m = torch.zeros_like(w)
+    g = torch.from_numpy(g_np.view(np.int16)).cuda()
+    stream = torch.cuda.current_stream()
+    h = ags.AGS(lay.table(), w, m, K, grad_dtype="bf16", mode="ags", **HYPER)
+
+    for _ in range(args.warmup):
+        h.step(g, stream)
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps done")
+
+    # Timed region: K steps between two events on the launch stream, with the
+    # library's per-kernel events enabled (they sit on the same stream).
+    h.set_profiling(True)
+    h.kernel_times()  # reset
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        h.step(g, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = e0.elapsed_time(e1)
+    kms, ncalls = h.kernel_times()
+    h.set_profiling(False)
+    ms_step = ms_total / args.steps
+    log(f"timed {args.steps} steps: {ms_step * 1e3:.1f} us/step; per kernel (us): "
+        + ", ".join(f"{n} {kms[i] / ncalls * 1e3:.1f}" for i, n in enumerate(ags.KERNEL_NAMES)))
+    s = h.read_stats()
+
+    ab = algorithmic_bytes(N)
+    value = ab["step"] / (ms_step * 1e-3) / 1e9
+    avg_ms = {n: kms[i] / ncalls for i, n in enumerate(ags.KERNEL_NAMES)}
+    dom = max(avg_ms, key=avg_ms.get)
+    achieved = ab[dom] / (avg_ms[dom] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": read_traffic(dom),
+                "algorithmic_bytes_per_launch": ab[dom],
+                "avg_launch_us": round(avg_ms[dom] * 1e3, 2)}
+
+    copy_bw = copy_probe(torch)
+    log(f"device copy: {copy_bw:.1f} GB/s")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline: oracle on whole steps ...")
+        sec, n = cpu_baseline(lay, w0, g_np)
+        cpu = {"value": round(ab["step"] / sec / 1e9, 3), "unit": "GB/s", "cores": 1,
+               "kind": "oracle", "sec_per_step": round(sec, 3),
+               "sample": f"median of {n} whole ResNet-50 K=16 bf16 steps, float64, 1 thread"}
+        log(f"cpu baseline: {sec:.2f} s/step")
+
+    out = {
+        "metric": "AGS step+stats GB/s & % HBM peak (ResNet-50 layout, K=16); steps/s",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "steps_per_s": round(1e3 / ms_step, 1),
+        "hbm_peak_frac": round(value / HBM_PEAK_GBPS, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": WORKLOAD, "layout": "resnet50", "tensors": lay.n_layers,
+                   "params": N, "K": K, "grad_dtype": "bf16", "param_dtype": "f32",
+                   "mode": "ags", "algorithmic_bytes_per_step": ab["step"],
+                   "parallelism": "single GPU (K replicas stand in for K data-parallel workers)"},
+        "kernel_us": {n: round(v * 1e3, 2) for n, v in avg_ms.items()},
+        "device_copy_GBps": round(copy_bw, 1),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "last_step": {"delta": s.glob["delta"], "sensitive": s.glob["sensitive"],
+                      "step": s.glob["step"]},
+    }
+    h.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

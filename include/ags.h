@@ -1,0 +1,195 @@
+/*
+ * libags: the Adaptive Gradient Scaling (AGS) optimizer step with its
+ * gradient statistics, for one data-parallel training step on one MI355X
+ * (gfx950) GPU.
+ *
+ * Source of the method: Tula (arXiv 2603.18112), Sec. IV-B "Statistical
+ * Performance Model", Eq. (5)-(8) and Algorithm 1 "Adaptive Gradient
+ * Scaling"; synchronous data-parallel averaging of Eq. (1c); the wrapped
+ * momentum SGD with weight decay of Sec. V-A/V-B; the LARS baseline of
+ * Sec. V-D.
+ *
+ * One step, for a model whose parameter tensors ("layers") are laid end to
+ * end in one flat fp32 buffer w with momentum m of the same layout, given K
+ * replica gradients g_0..g_{K-1} (the K data-parallel workers' local
+ * gradients of the step, each laid out like w):
+ *
+ *   gbar        = (1/K) sum_k g_k                        large-batch gradient
+ *   W_l, G_l    = ||w_l||^2, ||gbar_l||^2                per layer
+ *   V_l         = (1/K) sum_k ||g_k,l - gbar_l||^2       cross-replica spread
+ *   S_l         = ||g_r,l||^2                            small-batch gradient
+ *   G           = sum_l G_l
+ *   Delta       = |G - G_prev| / G_prev                  gradient variability
+ *   sensitive   = !(Delta < delta)                       (inf on the 1st step)
+ *   d           = a_l gbar + b_l w                       a_l, b_l per mode
+ *   m <- mu m + d ;  w <- w - eta m                      momentum SGD
+ *   gradscale_l <- min(sqrt(S_l) / (sqrt(G_l) + eps), s_max)   (refresh)
+ *
+ * Modes: AGS   a_l = gradscale_l if the layer is scaled and the step is not
+ *              sensitive, else 1; b_l = lambda_l.
+ *        LARS  a_l = tau ||w_l|| / (||gbar_l|| + lambda_l ||w_l||) on scaled
+ *              layers (1 if either norm is 0); b_l = a_l lambda_l.
+ *        SGD   a_l = 1; b_l = lambda_l.
+ * lambda_l is weight_decay on layers with AGS_LAYER_DECAY, else 0.
+ *
+ * Conventions for every function:
+ *  - C linkage; every function returns an ags_status (0 = AGS_OK) except
+ *    where noted; nothing throws across the ABI.
+ *  - Pointers named d_* are device memory on the handle's device.  Host
+ *    arrays are read or written before the call returns.
+ *  - Argument, layout and alignment checks run on the host before any HIP
+ *    call; on error nothing is changed.  Device pointers are then checked
+ *    to be device allocations large enough for the access (AGS_E_ARG if
+ *    not), so that a bad pointer is an error, not a GPU fault.
+ *  - Work is enqueued on hip_stream (a hipStream_t; NULL is the default
+ *    stream) and the call returns without waiting, except ags_read_stats,
+ *    ags_get_state, ags_set_state and ags_get_kernel_times, which wait for
+ *    the handle's last stream.
+ *  - A handle is not thread-safe: one thread at a time.
+ */
+#ifndef AGS_H
+#define AGS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    AGS_OK = 0,
+    AGS_E_ARG = 1,     /* bad argument (null, out of range, not device memory) */
+    AGS_E_LAYOUT = 2,  /* layer table empty, overlapping, unordered, out of n_flat */
+    AGS_E_ALIGN = 3,   /* offset / stride / pointer misaligned                */
+    AGS_E_NOMEM = 4,   /* workspace allocation failed or over the cap          */
+    AGS_E_DEVICE = 5,  /* a HIP call failed; see ags_last_error               */
+    AGS_E_STATE = 6    /* handle state mismatch (e.g. wrong state length)      */
+} ags_status;
+
+typedef enum { AGS_F32 = 0, AGS_BF16 = 1 } ags_dtype;
+
+typedef enum { AGS_MODE_SGD = 0, AGS_MODE_AGS = 1, AGS_MODE_LARS = 2 } ags_mode;
+
+#define AGS_LAYER_SCALE 1u /* the layer takes part in AGS / LARS scaling  */
+#define AGS_LAYER_DECAY 2u /* the layer receives weight decay             */
+
+/* Layer offsets and the replica stride are multiples of this many elements,
+ * and d_w, d_m, d_grads are 16-byte aligned, so that every 8-element group
+ * is one aligned 16-byte (bf16) or two 16-byte (fp32) loads. */
+#define AGS_ALIGN_ELEMS 8
+#define AGS_MAX_K 1024
+
+/* One parameter tensor: elements [offset, offset + numel) of the flat
+ * buffers.  numel > 0; layers are in increasing offset order and do not
+ * overlap; offset + numel <= n_flat.  Elements outside every layer are
+ * never read or written. */
+typedef struct {
+    int64_t offset;
+    int64_t numel;
+    uint32_t flags;    /* AGS_LAYER_SCALE | AGS_LAYER_DECAY */
+    uint32_t reserved; /* must be 0 */
+} ags_layer;
+
+typedef struct {
+    int32_t n_layers;
+    const ags_layer *layers; /* host array [n_layers], copied at init       */
+    int64_t n_flat;          /* elements in d_w and d_m                     */
+    int32_t K;               /* replicas, 1..AGS_MAX_K                      */
+    ags_dtype grad_dtype;    /* dtype of the replica gradients              */
+    ags_mode mode;
+    double lr;               /* eta >= 0                                    */
+    double momentum;         /* mu in [0, 1)                                */
+    double weight_decay;     /* lambda >= 0                                 */
+    double delta;            /* sensitivity threshold; the paper uses 0.5   */
+    double eps;              /* stability term >= 0; the paper uses 1e-8    */
+    double s_max;            /* scale clip; <= 0 means sqrt(K)             */
+    double trust_coef;       /* LARS tau > 0 (used in AGS_MODE_LARS)        */
+    int32_t refresh_every;   /* refresh gradscale every n steps; 0 = never  */
+    int32_t small_replica;   /* replica r taken as the small-batch gradient;
+                                -1 = mean over replicas of ||g_k||^2        */
+} ags_config;
+
+/* Per-layer record of the last ags_stats / ags_step.  var is V_l (the 1/K
+ * normalised spread), noise_ratio = V_l / G_l (0 if both are 0, +inf if
+ * only G_l is 0), coef_a / coef_b the update coefficients used (or that
+ * would be used, for ags_stats), gradscale the state after the call. */
+typedef struct {
+    double w_sq, g_sq, var, gsmall_sq, noise_ratio, coef_a, coef_b, gradscale;
+} ags_layer_stats;
+
+/* Global record.  step: steps completed after the call; g_sq_prev: the
+ * previous norm the call compared against (0 on a first step); delta:
+ * +inf on a first step, when g_sq_prev <= 0 or when a norm is not finite;
+ * sensitive = !(delta < cfg.delta); nonfinite: a statistic was inf/nan. */
+typedef struct {
+    int64_t step;
+    double g_sq, g_sq_prev, delta;
+    int32_t sensitive, nonfinite;
+} ags_global_stats;
+
+typedef struct ags_handle ags_handle;
+
+/* Kernels of one step, in launch order, for ags_get_kernel_times. */
+#define AGS_N_KERNELS 3 /* 0: replica mean + tile statistics, 1: finalize, 2: update */
+
+/* Bytes of device workspace ags_init would allocate for cfg (host only). */
+ags_status ags_workspace_bytes(const ags_config *cfg, size_t *out_bytes);
+
+/* Create a handle bound to d_w, d_m (fp32 [n_flat], caller-owned, must
+ * outlive the handle) on the current HIP device.  The handle allocates its
+ * workspace (AGS_E_NOMEM on failure or when it exceeds the byte cap given
+ * by the environment variable AGS_MAX_WORKSPACE_BYTES; nothing is leaked).
+ * gradscale starts at 1 (Algorithm 1), the step count at 0. */
+ags_status ags_init(const ags_config *cfg, float *d_w, float *d_m, void *hip_stream,
+                    ags_handle **out);
+
+/* Statistics only: replica mean, per-layer and global statistics and the
+ * coefficients a step would use now.  w, m and the AGS state are not
+ * changed.  d_grads: [K][replica_stride] elements of grad_dtype, caller-
+ * owned; replica k starts at element k * replica_stride and uses the
+ * layout of w; replica_stride >= n_flat, a multiple of AGS_ALIGN_ELEMS. */
+ags_status ags_stats(ags_handle *h, const void *d_grads, int64_t replica_stride,
+                     void *hip_stream);
+
+/* One AGS step (Algorithm 1 iteration + UpdateGradScale when due): the
+ * statistics above, the sensitive decision, the update of w and m in
+ * place, then G_prev <- G, step += 1 and the gradscale refresh. */
+ags_status ags_step(ags_handle *h, const void *d_grads, int64_t replica_stride,
+                    void *hip_stream);
+
+/* Copy the records of the last ags_stats / ags_step to host arrays
+ * (out_layers [n_layers] may be NULL, out_global may be NULL). */
+ags_status ags_read_stats(ags_handle *h, ags_layer_stats *out_layers,
+                          ags_global_stats *out_global);
+
+/* Learning rate for the steps launched after this call (host schedules). */
+ags_status ags_set_lr(ags_handle *h, double lr);
+
+/* Checkpoint / resume of the AGS state (w and m are the caller's).
+ * gradscale_L: host [n_layers]. */
+ags_status ags_get_state(ags_handle *h, double *gradscale_L, double *g_sq_prev,
+                         int64_t *step);
+ags_status ags_set_state(ags_handle *h, const double *gradscale_L, double g_sq_prev,
+                         int64_t step);
+
+/* Per-kernel timing with HIP events on the launch stream: enable, then
+ * read the summed milliseconds per kernel (out_ms [AGS_N_KERNELS]) and the
+ * number of steps measured since the last read; reading resets. */
+ags_status ags_set_profiling(ags_handle *h, int enable);
+ags_status ags_get_kernel_times(ags_handle *h, double *out_ms, int64_t *out_calls);
+
+/* Static text for a status; last error text of a handle (or, with NULL, of
+ * the last failed ags_init / ags_workspace_bytes on this thread). */
+const char *ags_status_string(ags_status s);
+const char *ags_last_error(const ags_handle *h);
+
+/* Free the handle and its workspace (waits for its last stream).  NULL is
+ * a no-op. */
+void ags_destroy(ags_handle *h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AGS_H */

@@ -1,0 +1,640 @@
+// Host runtime of libags: argument validation, the tile map, the device
+// workspace, kernel launches, statistics read-back, checkpoint state and
+// per-kernel timing.  Everything the C-ABI (include/ags.h) promises about
+// errors is enforced here: host-side checks first, then device-pointer
+// checks, then work.
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "ags_internal.h"
+
+using ags::DevState;
+using ags::LayerDev;
+using ags::Partial;
+using ags::Tile;
+
+namespace {
+
+thread_local std::string g_thread_error;
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Byte offsets of the pieces of the device workspace.  The statistics
+// records, the gradscale array and the state are contiguous at the end so
+// that a read-back is one copy.
+struct WsLayout {
+    size_t gbar = 0, tiles = 0, partials = 0, ldev = 0, coef = 0;
+    size_t lstats = 0, gstats = 0, gradscale = 0, state = 0, end = 0;
+    size_t rec_bytes = 0;    // lstats .. gstats end
+    size_t state_bytes = 0;  // gradscale .. state end
+};
+
+size_t elem_bytes(ags_dtype dt) { return dt == AGS_BF16 ? 2 : 4; }
+
+bool materialize_gbar(const ags_config& c) {
+    // Keep the replica mean when re-reading the replicas in the update
+    // would cost more than writing and reading one fp32 per element.
+    return (size_t)c.K * elem_bytes(c.grad_dtype) > 8;
+}
+
+WsLayout ws_layout(const ags_config& c, int64_t n_tiles) {
+    WsLayout w;
+    size_t p = 0;
+    const size_t L = (size_t)c.n_layers;
+    w.gbar = p;
+    if (materialize_gbar(c)) p = align_up(p + (size_t)c.n_flat * sizeof(float));
+    w.tiles = p;
+    p = align_up(p + (size_t)n_tiles * sizeof(Tile));
+    w.partials = p;
+    p = align_up(p + (size_t)n_tiles * sizeof(Partial));
+    w.ldev = p;
+    p = align_up(p + L * sizeof(LayerDev));
+    w.coef = p;
+    p = align_up(p + L * sizeof(float2));
+    w.lstats = p;
+    p += L * sizeof(ags_layer_stats);
+    w.gstats = p;
+    p += sizeof(ags_global_stats);
+    w.rec_bytes = p - w.lstats;
+    p = (p + 7) / 8 * 8;
+    w.gradscale = p;
+    p += L * sizeof(double);
+    w.state = p;
+    p += sizeof(DevState);
+    w.state_bytes = p - w.gradscale;
+    w.end = align_up(p);
+    return w;
+}
+
+bool finite(double x) { return std::isfinite(x); }
+
+// Host-only validation of a configuration.  Fills why on failure.
+ags_status check_config(const ags_config* c, std::string& why) {
+    if (!c) { why = "cfg is NULL"; return AGS_E_ARG; }
+    if (c->n_layers < 1) { why = "n_layers must be >= 1"; return AGS_E_LAYOUT; }
+    if (!c->layers) { why = "layers is NULL"; return AGS_E_ARG; }
+    if (c->n_flat < 1) { why = "n_flat must be >= 1"; return AGS_E_LAYOUT; }
+    if (c->K < 1 || c->K > AGS_MAX_K) { why = "K out of range 1..AGS_MAX_K"; return AGS_E_ARG; }
+    if (c->grad_dtype != AGS_F32 && c->grad_dtype != AGS_BF16) { why = "bad grad_dtype"; return AGS_E_ARG; }
+    if (c->mode != AGS_MODE_SGD && c->mode != AGS_MODE_AGS && c->mode != AGS_MODE_LARS) {
+        why = "bad mode";
+        return AGS_E_ARG;
+    }
+    if (!finite(c->lr) || c->lr < 0) { why = "lr must be finite and >= 0"; return AGS_E_ARG; }
+    if (!finite(c->momentum) || c->momentum < 0 || c->momentum >= 1) {
+        why = "momentum must be in [0, 1)";
+        return AGS_E_ARG;
+    }
+    if (!finite(c->weight_decay) || c->weight_decay < 0) { why = "weight_decay must be >= 0"; return AGS_E_ARG; }
+    if (!finite(c->delta) || c->delta < 0) { why = "delta must be finite and >= 0"; return AGS_E_ARG; }
+    if (!finite(c->eps) || c->eps < 0) { why = "eps must be finite and >= 0"; return AGS_E_ARG; }
+    if (!finite(c->s_max)) { why = "s_max must be finite"; return AGS_E_ARG; }
+    if (c->mode == AGS_MODE_LARS && !(finite(c->trust_coef) && c->trust_coef > 0)) {
+        why = "trust_coef must be > 0 in LARS mode";
+        return AGS_E_ARG;
+    }
+    if (c->refresh_every < 0) { why = "refresh_every must be >= 0"; return AGS_E_ARG; }
+    if (c->small_replica < -1 || c->small_replica >= c->K) {
+        why = "small_replica must be -1 or in 0..K-1";
+        return AGS_E_ARG;
+    }
+    int64_t prev_end = 0;
+    for (int32_t l = 0; l < c->n_layers; ++l) {
+        const ags_layer& L = c->layers[l];
+        char buf[160];
+        if (L.numel < 1 || L.offset < 0) {
+            snprintf(buf, sizeof buf, "layer %d: numel must be > 0 and offset >= 0", l);
+            why = buf;
+            return AGS_E_LAYOUT;
+        }
+        if (L.offset % AGS_ALIGN_ELEMS != 0) {
+            snprintf(buf, sizeof buf, "layer %d: offset %lld is not a multiple of %d", l,
+                     (long long)L.offset, AGS_ALIGN_ELEMS);
+            why = buf;
+            return AGS_E_ALIGN;
+        }
+        if (L.offset < prev_end) {
+            snprintf(buf, sizeof buf, "layer %d overlaps or precedes the previous layer", l);
+            why = buf;
+            return AGS_E_LAYOUT;
+        }
+        if (L.numel > c->n_flat || L.offset > c->n_flat - L.numel) {
+            snprintf(buf, sizeof buf, "layer %d ends past n_flat", l);
+            why = buf;
+            return AGS_E_LAYOUT;
+        }
+        if ((L.flags & ~(AGS_LAYER_SCALE | AGS_LAYER_DECAY)) != 0 || L.reserved != 0) {
+            snprintf(buf, sizeof buf, "layer %d: unknown flags or nonzero reserved field", l);
+            why = buf;
+            return AGS_E_ARG;
+        }
+        prev_end = L.offset + L.numel;
+    }
+    return AGS_OK;
+}
+
+int64_t count_tiles(const ags_config& c) {
+    int64_t n = 0;
+    for (int32_t l = 0; l < c.n_layers; ++l) n += (c.layers[l].numel + ags::kTileElems - 1) / ags::kTileElems;
+    return n;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Is [p, p + bytes) inside one device allocation of the current device?
+ags_status check_device_range(const void* p, size_t bytes, const char* name, std::string& why) {
+    hipPointerAttribute_t attr;
+    std::memset(&attr, 0, sizeof attr);
+    hipError_t e = hipPointerGetAttributes(&attr, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        why = std::string(name) + " is not a HIP allocation";
+        return AGS_E_ARG;
+    }
+    if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged) {
+        why = std::string(name) + " is not device memory";
+        return AGS_E_ARG;
+    }
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || attr.device != dev) {
+        (void)hipGetLastError();
+        why = std::string(name) + " belongs to another device than the current one";
+        return AGS_E_ARG;
+    }
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    e = hipMemGetAddressRange(&base, &size, const_cast<void*>(p));
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        why = std::string(name) + ": allocation range unknown";
+        return AGS_E_ARG;
+    }
+    const uintptr_t b = reinterpret_cast<uintptr_t>(base), q = reinterpret_cast<uintptr_t>(p);
+    if (q < b || q - b > size || bytes > size - (q - b)) {
+        why = std::string(name) + " is smaller than the layout needs";
+        return AGS_E_ARG;
+    }
+    return AGS_OK;
+}
+
+size_t workspace_cap() {
+    const char* s = std::getenv("AGS_MAX_WORKSPACE_BYTES");
+    if (!s || !*s) return (size_t)-1;
+    char* end = nullptr;
+    const unsigned long long v = std::strtoull(s, &end, 10);
+    if (end == s) return (size_t)-1;
+    return (size_t)v;
+}
+
+}  // namespace
+
+struct ags_handle {
+    ags_config cfg{};
+    std::vector<ags_layer> layers;
+    float* d_w = nullptr;
+    float* d_m = nullptr;
+    int device = 0;
+    double lr = 0;
+    int64_t n_tiles = 0;
+    int64_t grad_extent = 0;  // elements of one replica that are read
+    bool materialize = false;
+    WsLayout wl;
+    char* ws = nullptr;
+    char* pinned = nullptr;
+    hipStream_t last_stream = nullptr;
+    bool has_stats = false;
+    std::string err;
+    bool profiling = false;
+    std::vector<std::array<hipEvent_t, 4>> ev_pending, ev_free;
+
+    Tile* tiles() const { return reinterpret_cast<Tile*>(ws + wl.tiles); }
+    Partial* partials() const { return reinterpret_cast<Partial*>(ws + wl.partials); }
+    LayerDev* ldev() const { return reinterpret_cast<LayerDev*>(ws + wl.ldev); }
+    float2* coef() const { return reinterpret_cast<float2*>(ws + wl.coef); }
+    float* gbar() const { return materialize ? reinterpret_cast<float*>(ws + wl.gbar) : nullptr; }
+    ags_layer_stats* lstats() const { return reinterpret_cast<ags_layer_stats*>(ws + wl.lstats); }
+    ags_global_stats* gstats() const { return reinterpret_cast<ags_global_stats*>(ws + wl.gstats); }
+    double* gradscale() const { return reinterpret_cast<double*>(ws + wl.gradscale); }
+    DevState* state() const { return reinterpret_cast<DevState*>(ws + wl.state); }
+
+    ags_status fail(ags_status s, const std::string& why) {
+        err = why;
+        return s;
+    }
+    ags_status hip_fail(hipError_t e, const char* what) {
+        err = std::string(what) + ": " + hipGetErrorString(e);
+        (void)hipGetLastError();
+        return AGS_E_DEVICE;
+    }
+};
+
+namespace {
+
+void free_handle(ags_handle* h) {
+    if (!h) return;
+    for (auto& q : h->ev_pending)
+        for (auto e : q) (void)hipEventDestroy(e);
+    for (auto& q : h->ev_free)
+        for (auto e : q) (void)hipEventDestroy(e);
+    if (h->ws) (void)hipFree(h->ws);
+    if (h->pinned) (void)hipHostFree(h->pinned);
+    delete h;
+}
+
+ags_status check_grads(ags_handle* h, const void* d_grads, int64_t stride) {
+    if (!h) return AGS_E_ARG;
+    if (!d_grads) return h->fail(AGS_E_ARG, "d_grads is NULL");
+    if (!aligned16(d_grads)) return h->fail(AGS_E_ALIGN, "d_grads must be 16-byte aligned");
+    if (stride < h->cfg.n_flat) return h->fail(AGS_E_ARG, "replica_stride must be >= n_flat");
+    if (stride % AGS_ALIGN_ELEMS != 0)
+        return h->fail(AGS_E_ALIGN, "replica_stride must be a multiple of AGS_ALIGN_ELEMS");
+    const double total = (double)(h->cfg.K - 1) * (double)stride + (double)h->grad_extent;
+    if (total * (double)elem_bytes(h->cfg.grad_dtype) > 9.0e18)
+        return h->fail(AGS_E_ARG, "replica_stride too large");
+    const size_t bytes = ((size_t)(h->cfg.K - 1) * (size_t)stride + (size_t)h->grad_extent) *
+                         elem_bytes(h->cfg.grad_dtype);
+    std::string why;
+    const ags_status s = check_device_range(d_grads, bytes, "d_grads", why);
+    if (s != AGS_OK) return h->fail(s, why);
+    return AGS_OK;
+}
+
+ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipStream_t s,
+                       bool commit) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess || cur != h->device) {
+        (void)hipGetLastError();
+        return h->fail(AGS_E_DEVICE, "the current HIP device is not the handle's device");
+    }
+    std::array<hipEvent_t, 4> ev{};
+    const bool prof = commit && h->profiling;
+    if (prof) {
+        if (!h->ev_free.empty()) {
+            ev = h->ev_free.back();
+            h->ev_free.pop_back();
+        } else {
+            for (int i = 0; i < 4; ++i) {
+                const hipError_t e = hipEventCreate(&ev[i]);
+                if (e != hipSuccess) {
+                    for (int j = 0; j < i; ++j) (void)hipEventDestroy(ev[j]);
+                    return h->hip_fail(e, "hipEventCreate");
+                }
+            }
+        }
+        (void)hipEventRecord(ev[0], s);
+    }
+    const ags_config& c = h->cfg;
+    const float invK = (float)(1.0 / (double)c.K);
+
+    ags::StatsArgs sa{};
+    sa.grads = d_grads;
+    sa.stride = stride;
+    sa.w = h->d_w;
+    sa.gbar = commit ? h->gbar() : nullptr;
+    sa.tiles = h->tiles();
+    sa.partials = h->partials();
+    sa.K = c.K;
+    sa.invK = invK;
+    sa.small_replica = c.small_replica;
+    hipError_t e = ags::launch_stats(sa, c.grad_dtype, (int)h->n_tiles, s);
+    if (e != hipSuccess) return h->hip_fail(e, "statistics kernel launch");
+    if (prof) (void)hipEventRecord(ev[1], s);
+
+    ags::FinalizeArgs fa{};
+    fa.partials = h->partials();
+    fa.layers = h->ldev();
+    fa.n_layers = c.n_layers;
+    fa.K = c.K;
+    fa.mode = c.mode;
+    fa.small_replica = c.small_replica;
+    fa.refresh_every = c.refresh_every;
+    fa.commit = commit ? 1 : 0;
+    fa.delta = c.delta;
+    fa.eps = c.eps;
+    fa.s_max = c.s_max;
+    fa.trust_coef = c.trust_coef;
+    fa.weight_decay = c.weight_decay;
+    fa.gradscale = h->gradscale();
+    fa.state = h->state();
+    fa.coef = h->coef();
+    fa.lstats = h->lstats();
+    fa.gstats = h->gstats();
+    e = ags::launch_finalize(fa, s);
+    if (e != hipSuccess) return h->hip_fail(e, "finalize kernel launch");
+    if (prof) (void)hipEventRecord(ev[2], s);
+
+    if (commit) {
+        ags::UpdateArgs ua{};
+        ua.tiles = h->tiles();
+        ua.gbar = h->gbar();
+        ua.grads = d_grads;
+        ua.stride = stride;
+        ua.K = c.K;
+        ua.invK = invK;
+        ua.w = h->d_w;
+        ua.m = h->d_m;
+        ua.coef = h->coef();
+        ua.lr = (float)h->lr;
+        ua.momentum = (float)c.momentum;
+        e = ags::launch_update(ua, c.grad_dtype, (int)h->n_tiles, s);
+        if (e != hipSuccess) return h->hip_fail(e, "update kernel launch");
+        if (prof) {
+            (void)hipEventRecord(ev[3], s);
+            h->ev_pending.push_back(ev);
+        }
+    }
+    h->last_stream = s;
+    h->has_stats = true;
+    return AGS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ags_status_string(ags_status s) {
+    switch (s) {
+        case AGS_OK: return "AGS_OK";
+        case AGS_E_ARG: return "AGS_E_ARG: bad argument";
+        case AGS_E_LAYOUT: return "AGS_E_LAYOUT: bad layer table";
+        case AGS_E_ALIGN: return "AGS_E_ALIGN: misaligned offset, stride or pointer";
+        case AGS_E_NOMEM: return "AGS_E_NOMEM: workspace allocation failed";
+        case AGS_E_DEVICE: return "AGS_E_DEVICE: HIP error";
+        case AGS_E_STATE: return "AGS_E_STATE: handle state mismatch";
+    }
+    return "unknown ags_status";
+}
+
+const char* ags_last_error(const ags_handle* h) {
+    return h ? h->err.c_str() : g_thread_error.c_str();
+}
+
+ags_status ags_workspace_bytes(const ags_config* cfg, size_t* out_bytes) {
+    std::string why;
+    ags_status s = check_config(cfg, why);
+    if (s != AGS_OK) {
+        g_thread_error = why;
+        return s;
+    }
+    if (!out_bytes) {
+        g_thread_error = "out_bytes is NULL";
+        return AGS_E_ARG;
+    }
+    *out_bytes = ws_layout(*cfg, count_tiles(*cfg)).end;
+    return AGS_OK;
+}
+
+ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_stream,
+                    ags_handle** out) {
+    std::string why;
+    if (!out) {
+        g_thread_error = "out is NULL";
+        return AGS_E_ARG;
+    }
+    *out = nullptr;
+    ags_status st = check_config(cfg, why);
+    if (st != AGS_OK) {
+        g_thread_error = why;
+        return st;
+    }
+    if (!d_w || !d_m) {
+        g_thread_error = "d_w and d_m must not be NULL";
+        return AGS_E_ARG;
+    }
+    if (!aligned16(d_w) || !aligned16(d_m)) {
+        g_thread_error = "d_w and d_m must be 16-byte aligned";
+        return AGS_E_ALIGN;
+    }
+    const int64_t n_tiles = count_tiles(*cfg);
+    if (n_tiles > 0x7fffffff) {
+        g_thread_error = "too many tiles";
+        return AGS_E_ARG;
+    }
+
+    // Host-side tables.
+    std::vector<Tile> tiles;
+    std::vector<LayerDev> ldev(cfg->n_layers);
+    tiles.reserve((size_t)n_tiles);
+    for (int32_t l = 0; l < cfg->n_layers; ++l) {
+        const ags_layer& L = cfg->layers[l];
+        ldev[l].tile_begin = (int32_t)tiles.size();
+        for (int64_t o = 0; o < L.numel; o += ags::kTileElems) {
+            Tile t;
+            t.begin = L.offset + o;
+            t.count = (int32_t)((L.numel - o) < ags::kTileElems ? (L.numel - o) : ags::kTileElems);
+            t.layer = l;
+            tiles.push_back(t);
+        }
+        ldev[l].tile_end = (int32_t)tiles.size();
+        ldev[l].flags = L.flags;
+        ldev[l].pad_ = 0;
+    }
+    int64_t extent = 0;
+    for (int32_t l = 0; l < cfg->n_layers; ++l)
+        extent = std::max<int64_t>(extent, cfg->layers[l].offset + cfg->layers[l].numel);
+
+    // Workspace size and the byte cap, still before any HIP call.
+    const WsLayout wl = ws_layout(*cfg, n_tiles);
+    const size_t cap = workspace_cap();
+    if (wl.end > cap) {
+        char buf[200];
+        snprintf(buf, sizeof buf, "workspace of %zu bytes exceeds AGS_MAX_WORKSPACE_BYTES=%zu",
+                 wl.end, cap);
+        g_thread_error = buf;
+        return AGS_E_NOMEM;
+    }
+
+    // Device checks (first HIP calls).
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        g_thread_error = std::string("hipGetDevice: ") + hipGetErrorString(e);
+        (void)hipGetLastError();
+        return AGS_E_DEVICE;
+    }
+    st = check_device_range(d_w, (size_t)extent * sizeof(float), "d_w", why);
+    if (st == AGS_OK) st = check_device_range(d_m, (size_t)extent * sizeof(float), "d_m", why);
+    if (st != AGS_OK) {
+        g_thread_error = why;
+        return st;
+    }
+
+    ags_handle* h = new (std::nothrow) ags_handle();
+    if (!h) {
+        g_thread_error = "host allocation failed";
+        return AGS_E_NOMEM;
+    }
+    h->cfg = *cfg;
+    h->layers.assign(cfg->layers, cfg->layers + cfg->n_layers);
+    h->cfg.layers = h->layers.data();
+    h->d_w = d_w;
+    h->d_m = d_m;
+    h->device = dev;
+    h->lr = cfg->lr;
+    h->n_tiles = n_tiles;
+    h->grad_extent = extent;
+    h->materialize = materialize_gbar(*cfg);
+    h->wl = wl;
+    e = hipMalloc(reinterpret_cast<void**>(&h->ws), h->wl.end);
+    if (e != hipSuccess) {
+        h->ws = nullptr;
+        (void)hipGetLastError();
+        g_thread_error = std::string("hipMalloc of the workspace failed: ") + hipGetErrorString(e);
+        free_handle(h);
+        return AGS_E_NOMEM;
+    }
+    const size_t pinned_bytes = h->wl.rec_bytes + h->wl.state_bytes + 64;
+    e = hipHostMalloc(reinterpret_cast<void**>(&h->pinned), pinned_bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        h->pinned = nullptr;
+        (void)hipGetLastError();
+        g_thread_error = std::string("hipHostMalloc of the staging buffer failed: ") + hipGetErrorString(e);
+        free_handle(h);
+        return AGS_E_NOMEM;
+    }
+
+    // Initial device state: tables, gradscale = 1, G_prev = 0, step = 0.
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    std::vector<double> ones(cfg->n_layers, 1.0);
+    DevState ds{0.0, 0};
+    const struct {
+        size_t off;
+        const void* src;
+        size_t bytes;
+    } up[] = {
+        {h->wl.tiles, tiles.data(), tiles.size() * sizeof(Tile)},
+        {h->wl.ldev, ldev.data(), ldev.size() * sizeof(LayerDev)},
+        {h->wl.gradscale, ones.data(), ones.size() * sizeof(double)},
+        {h->wl.state, &ds, sizeof ds},
+    };
+    e = hipMemsetAsync(h->ws + h->wl.lstats, 0, h->wl.rec_bytes, s);
+    for (const auto& u : up) {
+        if (e != hipSuccess) break;
+        e = hipMemcpyAsync(h->ws + u.off, u.src, u.bytes, hipMemcpyHostToDevice, s);
+    }
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        g_thread_error = std::string("initial upload: ") + hipGetErrorString(e);
+        (void)hipGetLastError();
+        free_handle(h);
+        return AGS_E_DEVICE;
+    }
+    h->last_stream = s;
+    *out = h;
+    return AGS_OK;
+}
+
+ags_status ags_stats(ags_handle* h, const void* d_grads, int64_t replica_stride, void* hip_stream) {
+    ags_status s = check_grads(h, d_grads, replica_stride);
+    if (s != AGS_OK) return s;
+    return launch_step(h, d_grads, replica_stride, static_cast<hipStream_t>(hip_stream), false);
+}
+
+ags_status ags_step(ags_handle* h, const void* d_grads, int64_t replica_stride, void* hip_stream) {
+    ags_status s = check_grads(h, d_grads, replica_stride);
+    if (s != AGS_OK) return s;
+    return launch_step(h, d_grads, replica_stride, static_cast<hipStream_t>(hip_stream), true);
+}
+
+ags_status ags_read_stats(ags_handle* h, ags_layer_stats* out_layers, ags_global_stats* out_global) {
+    if (!h) return AGS_E_ARG;
+    if (!h->has_stats) return h->fail(AGS_E_STATE, "no ags_stats / ags_step has run yet");
+    hipError_t e = hipMemcpyAsync(h->pinned, h->ws + h->wl.lstats, h->wl.rec_bytes,
+                                  hipMemcpyDeviceToHost, h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "reading statistics");
+    if (out_layers)
+        std::memcpy(out_layers, h->pinned, (size_t)h->cfg.n_layers * sizeof(ags_layer_stats));
+    if (out_global)
+        std::memcpy(out_global, h->pinned + (h->wl.gstats - h->wl.lstats), sizeof(ags_global_stats));
+    return AGS_OK;
+}
+
+ags_status ags_set_lr(ags_handle* h, double lr) {
+    if (!h) return AGS_E_ARG;
+    if (!std::isfinite(lr) || lr < 0) return h->fail(AGS_E_ARG, "lr must be finite and >= 0");
+    h->lr = lr;
+    return AGS_OK;
+}
+
+ags_status ags_get_state(ags_handle* h, double* gradscale_L, double* g_sq_prev, int64_t* step) {
+    if (!h) return AGS_E_ARG;
+    if (!gradscale_L || !g_sq_prev || !step) return h->fail(AGS_E_ARG, "NULL output pointer");
+    hipError_t e = hipMemcpyAsync(h->pinned, h->ws + h->wl.gradscale, h->wl.state_bytes,
+                                  hipMemcpyDeviceToHost, h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "reading state");
+    const size_t L = (size_t)h->cfg.n_layers;
+    std::memcpy(gradscale_L, h->pinned, L * sizeof(double));
+    DevState ds;
+    std::memcpy(&ds, h->pinned + (h->wl.state - h->wl.gradscale), sizeof ds);
+    *g_sq_prev = ds.g_prev;
+    *step = ds.step;
+    return AGS_OK;
+}
+
+ags_status ags_set_state(ags_handle* h, const double* gradscale_L, double g_sq_prev, int64_t step) {
+    if (!h) return AGS_E_ARG;
+    if (!gradscale_L) return h->fail(AGS_E_ARG, "gradscale_L is NULL");
+    if (!std::isfinite(g_sq_prev) || g_sq_prev < 0) return h->fail(AGS_E_ARG, "g_sq_prev must be finite and >= 0");
+    if (step < 0) return h->fail(AGS_E_ARG, "step must be >= 0");
+    const size_t L = (size_t)h->cfg.n_layers;
+    for (size_t l = 0; l < L; ++l)
+        if (!std::isfinite(gradscale_L[l]) || !(gradscale_L[l] > 0))
+            return h->fail(AGS_E_ARG, "gradscale values must be finite and > 0");
+    // Wait for queued steps first: the staging buffer and the state are
+    // shared with them.
+    hipError_t e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "waiting for the last stream");
+    std::memcpy(h->pinned, gradscale_L, L * sizeof(double));
+    DevState ds{g_sq_prev, step};
+    std::memcpy(h->pinned + (h->wl.state - h->wl.gradscale), &ds, sizeof ds);
+    e = hipMemcpyAsync(h->ws + h->wl.gradscale, h->pinned, h->wl.state_bytes,
+                       hipMemcpyHostToDevice, h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "writing state");
+    return AGS_OK;
+}
+
+ags_status ags_set_profiling(ags_handle* h, int enable) {
+    if (!h) return AGS_E_ARG;
+    h->profiling = enable != 0;
+    return AGS_OK;
+}
+
+ags_status ags_get_kernel_times(ags_handle* h, double* out_ms, int64_t* out_calls) {
+    if (!h) return AGS_E_ARG;
+    if (!out_ms || !out_calls) return h->fail(AGS_E_ARG, "NULL output pointer");
+    double tot[AGS_N_KERNELS] = {0, 0, 0};
+    for (auto& q : h->ev_pending) {
+        hipError_t e = hipEventSynchronize(q[3]);
+        if (e != hipSuccess) return h->hip_fail(e, "hipEventSynchronize");
+        for (int k = 0; k < AGS_N_KERNELS; ++k) {
+            float ms = 0;
+            e = hipEventElapsedTime(&ms, q[k], q[k + 1]);
+            if (e != hipSuccess) return h->hip_fail(e, "hipEventElapsedTime");
+            tot[k] += ms;
+        }
+    }
+    *out_calls = (int64_t)h->ev_pending.size();
+    for (int k = 0; k < AGS_N_KERNELS; ++k) out_ms[k] = tot[k];
+    for (auto& q : h->ev_pending) h->ev_free.push_back(q);
+    h->ev_pending.clear();
+    return AGS_OK;
+}
+
+void ags_destroy(ags_handle* h) {
+    if (!h) return;
+    (void)hipStreamSynchronize(h->last_stream);
+    free_handle(h);
+}
+
+}  // extern "C"

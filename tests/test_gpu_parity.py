@@ -1,0 +1,306 @@
+"""HIP path vs the float64 oracle on MI355X, through the C-ABI.
+
+Workloads: the five CNN-shaped configurations (tiny CNN K=4 fp32 3 steps;
+ResNet-18 CIFAR K=8 fp32 1 step; ResNet-50 K=16 bf16 10 steps; VGG-16 K=8
+fp32 5 steps; the ResNet-50 K sweep, bf16) plus ragged and degenerate
+layouts.  Every step compares all statistics and, after each step, every
+element of w and m.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from ags_parity import Pair, check_params, check_stats, log, run_steps, to_device
+from oracle import OracleAGS
+from paper_2603_18112_amd import ags, layouts, synth
+
+pytestmark = pytest.mark.gpu
+
+SD = layouts.LAYER_SCALE | layouts.LAYER_DECAY
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    ags.load_library()   # fails loudly if libags.so is not built
+    yield
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------ the configs --
+
+
+@pytest.mark.parametrize("mode", ["ags", "lars", "sgd"])
+def test_tiny_cnn_k4_three_steps(mode):
+    lay = layouts.get_layout("tiny_cnn")
+    run_steps(lay, 4, 3, mode=mode, label=f"tiny {mode}")
+
+
+def test_resnet18_cifar_k8_one_step():
+    lay = layouts.get_layout("resnet18_cifar")
+    run_steps(lay, 8, 1, label="r18")
+
+
+def test_resnet50_k16_bf16_ten_steps():
+    lay = layouts.get_layout("resnet50")
+    w = run_steps(lay, 16, 10, dtype="bf16", check_each=False, label="r50")
+    log(f"  r50 worst param error / tolerance scale: w {w[0]:.2e} m {w[1]:.2e}")
+
+
+def test_vgg16_k8_five_steps():
+    lay = layouts.get_layout("vgg16")
+    run_steps(lay, 8, 5, check_each=False, label="vgg16")
+
+
+@pytest.mark.parametrize("K", [1, 2, 4, 8, 32, 64])
+def test_resnet50_sweep_parity(K):
+    lay = layouts.get_layout("resnet50")
+    run_steps(lay, K, 2, dtype="bf16", check_each=False, label=f"r50 K={K}")
+
+
+def test_resnet50_sweep_noise_statistic_closed_form():
+    """Per-layer noise ratio rho_l = V_l / G_l against its expectation under
+    the generator, E[V]/E[G] = c^2 (K-1) / (K + c^2), for every K and c of the
+    sweep (a property that holds at any size)."""
+    import torch
+    lay = layouts.get_layout("resnet50")
+    sig = synth.layer_sigmas(lay, 0)
+    w = torch.from_numpy(synth.init_weights(lay, 0)).cuda()
+    m = torch.zeros_like(w)
+    big = lay.numels >= 100_000
+    for K in (1, 2, 4, 8, 16, 32, 64):
+        h = ags.AGS(lay.table(), w, m, K, grad_dtype="bf16")
+        for c in (0.1, 0.5, 2.0):
+            g = to_device(synth.replica_grads(lay, K, 0, 0, noise=c, dtype="bf16", sigmas=sig))
+            h.stats(g)
+            s = h.read_stats()
+            rho = s.layer["noise_ratio"]
+            expect = c * c * (K - 1) / (K + c * c)
+            if K == 1:
+                assert np.all(rho == 0.0)
+            else:
+                n = lay.numels[big].astype(np.float64)
+                tol = 8.0 / np.sqrt(n)
+                err = np.abs(rho[big] / expect - 1)
+                assert np.all(err < tol), (K, c, float(err.max()))
+            # 0 < s <= s_max = sqrt(K) for every layer (state after refresh is
+            # only formed by a step; the stats record holds the current one)
+            assert np.all(s.layer["gradscale"] == 1.0)
+            del g
+        h.close()
+        log(f"  sweep K={K} ok")
+
+
+# ------------------------------------------------ ragged and edge layouts --
+
+
+RAGGED = [1, 7, 8, 9, 63, 2047, 2048, 2049, 8191, 8192, 8193, 20003, 5, 64]
+
+
+@pytest.mark.parametrize("K,dtype,r", [(3, "f32", 0), (5, "bf16", 2), (16, "bf16", -1),
+                                       (2, "f32", 1), (6, "f32", -1), (1, "bf16", 0)])
+def test_ragged_layout(K, dtype, r):
+    flags = [SD, SD, 0, layouts.LAYER_SCALE, layouts.LAYER_DECAY] * 3
+    lay = layouts.custom_layout(RAGGED, flags[:len(RAGGED)], pad=8)
+    run_steps(lay, K, 4, dtype=dtype, small_replica=r, label=f"ragged K={K} {dtype} r={r}")
+
+
+def test_stride_larger_than_n_flat():
+    lay = layouts.custom_layout([100, 9000, 13], pad=8)
+    run_steps(lay, 4, 2, stride=lay.n_flat + 4096 + 8, label="stride")
+
+
+def test_single_element_layers_and_lars():
+    lay = layouts.custom_layout([1] * 40 + [10_000], pad=8)
+    run_steps(lay, 4, 3, mode="lars", label="1-elem lars")
+
+
+def test_identical_replicas_zero_variance_exactly():
+    lay = layouts.get_layout("tiny_cnn")
+    x = synth.replica_grads(lay, 1, 0, 0)
+    for K, dt in ((7, "f32"), (16, "bf16"), (64, "bf16")):
+        g = np.tile(x if dt == "f32" else synth.to_bf16_bits(x), (K, 1))
+        p = Pair(lay, K, dtype=dt)
+        s, _ = p.step(g)
+        assert np.all(s.layer["var"] == 0.0) and np.all(s.layer["noise_ratio"] == 0.0)
+        p.check_state("identical")
+        p.close()
+
+
+def test_k1_sgd_matches_oracle_and_plain_sgd():
+    # K = 1 with scaling off is plain momentum SGD (the oracle is pinned to
+    # torch.optim.SGD on the CPU for exactly this case).
+    lay = layouts.get_layout("tiny_cnn")
+    run_steps(lay, 1, 5, mode="sgd", label="K=1 sgd")
+    lay2 = layouts.make_layout("tiny", layouts.tiny_cnn_tensors(), "all")
+    t = [(o, n, layouts.LAYER_DECAY) for o, n, _ in lay2.table()]
+    lay2.flags[:] = [f for _, _, f in t]
+    run_steps(lay2, 1, 5, mode="ags", label="K=1 ags scale off")
+
+
+def test_forced_spike_takes_unscaled_branch():
+    lay = layouts.get_layout("resnet18_cifar")
+    g1 = synth.replica_grads(lay, 8, 0, 0)
+    p = Pair(lay, 8)
+    s, _ = p.step(g1, what="spike 1")
+    assert s.glob["sensitive"] == 1
+    s, _ = p.step(g1, what="spike 2")          # Delta = 0: scaled
+    assert s.glob["sensitive"] == 0 and s.glob["delta"] == 0.0
+    scaled = lay.flags & layouts.LAYER_SCALE != 0
+    assert np.any(s.layer["coef_a"][scaled] != 1.0)
+    s, _ = p.step((g1 * np.float32(2)).astype(np.float32), what="spike 3")  # Delta = 3
+    assert s.glob["sensitive"] == 1 and abs(s.glob["delta"] - 3.0) < 1e-6
+    assert np.all(s.layer["coef_a"] == 1.0)
+    p.check_state("spike")
+    p.close()
+
+
+def test_zero_and_nonfinite_gradients():
+    lay = layouts.custom_layout([300, 17], pad=8)
+    p = Pair(lay, 3, w0=np.ones(lay.n_flat, np.float32))
+    z = np.zeros((3, lay.n_flat), np.float32)
+    s, _ = p.step(z, what="zero 1")
+    assert np.all(s.layer["gradscale"] == 1.0)
+    s, _ = p.step(z, what="zero 2")
+    assert s.glob["sensitive"] == 1 and math.isinf(s.glob["delta"])
+    p.check_state("zero")
+    bad = np.ones((3, lay.n_flat), np.float32)
+    bad[1, 5] = np.inf
+    g = to_device(bad)
+    p.gpu.stats(g)
+    s = p.gpu.read_stats()
+    _, og = p.ora.stats(bad)
+    assert s.glob["nonfinite"] == 1 == og["nonfinite"] and s.glob["sensitive"] == 1
+    p.close()
+
+
+# ----------------------------------------------------- state and contract --
+
+
+def test_stats_call_does_not_mutate():
+    lay = layouts.get_layout("tiny_cnn")
+    p = Pair(lay, 4)
+    p.step(synth.replica_grads(lay, 4, 0, 0))
+    w, m = p.w.clone(), p.m.clone()
+    st = p.gpu.get_state()
+    p.step(synth.replica_grads(lay, 4, 1, 0), commit=False, what="stats only")
+    assert p.torch.equal(w, p.w) and p.torch.equal(m, p.m)
+    st2 = p.gpu.get_state()
+    assert np.array_equal(st[0], st2[0]) and st[1:] == st2[1:]
+    p.close()
+
+
+def test_bitwise_determinism():
+    lay = layouts.get_layout("resnet18_cifar")
+    grads = [to_device(synth.replica_grads(lay, 8, t, 1)) for t in range(3)]
+    outs = []
+    for _ in range(2):
+        p = Pair(lay, 8, seed=1)
+        for g in grads:
+            p.gpu.step(g)
+        s = p.gpu.read_stats()
+        outs.append((p.w.cpu().numpy(), p.m.cpu().numpy(), s.layer, p.gpu.get_state()))
+        p.close()
+    a, b = outs
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    for f in ags.LAYER_STATS_FIELDS:
+        assert np.array_equal(a[2][f], b[2][f]), f
+    assert np.array_equal(a[3][0], b[3][0]) and a[3][1:] == b[3][1:]
+
+
+def test_checkpoint_resume_bitwise():
+    import torch
+    lay = layouts.get_layout("resnet18_cifar")
+    grads = [to_device(synth.replica_grads(lay, 8, t, 2)) for t in range(10)]
+    a = Pair(lay, 8, seed=2)
+    for g in grads:
+        a.gpu.step(g)
+    b = Pair(lay, 8, seed=2)
+    for g in grads[:5]:
+        b.gpu.step(g)
+    state = b.gpu.get_state()
+    w2, m2 = b.w.clone(), b.m.clone()
+    b.close()
+    c = ags.AGS(lay.table(), w2, m2, 8, **{k: v for k, v in b.hyper.items()})
+    c.set_state(*state)
+    for g in grads[5:]:
+        c.step(g)
+    torch.cuda.synchronize()
+    assert torch.equal(a.w, w2) and torch.equal(a.m, m2)
+    sa, sc = a.gpu.get_state(), c.get_state()
+    assert np.array_equal(sa[0], sc[0]) and sa[1:] == sc[1:]
+    a.close()
+    c.close()
+
+
+def test_set_lr_and_profiling():
+    lay = layouts.get_layout("tiny_cnn")
+    p = Pair(lay, 4)
+    p.gpu.set_profiling(True)
+    for t, lr in enumerate([0.1, 0.05, 0.0]):
+        p.gpu.set_lr(lr)
+        g = synth.replica_grads(lay, 4, t, 0)
+        p.gpu.step(to_device(g))
+        p.ora.step(g, lr=lr)
+    p.check_state("set_lr")
+    ms, n = p.gpu.kernel_times()
+    assert n == 3 and np.all(ms > 0)
+    p.close()
+
+
+def _hip():
+    import ctypes
+    import torch  # noqa: F401  (its HIP runtime is the process's runtime)
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    hip.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
+    hip.hipFree.argtypes = [ctypes.c_void_p]
+    return hip
+
+
+def _hip_malloc(hip, nbytes):
+    import ctypes
+    p = ctypes.c_void_p()
+    assert hip.hipMalloc(ctypes.byref(p), nbytes) == 0
+    return p.value
+
+
+def test_bad_device_pointers_are_errors_not_faults():
+    """Pointers that are not device memory, or allocations smaller than the
+    layout needs, are rejected on the host (exact-size hipMalloc buffers:
+    the torch caching allocator hides the size of its blocks)."""
+    import torch
+    hip = _hip()
+    MB2 = 2 << 20
+    n_flat = MB2 // 4                      # one replica = 2 MiB of fp32
+    table = [(0, n_flat, SD)]
+    w = _hip_malloc(hip, MB2)
+    m = _hip_malloc(hip, MB2)
+    g2 = _hip_malloc(hip, 2 * MB2)         # room for 2 replicas, K = 4 needs 4
+    half = _hip_malloc(hip, MB2 // 2)
+    try:
+        cfg = ags.make_config(table, n_flat, 4)
+        h = ags.ags_init(cfg, w, m, 0)
+        for ptr, stride, status in [(g2, n_flat, ags.AGS_E_ARG),
+                                    (g2, n_flat - 8, ags.AGS_E_ARG),
+                                    (g2 + 4, n_flat, ags.AGS_E_ALIGN),
+                                    (np.zeros((4, n_flat), np.float32).ctypes.data, n_flat, ags.AGS_E_ARG)]:
+            with pytest.raises(ags.AGSError) as e:
+                ags.ags_step(h, ptr, stride)
+            assert e.value.status == status
+        with pytest.raises(ags.AGSError) as e:
+            ags.ags_read_stats(h, 1)       # nothing has run yet
+        assert e.value.status == ags.AGS_E_STATE
+        ags.ags_destroy(h)
+        with pytest.raises(ags.AGSError) as e:
+            ags.ags_init(cfg, half, m, 0)  # d_w smaller than n_flat floats
+        assert e.value.status == ags.AGS_E_ARG
+        host = np.zeros(n_flat, np.float32)
+        with pytest.raises(ags.AGSError) as e:
+            ags.ags_init(cfg, host.ctypes.data, m, 0)
+        assert e.value.status == ags.AGS_E_ARG
+    finally:
+        torch.cuda.synchronize()
+        for p in (w, m, g2, half):
+            hip.hipFree(p)
