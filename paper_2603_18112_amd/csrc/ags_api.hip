@@ -31,7 +31,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // records, the gradscale array and the state are contiguous at the end so
 // that a read-back is one copy.
 struct WsLayout {
-    size_t gbar = 0, tiles = 0, partials = 0, ldev = 0, coef = 0;
+    size_t gbar = 0, tiles = 0, partials = 0, ldev = 0, coef = 0, corr = 0, counters = 0;
+    size_t counters_bytes = 0;  // layer counters, done counter, correction flag
     size_t lstats = 0, gstats = 0, gradscale = 0, state = 0, end = 0;
     size_t rec_bytes = 0;    // lstats .. gstats end
     size_t state_bytes = 0;  // gradscale .. state end
@@ -40,9 +41,10 @@ struct WsLayout {
 size_t elem_bytes(ags_dtype dt) { return dt == AGS_BF16 ? 2 : 4; }
 
 bool materialize_gbar(const ags_config& c) {
-    // Keep the replica mean when re-reading the replicas in the update
-    // would cost more than writing and reading one fp32 per element.
-    return (size_t)c.K * elem_bytes(c.grad_dtype) > 8;
+    // Only a LARS step has a second pass over the replica mean.  Keep it when
+    // re-reading the replicas there would cost more than writing and reading
+    // one fp32 per element.
+    return c.mode == AGS_MODE_LARS && (size_t)c.K * elem_bytes(c.grad_dtype) > 8;
 }
 
 WsLayout ws_layout(const ags_config& c, int64_t n_tiles) {
@@ -59,6 +61,11 @@ WsLayout ws_layout(const ags_config& c, int64_t n_tiles) {
     p = align_up(p + L * sizeof(LayerDev));
     w.coef = p;
     p = align_up(p + L * sizeof(float2));
+    w.corr = p;
+    p = align_up(p + L * sizeof(float));
+    w.counters = p;
+    w.counters_bytes = (L + 2) * sizeof(unsigned);
+    p = align_up(p + w.counters_bytes);
     w.lstats = p;
     p += L * sizeof(ags_layer_stats);
     w.gstats = p;
@@ -213,12 +220,16 @@ struct ags_handle {
     bool has_stats = false;
     std::string err;
     bool profiling = false;
-    std::vector<std::array<hipEvent_t, 4>> ev_pending, ev_free;
+    std::vector<std::array<hipEvent_t, AGS_N_KERNELS + 1>> ev_pending, ev_free;
 
     Tile* tiles() const { return reinterpret_cast<Tile*>(ws + wl.tiles); }
     Partial* partials() const { return reinterpret_cast<Partial*>(ws + wl.partials); }
     LayerDev* ldev() const { return reinterpret_cast<LayerDev*>(ws + wl.ldev); }
     float2* coef() const { return reinterpret_cast<float2*>(ws + wl.coef); }
+    float* corr() const { return reinterpret_cast<float*>(ws + wl.corr); }
+    unsigned* layer_count() const { return reinterpret_cast<unsigned*>(ws + wl.counters); }
+    unsigned* done_count() const { return layer_count() + cfg.n_layers; }
+    int* corr_flag() const { return reinterpret_cast<int*>(layer_count() + cfg.n_layers + 1); }
     float* gbar() const { return materialize ? reinterpret_cast<float*>(ws + wl.gbar) : nullptr; }
     ags_layer_stats* lstats() const { return reinterpret_cast<ags_layer_stats*>(ws + wl.lstats); }
     ags_global_stats* gstats() const { return reinterpret_cast<ags_global_stats*>(ws + wl.gstats); }
@@ -274,14 +285,15 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         (void)hipGetLastError();
         return h->fail(AGS_E_DEVICE, "the current HIP device is not the handle's device");
     }
-    std::array<hipEvent_t, 4> ev{};
+    constexpr int NE = AGS_N_KERNELS + 1;
+    std::array<hipEvent_t, NE> ev{};
     const bool prof = commit && h->profiling;
     if (prof) {
         if (!h->ev_free.empty()) {
             ev = h->ev_free.back();
             h->ev_free.pop_back();
         } else {
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < NE; ++i) {
                 const hipError_t e = hipEventCreate(&ev[i]);
                 if (e != hipSuccess) {
                     for (int j = 0; j < i; ++j) (void)hipEventDestroy(ev[j]);
@@ -293,47 +305,50 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     }
     const ags_config& c = h->cfg;
     const float invK = (float)(1.0 / (double)c.K);
+    // AGS and SGD steps update w and m in the statistics pass with the
+    // predicted coefficients; a LARS step needs its layer norms first.
+    const bool fused = commit && c.mode != AGS_MODE_LARS;
 
-    ags::StatsArgs sa{};
+    ags::StepArgs sa{};
     sa.grads = d_grads;
     sa.stride = stride;
     sa.w = h->d_w;
-    sa.gbar = commit ? h->gbar() : nullptr;
+    sa.m = h->d_m;
+    sa.gbar = (commit && !fused) ? h->gbar() : nullptr;
     sa.tiles = h->tiles();
     sa.partials = h->partials();
+    sa.layers = h->ldev();
+    sa.n_layers = c.n_layers;
     sa.K = c.K;
     sa.invK = invK;
     sa.small_replica = c.small_replica;
-    hipError_t e = ags::launch_stats(sa, c.grad_dtype, (int)h->n_tiles, s);
-    if (e != hipSuccess) return h->hip_fail(e, "statistics kernel launch");
+    sa.mode = c.mode;
+    sa.commit = commit ? 1 : 0;
+    sa.refresh_every = c.refresh_every;
+    sa.lr = (float)h->lr;
+    sa.momentum = (float)c.momentum;
+    sa.delta = c.delta;
+    sa.eps = c.eps;
+    sa.s_max = c.s_max;
+    sa.trust_coef = c.trust_coef;
+    sa.weight_decay = c.weight_decay;
+    sa.gradscale = h->gradscale();
+    sa.state = h->state();
+    sa.coef = h->coef();
+    sa.corr = h->corr();
+    sa.corr_flag = h->corr_flag();
+    sa.layer_count = h->layer_count();
+    sa.done_count = h->done_count();
+    sa.lstats = h->lstats();
+    sa.gstats = h->gstats();
+    hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s);
+    if (e != hipSuccess) return h->hip_fail(e, "step kernel launch");
     if (prof) (void)hipEventRecord(ev[1], s);
 
-    ags::FinalizeArgs fa{};
-    fa.partials = h->partials();
-    fa.layers = h->ldev();
-    fa.n_layers = c.n_layers;
-    fa.K = c.K;
-    fa.mode = c.mode;
-    fa.small_replica = c.small_replica;
-    fa.refresh_every = c.refresh_every;
-    fa.commit = commit ? 1 : 0;
-    fa.delta = c.delta;
-    fa.eps = c.eps;
-    fa.s_max = c.s_max;
-    fa.trust_coef = c.trust_coef;
-    fa.weight_decay = c.weight_decay;
-    fa.gradscale = h->gradscale();
-    fa.state = h->state();
-    fa.coef = h->coef();
-    fa.lstats = h->lstats();
-    fa.gstats = h->gstats();
-    e = ags::launch_finalize(fa, s);
-    if (e != hipSuccess) return h->hip_fail(e, "finalize kernel launch");
-    if (prof) (void)hipEventRecord(ev[2], s);
-
-    if (commit) {
+    if (commit && c.mode != AGS_MODE_SGD) {
         ags::UpdateArgs ua{};
         ua.tiles = h->tiles();
+        ua.n_tiles = (int)h->n_tiles;
         ua.gbar = h->gbar();
         ua.grads = d_grads;
         ua.stride = stride;
@@ -342,14 +357,17 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         ua.w = h->d_w;
         ua.m = h->d_m;
         ua.coef = h->coef();
+        ua.corr = h->corr();
+        ua.corr_flag = h->corr_flag();
         ua.lr = (float)h->lr;
         ua.momentum = (float)c.momentum;
-        e = ags::launch_update(ua, c.grad_dtype, (int)h->n_tiles, s);
-        if (e != hipSuccess) return h->hip_fail(e, "update kernel launch");
-        if (prof) {
-            (void)hipEventRecord(ev[3], s);
-            h->ev_pending.push_back(ev);
-        }
+        e = (c.mode == AGS_MODE_LARS) ? ags::launch_update(ua, c.grad_dtype, s)
+                                      : ags::launch_correct(ua, c.grad_dtype, s);
+        if (e != hipSuccess) return h->hip_fail(e, "second-pass kernel launch");
+    }
+    if (prof) {
+        (void)hipEventRecord(ev[2], s);
+        h->ev_pending.push_back(ev);
     }
     h->last_stream = s;
     h->has_stats = true;
@@ -516,6 +534,7 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         {h->wl.state, &ds, sizeof ds},
     };
     e = hipMemsetAsync(h->ws + h->wl.lstats, 0, h->wl.rec_bytes, s);
+    if (e == hipSuccess) e = hipMemsetAsync(h->ws + h->wl.counters, 0, h->wl.counters_bytes, s);
     for (const auto& u : up) {
         if (e != hipSuccess) break;
         e = hipMemcpyAsync(h->ws + u.off, u.src, u.bytes, hipMemcpyHostToDevice, s);
@@ -613,9 +632,9 @@ ags_status ags_set_profiling(ags_handle* h, int enable) {
 ags_status ags_get_kernel_times(ags_handle* h, double* out_ms, int64_t* out_calls) {
     if (!h) return AGS_E_ARG;
     if (!out_ms || !out_calls) return h->fail(AGS_E_ARG, "NULL output pointer");
-    double tot[AGS_N_KERNELS] = {0, 0, 0};
+    double tot[AGS_N_KERNELS] = {0, 0};
     for (auto& q : h->ev_pending) {
-        hipError_t e = hipEventSynchronize(q[3]);
+        hipError_t e = hipEventSynchronize(q[AGS_N_KERNELS]);
         if (e != hipSuccess) return h->hip_fail(e, "hipEventSynchronize");
         for (int k = 0; k < AGS_N_KERNELS; ++k) {
             float ms = 0;

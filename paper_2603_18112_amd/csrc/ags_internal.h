@@ -15,8 +15,12 @@ namespace ags {
 // tile's partial sums belong to exactly one layer.
 constexpr int kBlock = 256;
 constexpr int kVec = 8;
-constexpr int kTileElems = 8192;  // 4 groups of 8 per thread
-constexpr int kFinalizeThreads = 1024;
+#ifndef AGS_TILE_ELEMS
+#define AGS_TILE_ELEMS 8192
+#endif
+constexpr int kTileElems = AGS_TILE_ELEMS;  // a multiple of kBlock * kVec
+static_assert(kTileElems % (kBlock * kVec) == 0, "tile must hold whole block rounds");
+constexpr int kCorrectBlocks = 2048;  // grid of the correction pass (grid-stride)
 
 struct Tile {
     int64_t begin;  // first element (flat index), a multiple of kVec
@@ -30,7 +34,7 @@ struct LayerDev {
     int32_t pad_;
 };
 
-// Device-resident AGS state, updated by the finalize kernel.
+// Device-resident AGS state, updated by the last block of a committed step.
 struct DevState {
     double g_prev;  // ||G||^2 of the last committed step (0 before the first)
     int64_t step;   // steps completed
@@ -43,37 +47,41 @@ struct Partial {
     float w, g, d, s;
 };
 
-struct StatsArgs {
+// Arguments of the fused step kernel (statistics of every tile, the
+// per-layer and global finalize in the last blocks, and -- when update is
+// on -- the momentum-SGD update with the predicted coefficients).
+struct StepArgs {
     const void* grads;
     int64_t stride;
-    const float* w;
-    float* gbar;          // nullptr: do not store the replica mean
+    float* w;
+    float* m;
+    float* gbar;             // store the replica mean here (or nullptr)
     const Tile* tiles;
     Partial* partials;
-    int K;
-    float invK;
-    int small_replica;    // -1, or 0..K-1
-};
-
-struct FinalizeArgs {
-    const Partial* partials;
     const LayerDev* layers;
     int n_layers;
     int K;
-    int mode;
-    int small_replica;
+    float invK;
+    int small_replica;       // -1, or 0..K-1
+    int mode;                // ags_mode
+    int commit;              // 1: a step (state advances), 0: statistics only
     int refresh_every;
-    int commit;
+    float lr, momentum;      // used when the kernel updates w and m
     double delta, eps, s_max, trust_coef, weight_decay;
-    double* gradscale;     // [n_layers]
+    double* gradscale;       // [n_layers]
     DevState* state;
-    float2* coef;          // [n_layers] (a_l, b_l)
+    float2* coef;            // [n_layers] (a_l, b_l) as applied, fp32
+    float* corr;             // [n_layers] a_true - a_predicted (fp32)
+    int* corr_flag;          // 1 when some layer needs the correction pass
+    unsigned* layer_count;   // [n_layers] tiles finished (reset by the last block)
+    unsigned* done_count;    // layers finished (reset by the last block)
     ags_layer_stats* lstats;
     ags_global_stats* gstats;
 };
 
 struct UpdateArgs {
     const Tile* tiles;
+    int n_tiles;
     const float* gbar;    // materialised replica mean, or nullptr to recompute
     const void* grads;
     int64_t stride;
@@ -81,15 +89,17 @@ struct UpdateArgs {
     float invK;
     float* w;
     float* m;
-    const float2* coef;
+    const float2* coef;   // LARS update: (a_l, b_l)
+    const float* corr;    // correction pass: a_true - a_predicted
+    const int* corr_flag;
     float lr;
     float momentum;
 };
 
 // Launchers (ags_kernels.hip).  They only enqueue; the return value is the
-// launch status.
-hipError_t launch_stats(const StatsArgs& a, ags_dtype dt, int n_tiles, hipStream_t s);
-hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s);
-hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, int n_tiles, hipStream_t s);
+// launch status.  update != 0 makes the step kernel apply the update.
+hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s);
+hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s);
+hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s);
 
 }  // namespace ags

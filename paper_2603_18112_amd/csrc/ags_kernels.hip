@@ -1,14 +1,26 @@
-// gfx950 kernels of one AGS step: replica mean + per-tile statistics,
-// per-layer finalize (fp64) with the sensitive decision and the gradscale
-// refresh, and the fused momentum-SGD update.
+// gfx950 kernels of one AGS step.
 //
-// All three are HBM-bound streaming kernels (well under 1 flop per byte):
-// they use no matrix cores.  Every thread owns groups of 8 consecutive
-// elements so that each replica row is read with one 16-byte load (bf16)
-// or two (fp32), fully coalesced across the wave.  Reductions are
-// atomic-free and in a fixed order (per-thread, wave butterfly, then the
-// four waves of the block in index order; per layer in fp64 over tiles),
-// so a step is bitwise reproducible.
+// step_kernel     one block per tile: K replica loads -> replica mean and
+//                 spread, per-tile statistics, and (AGS / SGD steps) the
+//                 momentum-SGD update with the coefficient predicted before
+//                 the step.  The last block to finish a layer reduces that
+//                 layer's tile partials in fp64; the last layer to finish
+//                 runs the global decision (Eq. (5), Algorithm 1), the
+//                 coefficients and the gradscale refresh.
+// correct_kernel  AGS steps whose sensitive bit was mispredicted: adds
+//                 (a_true - a_predicted) * gbar to m and -eta times it to w;
+//                 exits at once otherwise.
+// update_kernel   LARS steps: the trust ratio needs the layer norms first,
+//                 so the update is a second pass with the final coefficients.
+//
+// All kernels are HBM-bound streaming kernels (well under one flop per
+// byte) and use no matrix cores.  Every thread owns groups of 8 consecutive
+// elements so each replica row is read with one 16-byte load (bf16) or two
+// (fp32), fully coalesced across the wave.  Reductions are atomic-free in
+// their values and run in a fixed order (per thread, wave butterfly, the
+// four waves in index order, then per layer in fp64 over tiles in index
+// order); the atomics only count finished tiles, so a step is bitwise
+// reproducible.
 #include <math.h>
 
 #include "ags_internal.h"
@@ -47,6 +59,12 @@ __device__ __forceinline__ void load_tail(const T* __restrict__ p, int n, float 
     for (int e = 0; e < kVec; ++e) v[e] = (e < n) ? load1(p + e) : 0.0f;
 }
 
+template <typename GT, bool FULL>
+__device__ __forceinline__ void load_group(const GT* __restrict__ p, int n, float (&v)[kVec]) {
+    if (FULL) load8(p, v);
+    else load_tail(p, n, v);
+}
+
 __device__ __forceinline__ void store8(float* __restrict__ p, const float (&v)[kVec]) {
     *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
     *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
@@ -58,33 +76,34 @@ __device__ __forceinline__ void store_tail(float* __restrict__ p, int n, const f
         if (e < n) p[e] = v[e];
 }
 
-// ------------------------------------------------------ replica moments ---
-//
-// Replica mean and spread of one group, with replica 0 as the shift: for
-// k >= 1, d_k = g_k - g_0, s1 = sum d_k, s2 = sum d_k^2; then
-//   gbar = g_0 + s1 / K   and   sum_k (g_k - gbar)^2 = s2 - s1^2 / K.
-// Identical replicas give d_k = 0, hence gbar = g_0 and a spread of exactly
-// 0; the spread is formed from differences, never as E[g^2] - E[g]^2.
-// The same code produces gbar in the statistics and in the update kernel,
-// so both see the same bits.
-//
-// RMODE selects the small-batch gradient: 0 = replica 0, 1 = mean over
-// replicas (no per-replica value needed), 2 = replica r (runtime).
-
-template <typename GT, bool FULL>
-__device__ __forceinline__ void load_group(const GT* __restrict__ p, int n, float (&v)[kVec]) {
-    if (FULL) load8(p, v);
-    else load_tail(p, n, v);
+template <bool FULL>
+__device__ __forceinline__ void store_group(float* __restrict__ p, int n, const float (&v)[kVec]) {
+    if (FULL) store8(p, v);
+    else store_tail(p, n, v);
 }
 
 // A group of 8 replica values as loaded, before widening to fp32: one
 // 16-byte vector for bf16, two for fp32.  Batches of loads are held in this
 // form so that a batch costs 64 VGPRs whatever the dtype.
 template <typename GT> struct RawGroup;
+// Replica rows are read once per step: AGS_NT_LOADS marks those loads
+// non-temporal (streaming) so they do not displace reused lines.
+#ifndef AGS_NT_LOADS
+#define AGS_NT_LOADS 0
+#endif
+template <typename V>
+__device__ __forceinline__ V stream_load(const V* p) {
+#if AGS_NT_LOADS
+    return __builtin_nontemporal_load(p);
+#else
+    return *p;
+#endif
+}
+
 template <> struct RawGroup<uint16_t> {
     uint4 v;
     __device__ __forceinline__ void load(const uint16_t* __restrict__ p) {
-        v = *reinterpret_cast<const uint4*>(p);
+        v = stream_load(reinterpret_cast<const uint4*>(p));
     }
     __device__ __forceinline__ void widen(float (&o)[kVec]) const {
         o[0] = __uint_as_float(v.x << 16); o[1] = __uint_as_float(v.x & 0xffff0000u);
@@ -96,14 +115,26 @@ template <> struct RawGroup<uint16_t> {
 template <> struct RawGroup<float> {
     float4 a, b;
     __device__ __forceinline__ void load(const float* __restrict__ p) {
-        a = *reinterpret_cast<const float4*>(p);
-        b = *reinterpret_cast<const float4*>(p + 4);
+        a = stream_load(reinterpret_cast<const float4*>(p));
+        b = stream_load(reinterpret_cast<const float4*>(p + 4));
     }
     __device__ __forceinline__ void widen(float (&o)[kVec]) const {
         o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
         o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
     }
 };
+
+// ------------------------------------------------------ replica moments ---
+//
+// Replica mean and spread of one group, with replica 0 as the shift: for
+// k >= 1, d_k = g_k - g_0, s1 = sum d_k, s2 = sum d_k^2; then
+//   gbar = g_0 + s1 / K   and   sum_k (g_k - gbar)^2 = s2 - s1^2 / K.
+// Identical replicas give d_k = 0, hence gbar = g_0 and a spread of exactly
+// 0; the spread is formed from differences, never as E[g^2] - E[g]^2.
+// Every kernel forms gbar with this code, so all of them see the same bits.
+//
+// RMODE selects the small-batch gradient: 0 = replica 0, 1 = mean over
+// replicas (no per-replica value needed), 2 = replica r (runtime).
 
 template <typename GT, int KT, int RMODE, bool FULL>
 __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride, int64_t idx,
@@ -128,22 +159,35 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
     };
     if constexpr (KT > 0 && FULL) {
         // Batches of 64 bytes of replica data per lane (16 bf16 or 8 fp32
-        // replicas): every load of a batch is issued before any is used.
+        // replicas): every load of a batch is issued before any of its
+        // values is used.  The first batch holds replicas 1..KB-1 (replica 0
+        // is the shift); later batches run as a loop so that only one batch
+        // is in registers at a time.
         constexpr int KBMAX = 64 / (int)sizeof(RawGroup<GT>);
         constexpr int KB = KT < KBMAX ? KT : KBMAX;
-#pragma unroll 1
-        for (int kb = 0; kb < KT; kb += KB) {
+        static_assert(KT % KB == 0, "K must be a multiple of the batch");
+        {
             RawGroup<GT> x[KB];
 #pragma unroll
-            for (int j = 0; j < KB; ++j)
-                if (kb + j > 0) x[j].load(g + (int64_t)(kb + j) * stride + idx);
+            for (int j = 1; j < KB; ++j) x[j].load(g + (int64_t)j * stride + idx);
 #pragma unroll
-            for (int j = 0; j < KB; ++j)
-                if (kb + j > 0) {
-                    float v[kVec];
-                    x[j].widen(v);
-                    acc(kb + j, v);
-                }
+            for (int j = 1; j < KB; ++j) {
+                float v[kVec];
+                x[j].widen(v);
+                acc(j, v);
+            }
+        }
+#pragma unroll 1
+        for (int kb = KB; kb < KT; kb += KB) {
+            RawGroup<GT> x[KB];
+#pragma unroll
+            for (int j = 0; j < KB; ++j) x[j].load(g + (int64_t)(kb + j) * stride + idx);
+#pragma unroll
+            for (int j = 0; j < KB; ++j) {
+                float v[kVec];
+                x[j].widen(v);
+                acc(kb + j, v);
+            }
         }
     } else {
         // Runtime K, and the ragged end of a layer (rare; unrolling it
@@ -186,19 +230,164 @@ __device__ __forceinline__ double wave_sum(double v) {
     return v;
 }
 
-// ------------------------------------------- K1: mean + tile statistics ---
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
 
-template <typename GT, int KT, int RMODE, bool FULL>
-__device__ __forceinline__ void stats_group(const StatsArgs& a, const GT* __restrict__ g,
-                                            int64_t idx, int n, int K, float& sw, float& sg,
-                                            float& sd, float& ss) {
-    float wv[kVec], gb[kVec], dv[kVec], gr[kVec];
-    load_group<float, FULL>(a.w + idx, n, wv);
-    moments<GT, KT, RMODE, FULL>(g, a.stride, idx, n, K, a.small_replica, a.invK, gb, dv, gr);
-    if (a.gbar) {
-        if (FULL) store8(a.gbar + idx, gb);
-        else store_tail(a.gbar + idx, n, gb);
+// Sum of v over the block, in a fixed order; every thread gets the result.
+template <typename T>
+__device__ __forceinline__ T block_sum(T v, T* sh /* [kBlock / 64] */) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    v = wave_sum(v);
+    __syncthreads();
+    if (lane == 0) sh[wid] = v;
+    __syncthreads();
+    return (sh[0] + sh[1]) + (sh[2] + sh[3]);
+}
+
+// The step's sensitivity is known before the step when Delta is infinite
+// by definition: a first step, or no positive finite previous norm.
+__device__ __forceinline__ bool surely_sensitive(double g_prev, long long step) {
+    return step == 0 || !(g_prev > 0.0) || !isfinite(g_prev);
+}
+
+// --------------------------------------------- last-block finalize ------
+
+// Per-layer statistics from the layer's tile partials (fp64, fixed order).
+__device__ void finalize_layer(const StepArgs& a, int l, double* shd) {
+    const LayerDev ld = a.layers[l];
+    double w = 0.0, g = 0.0, d = 0.0, s = 0.0;
+    for (int i = ld.tile_begin + (int)threadIdx.x; i < ld.tile_end; i += kBlock) {
+        const Partial p = a.partials[i];
+        w += (double)p.w;
+        g += (double)p.g;
+        d += (double)p.d;
+        s += (double)p.s;
     }
+    w = block_sum(w, shd);
+    g = block_sum(g, shd);
+    d = block_sum(d, shd);
+    s = block_sum(s, shd);
+    if (threadIdx.x == 0) {
+        ags_layer_stats& o = a.lstats[l];
+        o.w_sq = w;
+        o.g_sq = g;
+        o.var = d / (double)a.K;
+        o.gsmall_sq = s;
+    }
+}
+
+// The global decision and every layer's coefficients (one block, after all
+// layers are final).  Delta = |G - G_prev| / G_prev, infinite on a first
+// step, when G_prev <= 0 or when a value is not finite; sensitive =
+// !(Delta < delta).  AGS: a_l = gradscale_l on scaled layers of a
+// non-sensitive step, else 1; LARS: a_l = tau ||w|| / (||g|| + lambda ||w||);
+// b_l = lambda_l (AGS, SGD) or a_l lambda_l (LARS).  When the refresh is due,
+// gradscale_l = min(sqrt(S_l) / (sqrt(G_l) + eps), s_max) (1 if a norm is 0)
+// for the steps that follow.  updated: the step kernel has already applied
+// the predicted coefficients, so record their difference for the correction.
+__device__ void finalize_global(const StepArgs& a, bool updated, double* shd, int* shi) {
+    __shared__ int sh_sens, sh_pred;
+    __shared__ long long sh_t;
+    double G = 0.0;
+    int nf = 0;
+    for (int l = threadIdx.x; l < a.n_layers; l += kBlock) {
+        const ags_layer_stats& o = a.lstats[l];
+        G += o.g_sq;
+        nf |= !(isfinite(o.w_sq) && isfinite(o.g_sq) && isfinite(o.var) && isfinite(o.gsmall_sq));
+    }
+    G = block_sum(G, shd);
+    nf = block_sum(nf, shi) != 0;
+    if (threadIdx.x == 0) {
+        const double Gp = __hip_atomic_load(&a.state->g_prev, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const long long step = __hip_atomic_load(&a.state->step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const long long t = step + 1;
+        double delta;
+        if (surely_sensitive(Gp, step) || !isfinite(G))
+            delta = INFINITY;
+        else
+            delta = fabs((G - Gp) / Gp);
+        const int sens = !(delta < a.delta);
+        if (!isfinite(G)) nf = 1;
+        ags_global_stats gs;
+        gs.step = a.commit ? t : step;
+        gs.g_sq = G;
+        gs.g_sq_prev = (t == 1) ? 0.0 : Gp;
+        gs.delta = delta;
+        gs.sensitive = sens;
+        gs.nonfinite = nf;
+        *a.gstats = gs;
+        if (a.commit) {
+            a.state->g_prev = G;
+            a.state->step = t;
+        }
+        sh_sens = sens;
+        sh_pred = surely_sensitive(Gp, step);
+        sh_t = t;
+    }
+    __syncthreads();
+    const int sens = sh_sens, pred = sh_pred;
+    const long long t = sh_t;
+    const bool refresh = a.commit && a.mode == AGS_MODE_AGS && a.refresh_every > 0 &&
+                         (t % a.refresh_every) == 0;
+    const double smax = a.s_max > 0.0 ? a.s_max : sqrt((double)a.K);
+    int need = 0;
+    for (int l = threadIdx.x; l < a.n_layers; l += kBlock) {
+        ags_layer_stats& o = a.lstats[l];
+        const uint32_t f = a.layers[l].flags;
+        const bool scaled = (f & AGS_LAYER_SCALE) != 0;
+        const double lam = (f & AGS_LAYER_DECAY) ? a.weight_decay : 0.0;
+        const double gs_old = a.gradscale[l];
+        double ca = 1.0, cb = lam;
+        if (a.mode == AGS_MODE_AGS) {
+            ca = (scaled && !sens) ? gs_old : 1.0;
+        } else if (a.mode == AGS_MODE_LARS) {
+            if (scaled) {
+                const double wn = sqrt(o.w_sq), gn = sqrt(o.g_sq);
+                ca = (wn > 0.0 && gn > 0.0) ? a.trust_coef * wn / (gn + lam * wn) : 1.0;
+            }
+            cb = ca * lam;
+        }
+        o.noise_ratio = (o.g_sq > 0.0) ? o.var / o.g_sq : ((o.var > 0.0) ? INFINITY : 0.0);
+        o.coef_a = ca;
+        o.coef_b = cb;
+        a.coef[l] = make_float2((float)ca, (float)cb);
+        if (updated) {
+            const double ap = (a.mode == AGS_MODE_AGS && scaled && !pred) ? gs_old : 1.0;
+            const float c = (float)ca - (float)ap;
+            a.corr[l] = c;
+            need |= (c != 0.0f);
+        }
+        double gsc = gs_old;
+        if (refresh && scaled) {
+            const double S = o.gsmall_sq, Gl = o.g_sq;
+            if (S > 0.0 && Gl > 0.0) {
+                gsc = sqrt(S) / (sqrt(Gl) + a.eps);
+                if (gsc > smax) gsc = smax;
+            } else {
+                gsc = 1.0;
+            }
+            a.gradscale[l] = gsc;
+        }
+        o.gradscale = gsc;
+    }
+    need = block_sum(need, shi);
+    if (threadIdx.x == 0) *a.corr_flag = (updated && need) ? 1 : 0;
+}
+
+// ------------------------------------------------- the fused step kernel ---
+
+template <typename GT, int KT, int RMODE, bool UPD, bool FULL>
+__device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restrict__ g,
+                                           int64_t idx, int n, int K, float ca, float cb,
+                                           float& sw, float& sg, float& sd, float& ss) {
+    float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
+    load_group<float, FULL>(a.w + idx, n, wv);
+    if (UPD) load_group<float, FULL>(a.m + idx, n, mv);
+    moments<GT, KT, RMODE, FULL>(g, a.stride, idx, n, K, a.small_replica, a.invK, gb, dv, gr);
+    if (!UPD && a.gbar) store_group<FULL>(a.gbar + idx, n, gb);
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
         sw = fmaf(wv[e], wv[e], sw);
@@ -208,22 +397,53 @@ __device__ __forceinline__ void stats_group(const StatsArgs& a, const GT* __rest
         if (RMODE == 1) ss += fmaf(gb[e], gb[e], dv[e] * a.invK);
         else ss = fmaf(gr[e], gr[e], ss);
     }
+    if (UPD) {
+        // d = a gbar + b w ; m <- mu m + d ; w <- w - eta m
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) {
+            const float d = fmaf(ca, gb[e], cb * wv[e]);
+            mv[e] = fmaf(a.momentum, mv[e], d);
+            wv[e] = fmaf(-a.lr, mv[e], wv[e]);
+        }
+        store_group<FULL>(a.w + idx, n, wv);
+        store_group<FULL>(a.m + idx, n, mv);
+    }
 }
 
-template <typename GT, int KT, int RMODE>
-__global__ __launch_bounds__(kBlock) void stats_kernel(StatsArgs a) {
+#ifndef AGS_STEP_MIN_WAVES
+#define AGS_STEP_MIN_WAVES 1
+#endif
+template <typename GT, int KT, int RMODE, bool UPD>
+__global__ __launch_bounds__(kBlock, AGS_STEP_MIN_WAVES) void step_kernel(StepArgs a) {
     __shared__ float red[4][kBlock / 64];
+    __shared__ double shd[kBlock / 64];
+    __shared__ int shi[kBlock / 64];
+    __shared__ int sh_last;
     const Tile t = a.tiles[blockIdx.x];
+    const int l = t.layer;
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
+
+    // Coefficients predicted before the step: on a step whose Delta is
+    // infinite by definition the unscaled ones, otherwise the scaled ones.
+    float ca = 1.0f, cb = 0.0f;
+    if (UPD) {
+        const uint32_t f = a.layers[l].flags;
+        const bool pred = surely_sensitive(a.state->g_prev, a.state->step);
+        if (a.mode == AGS_MODE_AGS && (f & AGS_LAYER_SCALE) && !pred) ca = (float)a.gradscale[l];
+        cb = (f & AGS_LAYER_DECAY) ? (float)a.weight_decay : 0.0f;
+    }
+
     float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f;
     const int nfull = t.count / kVec;
 #pragma unroll 1
     for (int c = threadIdx.x; c < nfull; c += kBlock)
-        stats_group<GT, KT, RMODE, true>(a, g, t.begin + (int64_t)c * kVec, kVec, K, sw, sg, sd, ss);
+        step_group<GT, KT, RMODE, UPD, true>(a, g, t.begin + (int64_t)c * kVec, kVec, K, ca, cb,
+                                             sw, sg, sd, ss);
     const int rem = t.count - nfull * kVec;
     if (rem > 0 && (int)threadIdx.x == nfull % kBlock)
-        stats_group<GT, KT, RMODE, false>(a, g, t.begin + (int64_t)nfull * kVec, rem, K, sw, sg, sd, ss);
+        step_group<GT, KT, RMODE, UPD, false>(a, g, t.begin + (int64_t)nfull * kVec, rem, K, ca,
+                                              cb, sw, sg, sd, ss);
 
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
     sw = wave_sum(sw);
@@ -244,135 +464,75 @@ __global__ __launch_bounds__(kBlock) void stats_kernel(StatsArgs a) {
         p.d = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
         p.s = (red[3][0] + red[3][1]) + (red[3][2] + red[3][3]);
         a.partials[blockIdx.x] = p;
-    }
-}
-
-// ----------------------------------- K2: per-layer finalize + decision ---
-//
-// One block.  (A) each wave sums the fp32 tile partials of its layers in
-// fp64 (lane-strided, then a butterfly); (B) wave 0 forms G = sum_l G_l,
-// Delta = |G - G_prev| / G_prev (inf on a first step, when G_prev <= 0 or
-// a value is not finite), sensitive = !(Delta < delta), and commits
-// G_prev / step; (C) one thread per layer forms the update coefficients
-// and, when due, refreshes gradscale = min(sqrt(S)/(sqrt(G_l)+eps), s_max)
-// (1 when a norm is 0) for the steps that follow.
-
-__global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(FinalizeArgs a) {
-    __shared__ int sh_sens;
-    __shared__ long long sh_t;
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    const double invK = 1.0 / (double)a.K;
-
-    for (int l = wid; l < a.n_layers; l += nw) {
+        // Publish the partial, then count the tile; the block that counts a
+        // layer's last tile reduces the layer.
+        __threadfence();
         const LayerDev ld = a.layers[l];
-        double w = 0.0, g = 0.0, d = 0.0, s = 0.0;
-        for (int t = ld.tile_begin + lane; t < ld.tile_end; t += 64) {
-            const Partial p = a.partials[t];
-            w += (double)p.w;
-            g += (double)p.g;
-            d += (double)p.d;
-            s += (double)p.s;
-        }
-        w = wave_sum(w);
-        g = wave_sum(g);
-        d = wave_sum(d);
-        s = wave_sum(s);
-        if (lane == 0) {
-            ags_layer_stats& o = a.lstats[l];
-            o.w_sq = w;
-            o.g_sq = g;
-            o.var = d * invK;
-            o.gsmall_sq = s;
-        }
-    }
-    __threadfence_block();
-    __syncthreads();
-
-    if (wid == 0) {
-        double G = 0.0;
-        int nf = 0;
-        for (int l = lane; l < a.n_layers; l += 64) {
-            const ags_layer_stats& o = a.lstats[l];
-            G += o.g_sq;
-            nf |= !(isfinite(o.w_sq) && isfinite(o.g_sq) && isfinite(o.var) && isfinite(o.gsmall_sq));
-        }
-        G = wave_sum(G);
-        nf = __any(nf) ? 1 : 0;
-        if (lane == 0) {
-            const DevState st = *a.state;
-            const long long t = st.step + 1;
-            const double Gp = st.g_prev;
-            double delta;
-            if (t == 1 || !(Gp > 0.0) || !isfinite(Gp) || !isfinite(G))
-                delta = INFINITY;
-            else
-                delta = fabs((G - Gp) / Gp);
-            const int sens = !(delta < a.delta);
-            if (!isfinite(G)) nf = 1;
-            ags_global_stats gs;
-            gs.step = a.commit ? t : st.step;
-            gs.g_sq = G;
-            gs.g_sq_prev = (t == 1) ? 0.0 : Gp;
-            gs.delta = delta;
-            gs.sensitive = sens;
-            gs.nonfinite = nf;
-            *a.gstats = gs;
-            if (a.commit) {
-                a.state->g_prev = G;
-                a.state->step = t;
-            }
-            sh_sens = sens;
-            sh_t = t;
-        }
+        const unsigned prev = atomicAdd(&a.layer_count[l], 1u);
+        sh_last = (prev + 1 == (unsigned)(ld.tile_end - ld.tile_begin));
     }
     __syncthreads();
+    if (!sh_last) return;
+    __threadfence();
+    finalize_layer(a, l, shd);
+    if (threadIdx.x == 0) {
+        a.layer_count[l] = 0u;  // ready for the next launch
+        __threadfence();
+        const unsigned prev = atomicAdd(a.done_count, 1u);
+        sh_last = (prev + 1 == (unsigned)a.n_layers);
+    }
+    __syncthreads();
+    if (!sh_last) return;
+    __threadfence();
+    finalize_global(a, UPD, shd, shi);
+    if (threadIdx.x == 0) *a.done_count = 0u;
+}
 
-    const int sens = sh_sens;
-    const long long t = sh_t;
-    const bool refresh = a.commit && a.mode == AGS_MODE_AGS && a.refresh_every > 0 &&
-                         (t % a.refresh_every) == 0;
-    const double smax = a.s_max > 0.0 ? a.s_max : sqrt((double)a.K);
-    for (int l = threadIdx.x; l < a.n_layers; l += blockDim.x) {
-        ags_layer_stats& o = a.lstats[l];
-        const uint32_t f = a.layers[l].flags;
-        const bool scaled = (f & AGS_LAYER_SCALE) != 0;
-        const double lam = (f & AGS_LAYER_DECAY) ? a.weight_decay : 0.0;
-        double ca = 1.0, cb = lam;
-        if (a.mode == AGS_MODE_AGS) {
-            ca = (scaled && !sens) ? a.gradscale[l] : 1.0;
-        } else if (a.mode == AGS_MODE_LARS) {
-            if (scaled) {
-                const double wn = sqrt(o.w_sq), gn = sqrt(o.g_sq);
-                ca = (wn > 0.0 && gn > 0.0) ? a.trust_coef * wn / (gn + lam * wn) : 1.0;
-            }
-            cb = ca * lam;
-        }
-        o.noise_ratio = (o.g_sq > 0.0) ? o.var / o.g_sq : ((o.var > 0.0) ? INFINITY : 0.0);
-        o.coef_a = ca;
-        o.coef_b = cb;
-        a.coef[l] = make_float2((float)ca, (float)cb);
-        double gsc = a.gradscale[l];
-        if (refresh && scaled) {
-            const double S = o.gsmall_sq, Gl = o.g_sq;
-            if (S > 0.0 && Gl > 0.0) {
-                gsc = sqrt(S) / (sqrt(Gl) + a.eps);
-                if (gsc > smax) gsc = smax;
-            } else {
-                gsc = 1.0;
-            }
-            a.gradscale[l] = gsc;
-        }
-        o.gradscale = gsc;
+// ----------------------------------------- correction and LARS update ---
+
+// Correction of a mispredicted AGS step: m += c gbar, w -= eta c gbar with
+// c = a_true - a_predicted of the layer (0 for most layers).
+template <typename GT, int KT, bool FULL>
+__device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __restrict__ g,
+                                              int64_t idx, int n, int K, float c) {
+    float gb[kVec], dv[kVec], gr[kVec], wv[kVec], mv[kVec];
+    load_group<float, FULL>(a.w + idx, n, wv);
+    load_group<float, FULL>(a.m + idx, n, mv);
+    moments<GT, KT, 0, FULL>(g, a.stride, idx, n, K, 0, a.invK, gb, dv, gr);
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) {
+        const float cg = c * gb[e];
+        mv[e] += cg;
+        wv[e] = fmaf(-a.lr, cg, wv[e]);
+    }
+    store_group<FULL>(a.w + idx, n, wv);
+    store_group<FULL>(a.m + idx, n, mv);
+}
+
+template <typename GT, int KT>
+__global__ __launch_bounds__(kBlock) void correct_kernel(UpdateArgs a) {
+    if (*a.corr_flag == 0) return;
+    const GT* __restrict__ g = static_cast<const GT*>(a.grads);
+    const int K = KT > 0 ? KT : a.K;
+#pragma unroll 1
+    for (int ti = blockIdx.x; ti < a.n_tiles; ti += gridDim.x) {
+        const Tile t = a.tiles[ti];
+        const float c = a.corr[t.layer];
+        if (c == 0.0f) continue;
+        const int nfull = t.count / kVec;
+#pragma unroll 1
+        for (int q = threadIdx.x; q < nfull; q += kBlock)
+            correct_group<GT, KT, true>(a, g, t.begin + (int64_t)q * kVec, kVec, K, c);
+        const int rem = t.count - nfull * kVec;
+        if (rem > 0 && (int)threadIdx.x == nfull % kBlock)
+            correct_group<GT, KT, false>(a, g, t.begin + (int64_t)nfull * kVec, rem, K, c);
     }
 }
 
-// ----------------------------------------------- K3: fused update ---------
-//
-// d = a_l gbar + b_l w ; m <- mu m + d ; w <- w - eta m, read once, written
-// once.  gbar comes from the statistics kernel's buffer or, when re-reading
-// the replicas costs no more than that round trip (K * bytes <= 8), is
+// LARS: d = a_l gbar + b_l w ; m <- mu m + d ; w <- w - eta m with the
+// final coefficients.  gbar comes from the step kernel's buffer or, when
+// re-reading the replicas costs no more than that round trip, is
 // recomputed from them by the same code.
-
 template <typename GT, int KT, bool RECOMP, bool FULL>
 __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __restrict__ g,
                                              int64_t idx, int n, int K, float ca, float cb) {
@@ -391,13 +551,8 @@ __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __re
         mv[e] = fmaf(a.momentum, mv[e], d);
         wv[e] = fmaf(-a.lr, mv[e], wv[e]);
     }
-    if (FULL) {
-        store8(a.w + idx, wv);
-        store8(a.m + idx, mv);
-    } else {
-        store_tail(a.w + idx, n, wv);
-        store_tail(a.m + idx, n, mv);
-    }
+    store_group<FULL>(a.w + idx, n, wv);
+    store_group<FULL>(a.m + idx, n, mv);
 }
 
 template <typename GT, int KT, bool RECOMP>
@@ -418,34 +573,24 @@ __global__ __launch_bounds__(kBlock) void update_kernel(UpdateArgs a) {
 // ----------------------------------------------------------- dispatch ---
 
 template <typename GT, int KT>
-hipError_t stats_k(const StatsArgs& a, int n_tiles, hipStream_t s) {
+hipError_t step_k(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
     const dim3 grid(n_tiles), block(kBlock);
-    if (a.small_replica == 0)
-        hipLaunchKernelGGL((stats_kernel<GT, KT, 0>), grid, block, 0, s, a);
-    else if (a.small_replica < 0)
-        hipLaunchKernelGGL((stats_kernel<GT, KT, 1>), grid, block, 0, s, a);
-    else
-        hipLaunchKernelGGL((stats_kernel<GT, KT, 2>), grid, block, 0, s, a);
+    const int rm = a.small_replica == 0 ? 0 : (a.small_replica < 0 ? 1 : 2);
+    if (update) {
+        if (rm == 0) hipLaunchKernelGGL((step_kernel<GT, KT, 0, true>), grid, block, 0, s, a);
+        else if (rm == 1) hipLaunchKernelGGL((step_kernel<GT, KT, 1, true>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((step_kernel<GT, KT, 2, true>), grid, block, 0, s, a);
+    } else {
+        if (rm == 0) hipLaunchKernelGGL((step_kernel<GT, KT, 0, false>), grid, block, 0, s, a);
+        else if (rm == 1) hipLaunchKernelGGL((step_kernel<GT, KT, 1, false>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((step_kernel<GT, KT, 2, false>), grid, block, 0, s, a);
+    }
     return hipGetLastError();
 }
 
-template <typename GT>
-hipError_t stats_t(const StatsArgs& a, int n_tiles, hipStream_t s) {
-    switch (a.K) {
-        case 1: return stats_k<GT, 1>(a, n_tiles, s);
-        case 2: return stats_k<GT, 2>(a, n_tiles, s);
-        case 4: return stats_k<GT, 4>(a, n_tiles, s);
-        case 8: return stats_k<GT, 8>(a, n_tiles, s);
-        case 16: return stats_k<GT, 16>(a, n_tiles, s);
-        case 32: return stats_k<GT, 32>(a, n_tiles, s);
-        case 64: return stats_k<GT, 64>(a, n_tiles, s);
-        default: return stats_k<GT, 0>(a, n_tiles, s);
-    }
-}
-
 template <typename GT, int KT>
-hipError_t update_k(const UpdateArgs& a, int n_tiles, hipStream_t s) {
-    const dim3 grid(n_tiles), block(kBlock);
+hipError_t update_k(const UpdateArgs& a, hipStream_t s) {
+    const dim3 grid(a.n_tiles), block(kBlock);
     if (a.gbar)
         hipLaunchKernelGGL((update_kernel<GT, KT, false>), grid, block, 0, s, a);
     else
@@ -453,33 +598,51 @@ hipError_t update_k(const UpdateArgs& a, int n_tiles, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <typename GT>
-hipError_t update_t(const UpdateArgs& a, int n_tiles, hipStream_t s) {
-    switch (a.K) {
-        case 1: return update_k<GT, 1>(a, n_tiles, s);
-        case 2: return update_k<GT, 2>(a, n_tiles, s);
-        case 4: return update_k<GT, 4>(a, n_tiles, s);
-        case 8: return update_k<GT, 8>(a, n_tiles, s);
-        case 16: return update_k<GT, 16>(a, n_tiles, s);
-        case 32: return update_k<GT, 32>(a, n_tiles, s);
-        case 64: return update_k<GT, 64>(a, n_tiles, s);
-        default: return update_k<GT, 0>(a, n_tiles, s);
+template <typename GT, int KT>
+hipError_t correct_k(const UpdateArgs& a, hipStream_t s) {
+    const int nb = a.n_tiles < kCorrectBlocks ? a.n_tiles : kCorrectBlocks;
+    hipLaunchKernelGGL((correct_kernel<GT, KT>), dim3(nb), dim3(kBlock), 0, s, a);
+    return hipGetLastError();
+}
+
+#define AGS_K_DISPATCH(FN, GT, K, ...)           \
+    switch (K) {                                 \
+        case 1: return FN<GT, 1>(__VA_ARGS__);   \
+        case 2: return FN<GT, 2>(__VA_ARGS__);   \
+        case 4: return FN<GT, 4>(__VA_ARGS__);   \
+        case 8: return FN<GT, 8>(__VA_ARGS__);   \
+        case 16: return FN<GT, 16>(__VA_ARGS__); \
+        case 32: return FN<GT, 32>(__VA_ARGS__); \
+        case 64: return FN<GT, 64>(__VA_ARGS__); \
+        default: return FN<GT, 0>(__VA_ARGS__);  \
     }
+
+template <typename GT>
+hipError_t step_t(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
+    AGS_K_DISPATCH(step_k, GT, a.K, a, n_tiles, update, s)
+}
+template <typename GT>
+hipError_t update_t(const UpdateArgs& a, hipStream_t s) {
+    AGS_K_DISPATCH(update_k, GT, a.K, a, s)
+}
+template <typename GT>
+hipError_t correct_t(const UpdateArgs& a, hipStream_t s) {
+    AGS_K_DISPATCH(correct_k, GT, a.K, a, s)
 }
 
 }  // namespace
 
-hipError_t launch_stats(const StatsArgs& a, ags_dtype dt, int n_tiles, hipStream_t s) {
-    return dt == AGS_BF16 ? stats_t<uint16_t>(a, n_tiles, s) : stats_t<float>(a, n_tiles, s);
+hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s) {
+    return dt == AGS_BF16 ? step_t<uint16_t>(a, n_tiles, update, s)
+                          : step_t<float>(a, n_tiles, update, s);
 }
 
-hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kFinalizeThreads), 0, s, a);
-    return hipGetLastError();
+hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s) {
+    return dt == AGS_BF16 ? update_t<uint16_t>(a, s) : update_t<float>(a, s);
 }
 
-hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, int n_tiles, hipStream_t s) {
-    return dt == AGS_BF16 ? update_t<uint16_t>(a, n_tiles, s) : update_t<float>(a, n_tiles, s);
+hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s) {
+    return dt == AGS_BF16 ? correct_t<uint16_t>(a, s) : correct_t<float>(a, s);
 }
 
 }  // namespace ags

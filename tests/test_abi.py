@@ -69,14 +69,19 @@ def _ws(layers=None, n_flat=136, K=4, **kw):
 def test_valid_config_workspace_size(lib):
     st, n = _ws()
     assert st == ags.AGS_OK and n > 0
-    # ResNet-50, K = 16 bf16: the replica mean (fp32, one per element) is
-    # kept, plus small per-tile and per-layer tables.
+    # ResNet-50, K = 16 bf16.  AGS and SGD steps update w and m in the
+    # statistics pass, so the workspace is only per-tile and per-layer tables.
     lay = layouts.get_layout("resnet50")
-    cfg = ags.make_config(lay.table(), lay.n_flat, 16, grad_dtype="bf16")
+    for mode in ("ags", "sgd"):
+        cfg = ags.make_config(lay.table(), lay.n_flat, 16, grad_dtype="bf16", mode=mode)
+        assert ags.ags_workspace_bytes(cfg) < 2_000_000
+    # A LARS step needs its layer norms before the update: it keeps the
+    # replica mean (fp32, one per element) between its two passes ...
+    cfg = ags.make_config(lay.table(), lay.n_flat, 16, grad_dtype="bf16", mode="lars")
     n = ags.ags_workspace_bytes(cfg)
     assert lay.n_flat * 4 <= n < lay.n_flat * 4 + 2_000_000
-    # K = 4 bf16 (8 bytes per element) re-reads the replicas instead
-    cfg = ags.make_config(lay.table(), lay.n_flat, 4, grad_dtype="bf16")
+    # ... unless re-reading the replicas is as cheap (K = 4 bf16: 8 bytes).
+    cfg = ags.make_config(lay.table(), lay.n_flat, 4, grad_dtype="bf16", mode="lars")
     assert ags.ags_workspace_bytes(cfg) < 2_000_000
 
 

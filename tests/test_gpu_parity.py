@@ -157,6 +157,27 @@ def test_forced_spike_takes_unscaled_branch():
     p.close()
 
 
+@pytest.mark.parametrize("K,dtype", [(4, "f32"), (16, "bf16"), (3, "bf16")])
+def test_mispredicted_steps_are_corrected(K, dtype):
+    """AGS steps are applied with the coefficients predicted before the step
+    (scaled unless Delta is infinite by definition); a sensitive step then
+    takes the correction pass.  Gradient scales 1, 1, 2, 2, 0.25, 0.25, 1, 1
+    make steps 1, 3, 5 and 7 sensitive (Delta = inf, 3, 0.9375, 15)."""
+    lay = layouts.custom_layout(RAGGED, pad=8)
+    base = synth.replica_grads(lay, K, 0, 4, dtype="f32")
+    p = Pair(lay, K, dtype=dtype, seed=4)
+    sens = []
+    for t, c in enumerate([1, 1, 2, 2, 0.25, 0.25, 1, 1]):
+        g = (base * np.float32(c)).astype(np.float32)
+        if dtype == "bf16":
+            g = synth.to_bf16_bits(g)
+        s, _ = p.step(g, what=f"mispredict step {t + 1}")
+        sens.append(s.glob["sensitive"])
+        p.check_state(f"mispredict step {t + 1}")
+    assert sens == [1, 0, 1, 0, 1, 0, 1, 0]
+    p.close()
+
+
 def test_zero_and_nonfinite_gradients():
     lay = layouts.custom_layout([300, 17], pad=8)
     p = Pair(lay, 3, w0=np.ones(lay.n_flat, np.float32))
