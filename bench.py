@@ -3,8 +3,9 @@
 Workload: ResNet-50 ImageNet layout (161 tensors, 25,557,032 parameters),
 K = 16 bf16 replica gradients, fp32 weights and momentum, AGS mode.  A step
 is one full pass of the hot path: replica mean, per-layer statistics,
-decision and update (the step kernel, then the correction pass, which exits
-at once when the sensitive bit was predicted right, on one stream).  Inputs are seeded and
+decision and update (the step kernel, the finalize kernel and the correction
+pass, which exits at once when the sensitive bit was predicted right, on one
+stream).  Inputs are seeded and
 synthetic and already resident in HBM when timing starts; the timed steps
 reuse one generated gradient set.
 
@@ -65,7 +66,7 @@ def algorithmic_bytes(n_params: int):
     second pass (the correction of a mispredicted sensitive bit) moves no
     data on the steps timed here, whose bit is predicted correctly."""
     step = n_params * (K * E_G + 16)
-    return {"step": step, "second_pass": 0}
+    return {"step": step, "finalize": 0, "second_pass": 0}
 
 
 def read_traffic(kernel: str):

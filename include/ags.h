@@ -130,12 +130,13 @@ typedef struct {
 
 typedef struct ags_handle ags_handle;
 
-/* Passes of one step, in launch order, for ags_get_kernel_times:
- * 0: the step kernel (replica mean, statistics, decision and, for AGS and
- *    SGD, the update with the coefficients predicted before the step);
- * 1: the second pass (AGS: correction of a mispredicted sensitive bit,
- *    empty otherwise; LARS: the update; SGD: none). */
-#define AGS_N_KERNELS 2
+/* Kernels of one step, in launch order, for ags_get_kernel_times:
+ * 0: the step kernel (replica mean, tile statistics and, for AGS and SGD,
+ *    the update with the coefficients predicted before the step);
+ * 1: finalize (layer and global statistics, decision, refresh);
+ * 2: the second pass (AGS: correction of a mispredicted sensitive bit,
+ *    which exits at once otherwise; LARS: the update; SGD: none). */
+#define AGS_N_KERNELS 3
 
 /* Bytes of device workspace ags_init would allocate for cfg (host only). */
 ags_status ags_workspace_bytes(const ags_config *cfg, size_t *out_bytes);

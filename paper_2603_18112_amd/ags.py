@@ -30,8 +30,8 @@ AGS_MODE_SGD, AGS_MODE_AGS, AGS_MODE_LARS = 0, 1, 2
 AGS_LAYER_SCALE, AGS_LAYER_DECAY = 1, 2
 AGS_ALIGN_ELEMS = 8
 AGS_MAX_K = 1024
-AGS_N_KERNELS = 2
-KERNEL_NAMES = ("step", "second_pass")
+AGS_N_KERNELS = 3
+KERNEL_NAMES = ("step", "finalize", "second_pass")
 MODES = {"sgd": AGS_MODE_SGD, "ags": AGS_MODE_AGS, "lars": AGS_MODE_LARS}
 DTYPES = {"f32": AGS_F32, "bf16": AGS_BF16}
 

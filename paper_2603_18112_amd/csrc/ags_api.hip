@@ -32,7 +32,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // that a read-back is one copy.
 struct WsLayout {
     size_t gbar = 0, tiles = 0, partials = 0, ldev = 0, coef = 0, corr = 0, counters = 0;
-    size_t counters_bytes = 0;  // layer counters, done counter, correction flag
+    size_t counters_bytes = 0;  // finished-layer counter, correction flag
     size_t lstats = 0, gstats = 0, gradscale = 0, state = 0, end = 0;
     size_t rec_bytes = 0;    // lstats .. gstats end
     size_t state_bytes = 0;  // gradscale .. state end
@@ -64,7 +64,7 @@ WsLayout ws_layout(const ags_config& c, int64_t n_tiles) {
     w.corr = p;
     p = align_up(p + L * sizeof(float));
     w.counters = p;
-    w.counters_bytes = (L + 2) * sizeof(unsigned);
+    w.counters_bytes = 2 * sizeof(unsigned);
     p = align_up(p + w.counters_bytes);
     w.lstats = p;
     p += L * sizeof(ags_layer_stats);
@@ -227,9 +227,8 @@ struct ags_handle {
     LayerDev* ldev() const { return reinterpret_cast<LayerDev*>(ws + wl.ldev); }
     float2* coef() const { return reinterpret_cast<float2*>(ws + wl.coef); }
     float* corr() const { return reinterpret_cast<float*>(ws + wl.corr); }
-    unsigned* layer_count() const { return reinterpret_cast<unsigned*>(ws + wl.counters); }
-    unsigned* done_count() const { return layer_count() + cfg.n_layers; }
-    int* corr_flag() const { return reinterpret_cast<int*>(layer_count() + cfg.n_layers + 1); }
+    unsigned* done_count() const { return reinterpret_cast<unsigned*>(ws + wl.counters); }
+    int* corr_flag() const { return reinterpret_cast<int*>(done_count() + 1); }
     float* gbar() const { return materialize ? reinterpret_cast<float*>(ws + wl.gbar) : nullptr; }
     ags_layer_stats* lstats() const { return reinterpret_cast<ags_layer_stats*>(ws + wl.lstats); }
     ags_global_stats* gstats() const { return reinterpret_cast<ags_global_stats*>(ws + wl.gstats); }
@@ -337,13 +336,16 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.coef = h->coef();
     sa.corr = h->corr();
     sa.corr_flag = h->corr_flag();
-    sa.layer_count = h->layer_count();
+    sa.updated = fused ? 1 : 0;
     sa.done_count = h->done_count();
     sa.lstats = h->lstats();
     sa.gstats = h->gstats();
     hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s);
     if (e != hipSuccess) return h->hip_fail(e, "step kernel launch");
     if (prof) (void)hipEventRecord(ev[1], s);
+    e = ags::launch_finalize(sa, s);
+    if (e != hipSuccess) return h->hip_fail(e, "finalize kernel launch");
+    if (prof) (void)hipEventRecord(ev[2], s);
 
     if (commit && c.mode != AGS_MODE_SGD) {
         ags::UpdateArgs ua{};
@@ -366,7 +368,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         if (e != hipSuccess) return h->hip_fail(e, "second-pass kernel launch");
     }
     if (prof) {
-        (void)hipEventRecord(ev[2], s);
+        (void)hipEventRecord(ev[3], s);
         h->ev_pending.push_back(ev);
     }
     h->last_stream = s;
@@ -632,7 +634,7 @@ ags_status ags_set_profiling(ags_handle* h, int enable) {
 ags_status ags_get_kernel_times(ags_handle* h, double* out_ms, int64_t* out_calls) {
     if (!h) return AGS_E_ARG;
     if (!out_ms || !out_calls) return h->fail(AGS_E_ARG, "NULL output pointer");
-    double tot[AGS_N_KERNELS] = {0, 0};
+    double tot[AGS_N_KERNELS] = {0, 0, 0};
     for (auto& q : h->ev_pending) {
         hipError_t e = hipEventSynchronize(q[AGS_N_KERNELS]);
         if (e != hipSuccess) return h->hip_fail(e, "hipEventSynchronize");

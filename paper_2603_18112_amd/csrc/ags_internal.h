@@ -47,9 +47,9 @@ struct Partial {
     float w, g, d, s;
 };
 
-// Arguments of the fused step kernel (statistics of every tile, the
-// per-layer and global finalize in the last blocks, and -- when update is
-// on -- the momentum-SGD update with the predicted coefficients).
+// Arguments of the step kernel (statistics of every tile and -- when update
+// is on -- the momentum-SGD update with the predicted coefficients) and of
+// the finalize kernel (per-layer and global statistics, the decision).
 struct StepArgs {
     const void* grads;
     int64_t stride;
@@ -73,7 +73,7 @@ struct StepArgs {
     float2* coef;            // [n_layers] (a_l, b_l) as applied, fp32
     float* corr;             // [n_layers] a_true - a_predicted (fp32)
     int* corr_flag;          // 1 when some layer needs the correction pass
-    unsigned* layer_count;   // [n_layers] tiles finished (reset by the last block)
+    int updated;             // the step kernel applied predicted coefficients
     unsigned* done_count;    // layers finished (reset by the last block)
     ags_layer_stats* lstats;
     ags_global_stats* gstats;
@@ -99,6 +99,7 @@ struct UpdateArgs {
 // Launchers (ags_kernels.hip).  They only enqueue; the return value is the
 // launch status.  update != 0 makes the step kernel apply the update.
 hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s);
+hipError_t launch_finalize(const StepArgs& a, hipStream_t s);
 hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s);
 hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s);
 

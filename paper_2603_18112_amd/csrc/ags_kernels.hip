@@ -1,26 +1,26 @@
 // gfx950 kernels of one AGS step.
 //
-// step_kernel     one block per tile: K replica loads -> replica mean and
-//                 spread, per-tile statistics, and (AGS / SGD steps) the
-//                 momentum-SGD update with the coefficient predicted before
-//                 the step.  The last block to finish a layer reduces that
-//                 layer's tile partials in fp64; the last layer to finish
-//                 runs the global decision (Eq. (5), Algorithm 1), the
-//                 coefficients and the gradscale refresh.
-// correct_kernel  AGS steps whose sensitive bit was mispredicted: adds
-//                 (a_true - a_predicted) * gbar to m and -eta times it to w;
-//                 exits at once otherwise.
-// update_kernel   LARS steps: the trust ratio needs the layer norms first,
-//                 so the update is a second pass with the final coefficients.
+// step_kernel      one block per tile: K replica loads -> replica mean and
+//                  spread and the tile's partial statistics, and (AGS / SGD
+//                  steps) the momentum-SGD update with the coefficients
+//                  predicted before the step.
+// finalize_kernel  one block per layer: the layer's statistics from its tile
+//                  partials in fp64; the last layer to finish runs the global
+//                  decision (Eq. (5), Algorithm 1), the coefficients and the
+//                  gradscale refresh.
+// correct_kernel   AGS steps whose sensitive bit was mispredicted: adds
+//                  (a_true - a_predicted) * gbar to m and -eta times it to w;
+//                  exits at once otherwise.
+// update_kernel    LARS steps: the trust ratio needs the layer norms first,
+//                  so the update is a second pass with the final coefficients.
 //
-// All kernels are HBM-bound streaming kernels (well under one flop per
-// byte) and use no matrix cores.  Every thread owns groups of 8 consecutive
-// elements so each replica row is read with one 16-byte load (bf16) or two
-// (fp32), fully coalesced across the wave.  Reductions are atomic-free in
-// their values and run in a fixed order (per thread, wave butterfly, the
-// four waves in index order, then per layer in fp64 over tiles in index
-// order); the atomics only count finished tiles, so a step is bitwise
-// reproducible.
+// The streaming kernels are HBM-bound (well under one flop per byte) and use
+// no matrix cores.  Every thread owns groups of 8 consecutive elements so
+// each replica row is read with one 16-byte load (bf16) or two (fp32), fully
+// coalesced across the wave.  Reductions run in a fixed order (per thread,
+// wave butterfly, the four waves in index order, then per layer in fp64 over
+// tiles in index order); the one atomic only counts finished layers, so a
+// step is bitwise reproducible.
 #include <math.h>
 
 #include "ags_internal.h"
@@ -91,10 +91,20 @@ template <typename GT> struct RawGroup;
 #ifndef AGS_NT_LOADS
 #define AGS_NT_LOADS 0
 #endif
-template <typename V>
-__device__ __forceinline__ V stream_load(const V* p) {
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 stream_load(const uint4* p) {
 #if AGS_NT_LOADS
-    return __builtin_nontemporal_load(p);
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+#else
+    return *p;
+#endif
+}
+__device__ __forceinline__ float4 stream_load(const float4* p) {
+#if AGS_NT_LOADS
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                       __uint_as_float(v.w));
 #else
     return *p;
 #endif
@@ -416,9 +426,6 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
 template <typename GT, int KT, int RMODE, bool UPD>
 __global__ __launch_bounds__(kBlock, AGS_STEP_MIN_WAVES) void step_kernel(StepArgs a) {
     __shared__ float red[4][kBlock / 64];
-    __shared__ double shd[kBlock / 64];
-    __shared__ int shi[kBlock / 64];
-    __shared__ int sh_last;
     const Tile t = a.tiles[blockIdx.x];
     const int l = t.layer;
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
@@ -464,19 +471,17 @@ __global__ __launch_bounds__(kBlock, AGS_STEP_MIN_WAVES) void step_kernel(StepAr
         p.d = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
         p.s = (red[3][0] + red[3][1]) + (red[3][2] + red[3][3]);
         a.partials[blockIdx.x] = p;
-        // Publish the partial, then count the tile; the block that counts a
-        // layer's last tile reduces the layer.
-        __threadfence();
-        const LayerDev ld = a.layers[l];
-        const unsigned prev = atomicAdd(&a.layer_count[l], 1u);
-        sh_last = (prev + 1 == (unsigned)(ld.tile_end - ld.tile_begin));
     }
-    __syncthreads();
-    if (!sh_last) return;
-    __threadfence();
-    finalize_layer(a, l, shd);
+}
+
+// One block per layer.  The block that finishes the last layer (counted
+// with one device-scope atomic after a release fence) runs the global part.
+__global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
+    __shared__ double shd[kBlock / 64];
+    __shared__ int shi[kBlock / 64];
+    __shared__ int sh_last;
+    finalize_layer(a, blockIdx.x, shd);
     if (threadIdx.x == 0) {
-        a.layer_count[l] = 0u;  // ready for the next launch
         __threadfence();
         const unsigned prev = atomicAdd(a.done_count, 1u);
         sh_last = (prev + 1 == (unsigned)a.n_layers);
@@ -484,8 +489,8 @@ __global__ __launch_bounds__(kBlock, AGS_STEP_MIN_WAVES) void step_kernel(StepAr
     __syncthreads();
     if (!sh_last) return;
     __threadfence();
-    finalize_global(a, UPD, shd, shi);
-    if (threadIdx.x == 0) *a.done_count = 0u;
+    finalize_global(a, a.updated != 0, shd, shi);
+    if (threadIdx.x == 0) *a.done_count = 0u;  // ready for the next launch
 }
 
 // ----------------------------------------- correction and LARS update ---
@@ -635,6 +640,11 @@ hipError_t correct_t(const UpdateArgs& a, hipStream_t s) {
 hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s) {
     return dt == AGS_BF16 ? step_t<uint16_t>(a, n_tiles, update, s)
                           : step_t<float>(a, n_tiles, update, s);
+}
+
+hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(finalize_kernel, dim3(a.n_layers), dim3(kBlock), 0, s, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s) {
