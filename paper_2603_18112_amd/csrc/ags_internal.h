@@ -20,7 +20,12 @@ constexpr int kVec = 8;
 #endif
 constexpr int kTileElems = AGS_TILE_ELEMS;  // a multiple of kBlock * kVec
 static_assert(kTileElems % (kBlock * kVec) == 0, "tile must hold whole block rounds");
-constexpr int kCorrectBlocks = 2048;  // grid of the correction pass (grid-stride)
+#ifndef AGS_CORRECT_BLOCKS
+#define AGS_CORRECT_BLOCKS 512
+#endif
+// Grid of the correction pass (grid-stride over tiles): small, because on
+// most steps the pass only reads its flag and exits.
+constexpr int kCorrectBlocks = AGS_CORRECT_BLOCKS;
 
 struct Tile {
     int64_t begin;  // first element (flat index), a multiple of kVec

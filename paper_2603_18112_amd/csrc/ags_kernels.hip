@@ -28,11 +28,42 @@
 namespace ags {
 namespace {
 
+// Every byte of a step is touched once, so the replica rows are read with
+// non-temporal (streaming) loads: measured on MI355X, this cuts the step
+// kernel's time by about a quarter against ordinary loads.  AGS_NT_WM does
+// the same for the loads and stores of w and m.
+#ifndef AGS_NT_LOADS
+#define AGS_NT_LOADS 1
+#endif
+#ifndef AGS_NT_WM
+#define AGS_NT_WM 0
+#endif
+
 // ---------------------------------------------------------------- loads ---
 
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float4 wm_load(const float* p) {
+#if AGS_NT_WM
+    const f32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+#else
+    return *reinterpret_cast<const float4*>(p);
+#endif
+}
+
+__device__ __forceinline__ void wm_store(float* p, float4 v) {
+#if AGS_NT_WM
+    f32x4_t x = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(x, reinterpret_cast<f32x4_t*>(p));
+#else
+    *reinterpret_cast<float4*>(p) = v;
+#endif
+}
+
 __device__ __forceinline__ void load8(const float* __restrict__ p, float (&v)[kVec]) {
-    const float4 a = *reinterpret_cast<const float4*>(p);
-    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    const float4 a = wm_load(p);
+    const float4 b = wm_load(p + 4);
     v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
     v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
@@ -66,8 +97,8 @@ __device__ __forceinline__ void load_group(const GT* __restrict__ p, int n, floa
 }
 
 __device__ __forceinline__ void store8(float* __restrict__ p, const float (&v)[kVec]) {
-    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
-    *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+    wm_store(p, make_float4(v[0], v[1], v[2], v[3]));
+    wm_store(p + 4, make_float4(v[4], v[5], v[6], v[7]));
 }
 
 __device__ __forceinline__ void store_tail(float* __restrict__ p, int n, const float (&v)[kVec]) {
@@ -86,11 +117,7 @@ __device__ __forceinline__ void store_group(float* __restrict__ p, int n, const 
 // 16-byte vector for bf16, two for fp32.  Batches of loads are held in this
 // form so that a batch costs 64 VGPRs whatever the dtype.
 template <typename GT> struct RawGroup;
-// Replica rows are read once per step: AGS_NT_LOADS marks those loads
-// non-temporal (streaming) so they do not displace reused lines.
-#ifndef AGS_NT_LOADS
-#define AGS_NT_LOADS 0
-#endif
+
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 stream_load(const uint4* p) {
 #if AGS_NT_LOADS
@@ -151,7 +178,13 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
                                         int n, int K, int r, float invK, float (&gbar)[kVec],
                                         float (&dev)[kVec], float (&gr)[kVec]) {
     float g0[kVec], s1[kVec], s2[kVec];
-    load_group<GT, FULL>(g + idx, n, g0);
+    if (FULL) {
+        RawGroup<GT> r0;
+        r0.load(g + idx);
+        r0.widen(g0);
+    } else {
+        load_tail(g + idx, n, g0);
+    }
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
         s1[e] = 0.0f;
@@ -257,6 +290,28 @@ __device__ __forceinline__ T block_sum(T v, T* sh /* [kBlock / 64] */) {
     return (sh[0] + sh[1]) + (sh[2] + sh[3]);
 }
 
+struct Sum4 {
+    double w, g, d, s;
+};
+
+// Componentwise block sum of four values with one pair of barriers.
+__device__ __forceinline__ Sum4 block_sum4(Sum4 v, Sum4* sh /* [kBlock / 64] */) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    v.w = wave_sum(v.w);
+    v.g = wave_sum(v.g);
+    v.d = wave_sum(v.d);
+    v.s = wave_sum(v.s);
+    __syncthreads();
+    if (lane == 0) sh[wid] = v;
+    __syncthreads();
+    Sum4 r;
+    r.w = (sh[0].w + sh[1].w) + (sh[2].w + sh[3].w);
+    r.g = (sh[0].g + sh[1].g) + (sh[2].g + sh[3].g);
+    r.d = (sh[0].d + sh[1].d) + (sh[2].d + sh[3].d);
+    r.s = (sh[0].s + sh[1].s) + (sh[2].s + sh[3].s);
+    return r;
+}
+
 // The step's sensitivity is known before the step when Delta is infinite
 // by definition: a first step, or no positive finite previous norm.
 __device__ __forceinline__ bool surely_sensitive(double g_prev, long long step) {
@@ -266,26 +321,23 @@ __device__ __forceinline__ bool surely_sensitive(double g_prev, long long step) 
 // --------------------------------------------- last-block finalize ------
 
 // Per-layer statistics from the layer's tile partials (fp64, fixed order).
-__device__ void finalize_layer(const StepArgs& a, int l, double* shd) {
+__device__ void finalize_layer(const StepArgs& a, int l, Sum4* sh) {
     const LayerDev ld = a.layers[l];
-    double w = 0.0, g = 0.0, d = 0.0, s = 0.0;
+    Sum4 v = {0.0, 0.0, 0.0, 0.0};
     for (int i = ld.tile_begin + (int)threadIdx.x; i < ld.tile_end; i += kBlock) {
         const Partial p = a.partials[i];
-        w += (double)p.w;
-        g += (double)p.g;
-        d += (double)p.d;
-        s += (double)p.s;
+        v.w += (double)p.w;
+        v.g += (double)p.g;
+        v.d += (double)p.d;
+        v.s += (double)p.s;
     }
-    w = block_sum(w, shd);
-    g = block_sum(g, shd);
-    d = block_sum(d, shd);
-    s = block_sum(s, shd);
+    v = block_sum4(v, sh);
     if (threadIdx.x == 0) {
         ags_layer_stats& o = a.lstats[l];
-        o.w_sq = w;
-        o.g_sq = g;
-        o.var = d / (double)a.K;
-        o.gsmall_sq = s;
+        o.w_sq = v.w;
+        o.g_sq = v.g;
+        o.var = v.d / (double)a.K;
+        o.gsmall_sq = v.s;
     }
 }
 
@@ -298,18 +350,18 @@ __device__ void finalize_layer(const StepArgs& a, int l, double* shd) {
 // gradscale_l = min(sqrt(S_l) / (sqrt(G_l) + eps), s_max) (1 if a norm is 0)
 // for the steps that follow.  updated: the step kernel has already applied
 // the predicted coefficients, so record their difference for the correction.
-__device__ void finalize_global(const StepArgs& a, bool updated, double* shd, int* shi) {
+__device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* shi) {
     __shared__ int sh_sens, sh_pred;
     __shared__ long long sh_t;
-    double G = 0.0;
-    int nf = 0;
+    Sum4 v = {0.0, 0.0, 0.0, 0.0};
     for (int l = threadIdx.x; l < a.n_layers; l += kBlock) {
         const ags_layer_stats& o = a.lstats[l];
-        G += o.g_sq;
-        nf |= !(isfinite(o.w_sq) && isfinite(o.g_sq) && isfinite(o.var) && isfinite(o.gsmall_sq));
+        v.g += o.g_sq;
+        v.w += (isfinite(o.w_sq) && isfinite(o.g_sq) && isfinite(o.var) && isfinite(o.gsmall_sq)) ? 0.0 : 1.0;
     }
-    G = block_sum(G, shd);
-    nf = block_sum(nf, shi) != 0;
+    v = block_sum4(v, sh);
+    const double G = v.g;
+    int nf = v.w != 0.0;
     if (threadIdx.x == 0) {
         const double Gp = __hip_atomic_load(&a.state->g_prev, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const long long step = __hip_atomic_load(&a.state->step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -477,10 +529,10 @@ __global__ __launch_bounds__(kBlock, AGS_STEP_MIN_WAVES) void step_kernel(StepAr
 // One block per layer.  The block that finishes the last layer (counted
 // with one device-scope atomic after a release fence) runs the global part.
 __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
-    __shared__ double shd[kBlock / 64];
+    __shared__ Sum4 sh4[kBlock / 64];
     __shared__ int shi[kBlock / 64];
     __shared__ int sh_last;
-    finalize_layer(a, blockIdx.x, shd);
+    finalize_layer(a, blockIdx.x, sh4);
     if (threadIdx.x == 0) {
         __threadfence();
         const unsigned prev = atomicAdd(a.done_count, 1u);
@@ -489,7 +541,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
     __syncthreads();
     if (!sh_last) return;
     __threadfence();
-    finalize_global(a, a.updated != 0, shd, shi);
+    finalize_global(a, a.updated != 0, sh4, shi);
     if (threadIdx.x == 0) *a.done_count = 0u;  // ready for the next launch
 }
 
