@@ -38,6 +38,14 @@ namespace {
 #ifndef AGS_NT_WM
 #define AGS_NT_WM 0
 #endif
+#ifndef AGS_NT_STORES
+#define AGS_NT_STORES 0
+#endif
+#ifndef AGS_GROUP_UNROLL
+#define AGS_GROUP_UNROLL 1
+#endif
+#define AGS_PRAGMA(x) _Pragma(#x)
+#define AGS_UNROLL(n) AGS_PRAGMA(unroll n)
 
 // ---------------------------------------------------------------- loads ---
 
@@ -53,7 +61,7 @@ __device__ __forceinline__ float4 wm_load(const float* p) {
 }
 
 __device__ __forceinline__ void wm_store(float* p, float4 v) {
-#if AGS_NT_WM
+#if AGS_NT_WM || AGS_NT_STORES
     f32x4_t x = {v.x, v.y, v.z, v.w};
     __builtin_nontemporal_store(x, reinterpret_cast<f32x4_t*>(p));
 #else
@@ -495,7 +503,7 @@ __global__ __launch_bounds__(kBlock, AGS_STEP_MIN_WAVES) void step_kernel(StepAr
 
     float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f;
     const int nfull = t.count / kVec;
-#pragma unroll 1
+    AGS_UNROLL(AGS_GROUP_UNROLL)
     for (int c = threadIdx.x; c < nfull; c += kBlock)
         step_group<GT, KT, RMODE, UPD, true>(a, g, t.begin + (int64_t)c * kVec, kVec, K, ca, cb,
                                              sw, sg, sd, ss);
