@@ -37,13 +37,25 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+#: name -> (layout, K, gradient dtype, description).  The default is the
+#: headline workload; the others are the remaining configurations.
+WORKLOADS = {
+    "resnet50_k16_bf16": ("resnet50", 16, "bf16",
+                          "ResNet-50 ImageNet layout (161 tensors, 25,557,032 params), K=16 bf16"),
+    "tiny_cnn_k4_f32": ("tiny_cnn", 4, "f32", "tiny CNN layout (8 tensors, 24,234 params), K=4 fp32"),
+    "resnet18_cifar_k8_f32": ("resnet18_cifar", 8, "f32",
+                              "ResNet-18 CIFAR layout (62 tensors, 11,173,962 params), K=8 fp32"),
+    "vgg16_k8_f32": ("vgg16", 8, "f32", "VGG-16 layout (32 tensors, 138,357,544 params), K=8 fp32"),
+}
+for _k in (1, 2, 4, 8, 32, 64):
+    WORKLOADS[f"resnet50_k{_k}_bf16"] = ("resnet50", _k, "bf16",
+                                         f"ResNet-50 ImageNet layout, K={_k} bf16 (batch sweep)")
 WORKLOAD = "resnet50_k16_bf16"
 K = 16
-E_G = 2  # bytes per bf16 gradient element
+E_G = 2  # bytes per gradient element of the selected workload
 HYPER = dict(lr=0.1, momentum=0.9, weight_decay=5e-4, delta=0.5, eps=1e-8, s_max=0.0,
              trust_coef=1e-3, refresh_every=1, small_replica=0)
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2603_18112_amd", "csrc", "ags_kernels.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_resnet50_k16_bf16.txt")
 
 
 def log(msg):
@@ -58,30 +70,43 @@ def kernel_source_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(n_params: int):
-    """Per-launch algorithmic bytes of each pass and of the whole step.
+def algorithmic_bytes(n_params: int, mode: str = "ags"):
+    """Per-launch algorithmic bytes of each kernel and of the whole step.
 
-    The step kernel reads every replica once and reads and writes w and m
-    once: (K * 2 + 16) bytes per parameter, the step's own minimum.  The
-    second pass (the correction of a mispredicted sensitive bit) moves no
-    data on the steps timed here, whose bit is predicted correctly."""
+    A step reads every replica once and reads and writes w and m once:
+    (K * e_g + 16) bytes per parameter.  AGS and SGD steps do all of it in
+    the step kernel; the finalize kernel moves only per-tile partials, and
+    the correction pass moves nothing on the steps timed here, whose
+    sensitive bit is predicted right.  A LARS step reads the replicas and w
+    in the step kernel (and writes the replica mean when K * e_g > 8), then
+    reads w, m and the mean (or the replicas again) and writes w, m in the
+    update pass."""
     step = n_params * (K * E_G + 16)
-    return {"step": step, "finalize": 0, "second_pass": 0}
+    if mode != "lars":
+        return {"step": step, "finalize": 0, "second_pass": 0, "whole_step": step}
+    mat = K * E_G > 8
+    k0 = n_params * (K * E_G + 4 + (4 if mat else 0))
+    k2 = n_params * ((4 if mat else K * E_G) + 16)
+    return {"step": k0, "finalize": 0, "second_pass": k2, "whole_step": step}
 
 
-def read_traffic(kernel: str):
-    """HBM bytes per launch for ``kernel`` from the committed counter summary,
-    if it was taken on the current kernel source."""
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+
+
+def read_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of ``kernel`` from the committed counter summary
+    of ``workload``, if it was taken on the current kernel source."""
     try:
         kv = {}
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(workload)) as f:
             for line in f:
                 if "=" in line and not line.lstrip().startswith("#"):
                     k, v = line.split("=", 1)
                     kv[k.strip()] = v.strip()
         if kv.get("kernel_source_sha") != kernel_source_sha():
             return None
-        v = kv.get(f"{kernel}_bytes_per_launch")
+        v = kv.get(f"{kernel}_hbm_bytes_per_launch")
         return float(v) if v else None
     except OSError:
         return None
@@ -109,7 +134,8 @@ def copy_probe(torch, nbytes=1 << 30, reps=20):
 def cpu_baseline(layout, w0, grads_np, budget_s=12.0, max_steps=8):
     """The float64 oracle as it stands, single-threaded, on whole steps."""
     from oracle import OracleAGS
-    o = OracleAGS(layout.table(), layout.n_flat, K, w0, grad_dtype="bf16", **HYPER)
+    o = OracleAGS(layout.table(), layout.n_flat, K, w0, grad_dtype="bf16" if E_G == 2 else "f32",
+                  **HYPER)
     times = []
     t_start = time.time()
     while len(times) < max_steps and (time.time() - t_start) < budget_s:
@@ -126,6 +152,8 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(WORKLOADS))
+    ap.add_argument("--mode", default="ags", choices=["ags", "sgd", "lars"])
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -148,21 +176,24 @@ def main():
         print(json.dumps({"copy_probe_GBps": round(bw, 1), "bytes_per_copy": 2 * (1 << 30)}))
         return
 
+    global K, E_G
+    layout_name, K, gdt, desc = WORKLOADS[args.workload]
+    E_G = 2 if gdt == "bf16" else 4
     lib = ags.load_library()
     log(f"libags: {ags.library_path()}")
-    lay = layouts.get_layout("resnet50")
+    lay = layouts.get_layout(layout_name)
     N = lay.n_params
     t0 = time.time()
     w0 = synth.init_weights(lay, 0)
-    g_np = synth.replica_grads(lay, K, 0, 0, dtype="bf16")
-    log(f"inputs generated in {time.time() - t0:.1f}s: {N} params, K={K} bf16 "
+    g_np = synth.replica_grads(lay, K, 0, 0, dtype=gdt)
+    log(f"inputs generated in {time.time() - t0:.1f}s: {desc} "
         f"({g_np.nbytes / 1e9:.2f} GB of gradients)")
 
     w = torch.from_numpy(w0.copy()).cuda()
     m = torch.zeros_like(w)
-    g = torch.from_numpy(g_np.view(np.int16)).cuda()
+    g = torch.from_numpy(g_np.view(np.int16) if gdt == "bf16" else g_np).cuda()
     stream = torch.cuda.current_stream()
-    h = ags.AGS(lay.table(), w, m, K, grad_dtype="bf16", mode="ags", **HYPER)
+    h = ags.AGS(lay.table(), w, m, K, grad_dtype=gdt, mode=args.mode, **HYPER)
 
     for _ in range(args.warmup):
         h.step(g, stream)
@@ -194,14 +225,14 @@ def main():
                                          for i, n in enumerate(ags.KERNEL_NAMES)))
     s = h.read_stats()
 
-    ab = algorithmic_bytes(N)
-    value = ab["step"] / (ms_step * 1e-3) / 1e9
+    ab = algorithmic_bytes(N, args.mode)
+    value = ab["whole_step"] / (ms_step * 1e-3) / 1e9
     avg_ms = {n: kms[i] / ncalls for i, n in enumerate(ags.KERNEL_NAMES)}
     dom = max(avg_ms, key=avg_ms.get)
     achieved = ab[dom] / (avg_ms[dom] * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                "traffic": read_traffic(dom),
+                "traffic": read_traffic(args.workload, dom),
                 "algorithmic_bytes_per_launch": ab[dom],
                 "avg_launch_us": round(avg_ms[dom] * 1e3, 2)}
 
@@ -212,13 +243,14 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline: oracle on whole steps ...")
         sec, n = cpu_baseline(lay, w0, g_np)
-        cpu = {"value": round(ab["step"] / sec / 1e9, 3), "unit": "GB/s", "cores": 1,
+        cpu = {"value": round(ab["whole_step"] / sec / 1e9, 3), "unit": "GB/s", "cores": 1,
                "kind": "oracle", "sec_per_step": round(sec, 3),
-               "sample": f"median of {n} whole ResNet-50 K=16 bf16 steps, float64, 1 thread"}
+               "sample": f"median of {n} whole steps of {args.workload}, float64, 1 thread"}
         log(f"cpu baseline: {sec:.2f} s/step")
 
     out = {
-        "metric": "AGS step+stats GB/s & % HBM peak (ResNet-50 layout, K=16); steps/s",
+        "metric": ("AGS step+stats GB/s & % HBM peak (ResNet-50 layout, K=16); steps/s"
+                   if args.workload == WORKLOAD else f"AGS step+stats GB/s ({desc})"),
         "value": round(value, 1),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -230,11 +262,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": gdt,
         "data": "synthetic",
-        "config": {"workload": WORKLOAD, "layout": "resnet50", "tensors": lay.n_layers,
-                   "params": N, "K": K, "grad_dtype": "bf16", "param_dtype": "f32",
-                   "mode": "ags", "algorithmic_bytes_per_step": ab["step"],
+        "config": {"workload": args.workload, "layout": layout_name, "tensors": lay.n_layers,
+                   "params": N, "K": K, "grad_dtype": gdt, "param_dtype": "f32",
+                   "mode": args.mode, "algorithmic_bytes_per_step": ab["whole_step"],
                    "parallelism": "single GPU (K replicas stand in for K data-parallel workers)"},
         "kernel_us": {n: round(v * 1e3, 2) for n, v in avg_ms.items()},
         "device_copy_GBps": round(copy_bw, 1),
