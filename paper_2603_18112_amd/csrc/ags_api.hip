@@ -150,7 +150,10 @@ ags_status check_config(const ags_config* c, std::string& why) {
 
 int64_t count_tiles(const ags_config& c) {
     int64_t n = 0;
-    for (int32_t l = 0; l < c.n_layers; ++l) n += (c.layers[l].numel + ags::kTileElems - 1) / ags::kTileElems;
+    for (int32_t l = 0; l < c.n_layers; ++l) {
+        const int64_t te = ags::tile_elems_for(c.layers[l].numel);
+        n += (c.layers[l].numel + te - 1) / te;
+    }
     return n;
 }
 
@@ -446,10 +449,11 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
     for (int32_t l = 0; l < cfg->n_layers; ++l) {
         const ags_layer& L = cfg->layers[l];
         ldev[l].tile_begin = (int32_t)tiles.size();
-        for (int64_t o = 0; o < L.numel; o += ags::kTileElems) {
+        const int64_t te = ags::tile_elems_for(L.numel);
+        for (int64_t o = 0; o < L.numel; o += te) {
             Tile t;
             t.begin = L.offset + o;
-            t.count = (int32_t)((L.numel - o) < ags::kTileElems ? (L.numel - o) : ags::kTileElems);
+            t.count = (int32_t)((L.numel - o) < te ? (L.numel - o) : te);
             t.layer = l;
             tiles.push_back(t);
         }

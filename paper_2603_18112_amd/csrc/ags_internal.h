@@ -23,6 +23,17 @@ constexpr int kVec = 8;
 #endif
 constexpr int kTileElems = AGS_TILE_ELEMS;  // a multiple of kBlock * kVec
 static_assert(kTileElems % (kBlock * kVec) == 0, "tile must hold whole block rounds");
+// A layer is cut into at most this many tiles (bigger layers get tiles of a
+// multiple of kTileElems), so that the finalize block of any layer sums at
+// most four partials per thread.
+constexpr int64_t kMaxTilesPerLayer = 1024;
+
+// Elements per tile of a layer of numel elements.
+inline int64_t tile_elems_for(int64_t numel) {
+    const int64_t per = (int64_t)kTileElems * kMaxTilesPerLayer;
+    const int64_t mult = (numel + per - 1) / per;
+    return (int64_t)kTileElems * (mult > 0 ? mult : 1);
+}
 #ifndef AGS_CORRECT_BLOCKS
 #define AGS_CORRECT_BLOCKS 512
 #endif

@@ -15,13 +15,18 @@
 //                  so the update is a second pass with the final coefficients.
 //
 // The streaming kernels are HBM-bound (well under one flop per byte) and use
-// no matrix cores.  Every thread owns groups of 8 consecutive elements so
-// each replica row is read with one 16-byte load (bf16) or two (fp32), fully
-// coalesced across the wave.  Reductions run in a fixed order (per thread,
-// wave butterfly, the four waves in index order, then per layer in fp64 over
-// tiles in index order); the one atomic only counts finished layers, so a
-// step is bitwise reproducible.
+// no matrix cores.  Element mapping: a block works through its tile in
+// rounds of 2048 elements; in a round, wave w owns elements [512w, 512w+512)
+// and lane l of it owns two halves of 4 elements, [4l, 4l+4) and
+// [256+4l, 256+4l+4).  So every load or store instruction of a wave covers
+// one contiguous span -- 1 KiB of fp32 (w, m, fp32 replicas) or 512 B of
+// bf16 -- and no cache line is split between two instructions.  Reductions
+// run in a fixed order (per thread, wave butterfly, the four waves in index
+// order, then per layer in fp64 over tiles in index order); the one atomic
+// only counts finished layers, so a step is bitwise reproducible.
 #include <math.h>
+
+#include <type_traits>
 
 #include "ags_internal.h"
 
@@ -30,111 +35,45 @@ namespace {
 
 // Every byte of a step is touched once, so the replica rows are read with
 // non-temporal (streaming) loads: measured on MI355X, this cuts the step
-// kernel's time by about a quarter against ordinary loads.  AGS_NT_WM does
-// the same for the loads and stores of w and m.
+// kernel's time by about a quarter against ordinary loads (w and m keep
+// ordinary loads and stores, which measured faster than streaming ones).
 #ifndef AGS_NT_LOADS
 #define AGS_NT_LOADS 1
 #endif
-#ifndef AGS_NT_WM
-#define AGS_NT_WM 0
+// Replicas whose loads are issued together before any is used (a batch):
+// 8 bf16 replicas or 2 fp32 replicas per batch measured best.
+#ifndef AGS_BATCH_BF16
+#define AGS_BATCH_BF16 8
 #endif
-#ifndef AGS_NT_STORES
-#define AGS_NT_STORES 0
+#ifndef AGS_BATCH_F32
+#define AGS_BATCH_F32 2
 #endif
-#ifndef AGS_GROUP_UNROLL
-#define AGS_GROUP_UNROLL 1
+// From this many replicas on, w and m are loaded after the replica loop
+// rather than before it, so that they do not hold registers through it.
+#ifndef AGS_LATE_WM_K
+#define AGS_LATE_WM_K 1 << 30
 #endif
-#define AGS_PRAGMA(x) _Pragma(#x)
-#define AGS_UNROLL(n) AGS_PRAGMA(unroll n)
+
+constexpr int kHalf = 4;                    // elements per half group
+constexpr int kHalfStride = 64 * kHalf;     // 256: a lane's second half
+constexpr int kWaveSpan = 2 * kHalfStride;  // 512 elements per wave per round
+constexpr int kRound = kBlock * kVec;       // 2048 elements per block per round
+static_assert(kRound == (kBlock / 64) * kWaveSpan, "round layout");
 
 // ---------------------------------------------------------------- loads ---
 
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ float4 wm_load(const float* p) {
-#if AGS_NT_WM
-    const f32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p));
-    return make_float4(v.x, v.y, v.z, v.w);
-#else
-    return *reinterpret_cast<const float4*>(p);
-#endif
-}
-
-__device__ __forceinline__ void wm_store(float* p, float4 v) {
-#if AGS_NT_WM || AGS_NT_STORES
-    f32x4_t x = {v.x, v.y, v.z, v.w};
-    __builtin_nontemporal_store(x, reinterpret_cast<f32x4_t*>(p));
-#else
-    *reinterpret_cast<float4*>(p) = v;
-#endif
-}
-
-__device__ __forceinline__ void load8(const float* __restrict__ p, float (&v)[kVec]) {
-    const float4 a = wm_load(p);
-    const float4 b = wm_load(p + 4);
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-}
-
-// bf16 -> fp32 is exact: a bf16 value is the upper half of an fp32.
-__device__ __forceinline__ void load8(const uint16_t* __restrict__ p, float (&v)[kVec]) {
-    const uint4 a = *reinterpret_cast<const uint4*>(p);
-    v[0] = __uint_as_float(a.x << 16); v[1] = __uint_as_float(a.x & 0xffff0000u);
-    v[2] = __uint_as_float(a.y << 16); v[3] = __uint_as_float(a.y & 0xffff0000u);
-    v[4] = __uint_as_float(a.z << 16); v[5] = __uint_as_float(a.z & 0xffff0000u);
-    v[6] = __uint_as_float(a.w << 16); v[7] = __uint_as_float(a.w & 0xffff0000u);
-}
-
-__device__ __forceinline__ float load1(const float* __restrict__ p) { return *p; }
-__device__ __forceinline__ float load1(const uint16_t* __restrict__ p) {
-    return __uint_as_float(static_cast<uint32_t>(*p) << 16);
-}
-
-// Elements [0, n) of a group (n < 8, the ragged end of a layer); the rest
-// are 0 and contribute nothing to any sum.
-template <typename T>
-__device__ __forceinline__ void load_tail(const T* __restrict__ p, int n, float (&v)[kVec]) {
-#pragma unroll
-    for (int e = 0; e < kVec; ++e) v[e] = (e < n) ? load1(p + e) : 0.0f;
-}
-
-template <typename GT, bool FULL>
-__device__ __forceinline__ void load_group(const GT* __restrict__ p, int n, float (&v)[kVec]) {
-    if (FULL) load8(p, v);
-    else load_tail(p, n, v);
-}
-
-__device__ __forceinline__ void store8(float* __restrict__ p, const float (&v)[kVec]) {
-    wm_store(p, make_float4(v[0], v[1], v[2], v[3]));
-    wm_store(p + 4, make_float4(v[4], v[5], v[6], v[7]));
-}
-
-__device__ __forceinline__ void store_tail(float* __restrict__ p, int n, const float (&v)[kVec]) {
-#pragma unroll
-    for (int e = 0; e < kVec; ++e)
-        if (e < n) p[e] = v[e];
-}
-
-template <bool FULL>
-__device__ __forceinline__ void store_group(float* __restrict__ p, int n, const float (&v)[kVec]) {
-    if (FULL) store8(p, v);
-    else store_tail(p, n, v);
-}
-
-// A group of 8 replica values as loaded, before widening to fp32: one
-// 16-byte vector for bf16, two for fp32.  Batches of loads are held in this
-// form so that a batch costs 64 VGPRs whatever the dtype.
-template <typename GT> struct RawGroup;
-
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ uint4 stream_load(const uint4* p) {
+
+__device__ __forceinline__ uint2 stream_load(const uint2* p) {
 #if AGS_NT_LOADS
-    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
-    return make_uint4(v.x, v.y, v.z, v.w);
+    const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+    return make_uint2(v.x, v.y);
 #else
     return *p;
 #endif
 }
+
 __device__ __forceinline__ float4 stream_load(const float4* p) {
 #if AGS_NT_LOADS
     const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
@@ -145,23 +84,82 @@ __device__ __forceinline__ float4 stream_load(const float4* p) {
 #endif
 }
 
+// bf16 -> fp32 is exact: a bf16 value is the upper half of an fp32.
+__device__ __forceinline__ float bf16_lo(unsigned int x) { return __uint_as_float(x << 16); }
+__device__ __forceinline__ float bf16_hi(unsigned int x) { return __uint_as_float(x & 0xffff0000u); }
+
+__device__ __forceinline__ float load1(const float* __restrict__ p) { return *p; }
+__device__ __forceinline__ float load1(const uint16_t* __restrict__ p) {
+    return __uint_as_float(static_cast<uint32_t>(*p) << 16);
+}
+
+// A group of a lane: halves [p, p+4) and [p+256, p+260).  FULL groups are
+// two 16-byte (fp32) loads; the ragged end of a layer takes element loads
+// for the first n0 and n1 elements of the halves, the rest being 0 (which
+// adds nothing to any sum).
+template <bool FULL>
+__device__ __forceinline__ void load_f32(const float* __restrict__ p, int n0, int n1,
+                                         float (&v)[kVec]) {
+    if (FULL) {
+        const float4 a = *reinterpret_cast<const float4*>(p);
+        const float4 b = *reinterpret_cast<const float4*>(p + kHalfStride);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    } else {
+#pragma unroll
+        for (int e = 0; e < kHalf; ++e) {
+            v[e] = (e < n0) ? p[e] : 0.0f;
+            v[kHalf + e] = (e < n1) ? p[kHalfStride + e] : 0.0f;
+        }
+    }
+}
+
+template <bool FULL>
+__device__ __forceinline__ void store_f32(float* __restrict__ p, int n0, int n1,
+                                          const float (&v)[kVec]) {
+    if (FULL) {
+        *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(p + kHalfStride) = make_float4(v[4], v[5], v[6], v[7]);
+    } else {
+#pragma unroll
+        for (int e = 0; e < kHalf; ++e) {
+            if (e < n0) p[e] = v[e];
+            if (e < n1) p[kHalfStride + e] = v[kHalf + e];
+        }
+    }
+}
+
+template <typename GT>
+__device__ __forceinline__ void load_tail(const GT* __restrict__ p, int n0, int n1,
+                                          float (&v)[kVec]) {
+#pragma unroll
+    for (int e = 0; e < kHalf; ++e) {
+        v[e] = (e < n0) ? load1(p + e) : 0.0f;
+        v[kHalf + e] = (e < n1) ? load1(p + kHalfStride + e) : 0.0f;
+    }
+}
+
+// A full group of replica values as loaded, before widening to fp32: two
+// 8-byte vectors for bf16, two 16-byte vectors for fp32.
+template <typename GT> struct RawGroup;
 template <> struct RawGroup<uint16_t> {
-    uint4 v;
+    static constexpr int kBatch = AGS_BATCH_BF16;
+    uint2 a, b;
     __device__ __forceinline__ void load(const uint16_t* __restrict__ p) {
-        v = stream_load(reinterpret_cast<const uint4*>(p));
+        a = stream_load(reinterpret_cast<const uint2*>(p));
+        b = stream_load(reinterpret_cast<const uint2*>(p + kHalfStride));
     }
     __device__ __forceinline__ void widen(float (&o)[kVec]) const {
-        o[0] = __uint_as_float(v.x << 16); o[1] = __uint_as_float(v.x & 0xffff0000u);
-        o[2] = __uint_as_float(v.y << 16); o[3] = __uint_as_float(v.y & 0xffff0000u);
-        o[4] = __uint_as_float(v.z << 16); o[5] = __uint_as_float(v.z & 0xffff0000u);
-        o[6] = __uint_as_float(v.w << 16); o[7] = __uint_as_float(v.w & 0xffff0000u);
+        o[0] = bf16_lo(a.x); o[1] = bf16_hi(a.x); o[2] = bf16_lo(a.y); o[3] = bf16_hi(a.y);
+        o[4] = bf16_lo(b.x); o[5] = bf16_hi(b.x); o[6] = bf16_lo(b.y); o[7] = bf16_hi(b.y);
     }
 };
 template <> struct RawGroup<float> {
+    static constexpr int kBatch = AGS_BATCH_F32;
     float4 a, b;
     __device__ __forceinline__ void load(const float* __restrict__ p) {
         a = stream_load(reinterpret_cast<const float4*>(p));
-        b = stream_load(reinterpret_cast<const float4*>(p + 4));
+        b = stream_load(reinterpret_cast<const float4*>(p + kHalfStride));
     }
     __device__ __forceinline__ void widen(float (&o)[kVec]) const {
         o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
@@ -183,15 +181,16 @@ template <> struct RawGroup<float> {
 
 template <typename GT, int KT, int RMODE, bool FULL>
 __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride, int64_t idx,
-                                        int n, int K, int r, float invK, float (&gbar)[kVec],
-                                        float (&dev)[kVec], float (&gr)[kVec]) {
+                                        int n0, int n1, int K, int r, float invK,
+                                        float (&gbar)[kVec], float (&dev)[kVec],
+                                        float (&gr)[kVec]) {
     float g0[kVec], s1[kVec], s2[kVec];
     if (FULL) {
         RawGroup<GT> r0;
         r0.load(g + idx);
         r0.widen(g0);
     } else {
-        load_tail(g + idx, n, g0);
+        load_tail(g + idx, n0, n1, g0);
     }
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
@@ -209,13 +208,10 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
         }
     };
     if constexpr (KT > 0 && FULL) {
-        // Batches of 64 bytes of replica data per lane (16 bf16 or 8 fp32
-        // replicas): every load of a batch is issued before any of its
-        // values is used.  The first batch holds replicas 1..KB-1 (replica 0
-        // is the shift); later batches run as a loop so that only one batch
-        // is in registers at a time.
-        constexpr int KBMAX = 64 / (int)sizeof(RawGroup<GT>);
-        constexpr int KB = KT < KBMAX ? KT : KBMAX;
+        // Every load of a batch is issued before any of its values is used.
+        // The first batch holds replicas 1..KB-1 (replica 0 is the shift);
+        // later batches run as a loop, one batch in registers at a time.
+        constexpr int KB = KT < RawGroup<GT>::kBatch ? KT : RawGroup<GT>::kBatch;
         static_assert(KT % KB == 0, "K must be a multiple of the batch");
         {
             RawGroup<GT> x[KB];
@@ -248,14 +244,28 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
         for (; k + 3 < K; k += 4) {
             float x[4][kVec];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) load_group<GT, FULL>(g + (int64_t)(k + j) * stride + idx, n, x[j]);
+            for (int j = 0; j < 4; ++j) {
+                if (FULL) {
+                    RawGroup<GT> q;
+                    q.load(g + (int64_t)(k + j) * stride + idx);
+                    q.widen(x[j]);
+                } else {
+                    load_tail(g + (int64_t)(k + j) * stride + idx, n0, n1, x[j]);
+                }
+            }
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc(k + j, x[j]);
         }
 #pragma unroll 1
         for (; k < K; ++k) {
             float x[kVec];
-            load_group<GT, FULL>(g + (int64_t)k * stride + idx, n, x);
+            if (FULL) {
+                RawGroup<GT> q;
+                q.load(g + (int64_t)k * stride + idx);
+                q.widen(x);
+            } else {
+                load_tail(g + (int64_t)k * stride + idx, n0, n1, x);
+            }
             acc(k, x);
         }
     }
@@ -264,6 +274,21 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
         gbar[e] = fmaf(s1[e], invK, g0[e]);
         const float t = s1[e] * invK;
         dev[e] = fmaxf(fmaf(-t, s1[e], s2[e]), 0.0f);
+    }
+}
+
+// The groups of this thread in a tile of `count` elements starting at
+// `begin`: calls f(idx, n0, n1, full) for every group that holds data.
+template <typename F>
+__device__ __forceinline__ void for_each_group(int64_t begin, int count, F&& f) {
+    const int pos = (int)(threadIdx.x >> 6) * kWaveSpan + (int)(threadIdx.x & 63) * kHalf;
+#pragma unroll 1
+    for (int r0 = 0; r0 < count; r0 += kRound) {
+        const int off = r0 + pos;
+        const int n0 = min(max(count - off, 0), kHalf);
+        const int n1 = min(max(count - off - kHalfStride, 0), kHalf);
+        if (n1 == kHalf) f(begin + off, kHalf, kHalf, std::true_type{});
+        else if (n0 > 0) f(begin + off, n0, n1, std::false_type{});
     }
 }
 
@@ -326,19 +351,47 @@ __device__ __forceinline__ bool surely_sensitive(double g_prev, long long step) 
     return step == 0 || !(g_prev > 0.0) || !isfinite(g_prev);
 }
 
-// --------------------------------------------- last-block finalize ------
+// ------------------------------------------------------- finalize -------
 
 // Per-layer statistics from the layer's tile partials (fp64, fixed order).
 __device__ void finalize_layer(const StepArgs& a, int l, Sum4* sh) {
     const LayerDev ld = a.layers[l];
-    Sum4 v = {0.0, 0.0, 0.0, 0.0};
-    for (int i = ld.tile_begin + (int)threadIdx.x; i < ld.tile_end; i += kBlock) {
-        const Partial p = a.partials[i];
-        v.w += (double)p.w;
-        v.g += (double)p.g;
-        v.d += (double)p.d;
-        v.s += (double)p.s;
+    // Four independent accumulators per thread (tiles i, i + 256, i + 512,
+    // i + 768, then the next 1024), combined in a fixed order: long layers
+    // keep four loads in flight per thread instead of one.
+    constexpr int U = 4;
+    Sum4 acc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc[u] = {0.0, 0.0, 0.0, 0.0};
+    int i = ld.tile_begin + (int)threadIdx.x;
+    for (; i + (U - 1) * kBlock < ld.tile_end; i += U * kBlock) {
+        Partial p[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) p[u] = a.partials[i + u * kBlock];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            acc[u].w += (double)p[u].w;
+            acc[u].g += (double)p[u].g;
+            acc[u].d += (double)p[u].d;
+            acc[u].s += (double)p[u].s;
+        }
     }
+#pragma unroll
+    for (int u = 0; u < U - 1; ++u) {
+        const int j = i + u * kBlock;
+        if (j < ld.tile_end) {
+            const Partial p = a.partials[j];
+            acc[u].w += (double)p.w;
+            acc[u].g += (double)p.g;
+            acc[u].d += (double)p.d;
+            acc[u].s += (double)p.s;
+        }
+    }
+    Sum4 v;
+    v.w = (acc[0].w + acc[1].w) + (acc[2].w + acc[3].w);
+    v.g = (acc[0].g + acc[1].g) + (acc[2].g + acc[3].g);
+    v.d = (acc[0].d + acc[1].d) + (acc[2].d + acc[3].d);
+    v.s = (acc[0].s + acc[1].s) + (acc[2].s + acc[3].s);
     v = block_sum4(v, sh);
     if (threadIdx.x == 0) {
         ags_layer_stats& o = a.lstats[l];
@@ -451,13 +504,22 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
 
 template <typename GT, int KT, int RMODE, bool UPD, bool FULL>
 __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restrict__ g,
-                                           int64_t idx, int n, int K, float ca, float cb,
-                                           float& sw, float& sg, float& sd, float& ss) {
+                                           int64_t idx, int n0, int n1, int K, float ca,
+                                           float cb, float& sw, float& sg, float& sd,
+                                           float& ss) {
+    constexpr bool late_wm = KT >= AGS_LATE_WM_K;
     float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
-    load_group<float, FULL>(a.w + idx, n, wv);
-    if (UPD) load_group<float, FULL>(a.m + idx, n, mv);
-    moments<GT, KT, RMODE, FULL>(g, a.stride, idx, n, K, a.small_replica, a.invK, gb, dv, gr);
-    if (!UPD && a.gbar) store_group<FULL>(a.gbar + idx, n, gb);
+    if (!late_wm) {
+        load_f32<FULL>(a.w + idx, n0, n1, wv);
+        if (UPD) load_f32<FULL>(a.m + idx, n0, n1, mv);
+    }
+    moments<GT, KT, RMODE, FULL>(g, a.stride, idx, n0, n1, K, a.small_replica, a.invK, gb, dv,
+                                 gr);
+    if (late_wm) {
+        load_f32<FULL>(a.w + idx, n0, n1, wv);
+        if (UPD) load_f32<FULL>(a.m + idx, n0, n1, mv);
+    }
+    if (!UPD && a.gbar) store_f32<FULL>(a.gbar + idx, n0, n1, gb);
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
         sw = fmaf(wv[e], wv[e], sw);
@@ -475,16 +537,13 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
             mv[e] = fmaf(a.momentum, mv[e], d);
             wv[e] = fmaf(-a.lr, mv[e], wv[e]);
         }
-        store_group<FULL>(a.w + idx, n, wv);
-        store_group<FULL>(a.m + idx, n, mv);
+        store_f32<FULL>(a.w + idx, n0, n1, wv);
+        store_f32<FULL>(a.m + idx, n0, n1, mv);
     }
 }
 
-#ifndef AGS_STEP_MIN_WAVES
-#define AGS_STEP_MIN_WAVES 1
-#endif
 template <typename GT, int KT, int RMODE, bool UPD>
-__global__ __launch_bounds__(kBlock, AGS_STEP_MIN_WAVES) void step_kernel(StepArgs a) {
+__global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     __shared__ float red[4][kBlock / 64];
     const Tile t = a.tiles[blockIdx.x];
     const int l = t.layer;
@@ -502,15 +561,10 @@ __global__ __launch_bounds__(kBlock, AGS_STEP_MIN_WAVES) void step_kernel(StepAr
     }
 
     float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f;
-    const int nfull = t.count / kVec;
-    AGS_UNROLL(AGS_GROUP_UNROLL)
-    for (int c = threadIdx.x; c < nfull; c += kBlock)
-        step_group<GT, KT, RMODE, UPD, true>(a, g, t.begin + (int64_t)c * kVec, kVec, K, ca, cb,
-                                             sw, sg, sd, ss);
-    const int rem = t.count - nfull * kVec;
-    if (rem > 0 && (int)threadIdx.x == nfull % kBlock)
-        step_group<GT, KT, RMODE, UPD, false>(a, g, t.begin + (int64_t)nfull * kVec, rem, K, ca,
-                                              cb, sw, sg, sd, ss);
+    for_each_group(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
+        step_group<GT, KT, RMODE, UPD, decltype(full)::value>(a, g, idx, n0, n1, K, ca, cb, sw,
+                                                              sg, sd, ss);
+    });
 
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
     sw = wave_sum(sw);
@@ -559,19 +613,19 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
 // c = a_true - a_predicted of the layer (0 for most layers).
 template <typename GT, int KT, bool FULL>
 __device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __restrict__ g,
-                                              int64_t idx, int n, int K, float c) {
+                                              int64_t idx, int n0, int n1, int K, float c) {
     float gb[kVec], dv[kVec], gr[kVec], wv[kVec], mv[kVec];
-    load_group<float, FULL>(a.w + idx, n, wv);
-    load_group<float, FULL>(a.m + idx, n, mv);
-    moments<GT, KT, 0, FULL>(g, a.stride, idx, n, K, 0, a.invK, gb, dv, gr);
+    load_f32<FULL>(a.w + idx, n0, n1, wv);
+    load_f32<FULL>(a.m + idx, n0, n1, mv);
+    moments<GT, KT, 0, FULL>(g, a.stride, idx, n0, n1, K, 0, a.invK, gb, dv, gr);
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
         const float cg = c * gb[e];
         mv[e] += cg;
         wv[e] = fmaf(-a.lr, cg, wv[e]);
     }
-    store_group<FULL>(a.w + idx, n, wv);
-    store_group<FULL>(a.m + idx, n, mv);
+    store_f32<FULL>(a.w + idx, n0, n1, wv);
+    store_f32<FULL>(a.m + idx, n0, n1, mv);
 }
 
 template <typename GT, int KT>
@@ -584,13 +638,9 @@ __global__ __launch_bounds__(kBlock) void correct_kernel(UpdateArgs a) {
         const Tile t = a.tiles[ti];
         const float c = a.corr[t.layer];
         if (c == 0.0f) continue;
-        const int nfull = t.count / kVec;
-#pragma unroll 1
-        for (int q = threadIdx.x; q < nfull; q += kBlock)
-            correct_group<GT, KT, true>(a, g, t.begin + (int64_t)q * kVec, kVec, K, c);
-        const int rem = t.count - nfull * kVec;
-        if (rem > 0 && (int)threadIdx.x == nfull % kBlock)
-            correct_group<GT, KT, false>(a, g, t.begin + (int64_t)nfull * kVec, rem, K, c);
+        for_each_group(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
+            correct_group<GT, KT, decltype(full)::value>(a, g, idx, n0, n1, K, c);
+        });
     }
 }
 
@@ -600,15 +650,16 @@ __global__ __launch_bounds__(kBlock) void correct_kernel(UpdateArgs a) {
 // recomputed from them by the same code.
 template <typename GT, int KT, bool RECOMP, bool FULL>
 __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __restrict__ g,
-                                             int64_t idx, int n, int K, float ca, float cb) {
+                                             int64_t idx, int n0, int n1, int K, float ca,
+                                             float cb) {
     float gb[kVec], wv[kVec], mv[kVec];
-    load_group<float, FULL>(a.w + idx, n, wv);
-    load_group<float, FULL>(a.m + idx, n, mv);
+    load_f32<FULL>(a.w + idx, n0, n1, wv);
+    load_f32<FULL>(a.m + idx, n0, n1, mv);
     if (RECOMP) {
         float dv[kVec], gr[kVec];
-        moments<GT, KT, 0, FULL>(g, a.stride, idx, n, K, 0, a.invK, gb, dv, gr);
+        moments<GT, KT, 0, FULL>(g, a.stride, idx, n0, n1, K, 0, a.invK, gb, dv, gr);
     } else {
-        load_group<float, FULL>(a.gbar + idx, n, gb);
+        load_f32<FULL>(a.gbar + idx, n0, n1, gb);
     }
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
@@ -616,8 +667,8 @@ __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __re
         mv[e] = fmaf(a.momentum, mv[e], d);
         wv[e] = fmaf(-a.lr, mv[e], wv[e]);
     }
-    store_group<FULL>(a.w + idx, n, wv);
-    store_group<FULL>(a.m + idx, n, mv);
+    store_f32<FULL>(a.w + idx, n0, n1, wv);
+    store_f32<FULL>(a.m + idx, n0, n1, mv);
 }
 
 template <typename GT, int KT, bool RECOMP>
@@ -626,13 +677,9 @@ __global__ __launch_bounds__(kBlock) void update_kernel(UpdateArgs a) {
     const float2 ab = a.coef[t.layer];
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
-    const int nfull = t.count / kVec;
-#pragma unroll 1
-    for (int c = threadIdx.x; c < nfull; c += kBlock)
-        update_group<GT, KT, RECOMP, true>(a, g, t.begin + (int64_t)c * kVec, kVec, K, ab.x, ab.y);
-    const int rem = t.count - nfull * kVec;
-    if (rem > 0 && (int)threadIdx.x == nfull % kBlock)
-        update_group<GT, KT, RECOMP, false>(a, g, t.begin + (int64_t)nfull * kVec, rem, K, ab.x, ab.y);
+    for_each_group(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
+        update_group<GT, KT, RECOMP, decltype(full)::value>(a, g, idx, n0, n1, K, ab.x, ab.y);
+    });
 }
 
 // ----------------------------------------------------------- dispatch ---
