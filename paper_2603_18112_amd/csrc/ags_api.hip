@@ -32,6 +32,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // that a read-back is one copy.
 struct WsLayout {
     size_t gbar = 0, tiles = 0, partials = 0, ldev = 0, coef = 0, corr = 0, counters = 0;
+    size_t chunks = 0, chunk_sums = 0, chunk_count = 0;
     size_t counters_bytes = 0;  // finished-layer counter, correction flag
     size_t lstats = 0, gstats = 0, gradscale = 0, state = 0, end = 0;
     size_t rec_bytes = 0;    // lstats .. gstats end
@@ -47,7 +48,7 @@ bool materialize_gbar(const ags_config& c) {
     return c.mode == AGS_MODE_LARS && (size_t)c.K * elem_bytes(c.grad_dtype) > 8;
 }
 
-WsLayout ws_layout(const ags_config& c, int64_t n_tiles) {
+WsLayout ws_layout(const ags_config& c, int64_t n_tiles, int64_t n_chunks) {
     WsLayout w;
     size_t p = 0;
     const size_t L = (size_t)c.n_layers;
@@ -61,6 +62,12 @@ WsLayout ws_layout(const ags_config& c, int64_t n_tiles) {
     p = align_up(p + L * sizeof(LayerDev));
     w.coef = p;
     p = align_up(p + L * sizeof(float2));
+    w.chunks = p;
+    p = align_up(p + (size_t)n_chunks * sizeof(ags::FinChunk));
+    w.chunk_sums = p;
+    p = align_up(p + (size_t)n_chunks * sizeof(ags::ChunkSum));
+    w.chunk_count = p;
+    p = align_up(p + L * sizeof(unsigned));
     w.corr = p;
     p = align_up(p + L * sizeof(float));
     w.counters = p;
@@ -157,6 +164,16 @@ int64_t count_tiles(const ags_config& c) {
     return n;
 }
 
+int64_t count_chunks(const ags_config& c) {
+    int64_t n = 0;
+    for (int32_t l = 0; l < c.n_layers; ++l) {
+        const int64_t te = ags::tile_elems_for(c.layers[l].numel);
+        const int64_t tiles = (c.layers[l].numel + te - 1) / te;
+        n += (tiles + ags::kFinTilesPerChunk - 1) / ags::kFinTilesPerChunk;
+    }
+    return n;
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Is [p, p + bytes) inside one device allocation of the current device?
@@ -214,6 +231,7 @@ struct ags_handle {
     int device = 0;
     double lr = 0;
     int64_t n_tiles = 0;
+    int64_t n_chunks = 0;
     int64_t grad_extent = 0;  // elements of one replica that are read
     bool materialize = false;
     WsLayout wl;
@@ -341,12 +359,15 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.corr_flag = h->corr_flag();
     sa.updated = fused ? 1 : 0;
     sa.done_count = h->done_count();
+    sa.chunks = reinterpret_cast<const ags::FinChunk*>(h->ws + h->wl.chunks);
+    sa.chunk_sums = reinterpret_cast<ags::ChunkSum*>(h->ws + h->wl.chunk_sums);
+    sa.layer_chunk_count = reinterpret_cast<unsigned*>(h->ws + h->wl.chunk_count);
     sa.lstats = h->lstats();
     sa.gstats = h->gstats();
     hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s);
     if (e != hipSuccess) return h->hip_fail(e, "step kernel launch");
     if (prof) (void)hipEventRecord(ev[1], s);
-    e = ags::launch_finalize(sa, s);
+    e = ags::launch_finalize(sa, (int)h->n_chunks, s);
     if (e != hipSuccess) return h->hip_fail(e, "finalize kernel launch");
     if (prof) (void)hipEventRecord(ev[2], s);
 
@@ -411,7 +432,7 @@ ags_status ags_workspace_bytes(const ags_config* cfg, size_t* out_bytes) {
         g_thread_error = "out_bytes is NULL";
         return AGS_E_ARG;
     }
-    *out_bytes = ws_layout(*cfg, count_tiles(*cfg)).end;
+    *out_bytes = ws_layout(*cfg, count_tiles(*cfg), count_chunks(*cfg)).end;
     return AGS_OK;
 }
 
@@ -445,6 +466,7 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
     // Host-side tables.
     std::vector<Tile> tiles;
     std::vector<LayerDev> ldev(cfg->n_layers);
+    std::vector<ags::FinChunk> chunks;
     tiles.reserve((size_t)n_tiles);
     for (int32_t l = 0; l < cfg->n_layers; ++l) {
         const ags_layer& L = cfg->layers[l];
@@ -459,6 +481,16 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         }
         ldev[l].tile_end = (int32_t)tiles.size();
         ldev[l].flags = L.flags;
+        ldev[l].chunk_begin = (int32_t)chunks.size();
+        for (int32_t tb = ldev[l].tile_begin; tb < ldev[l].tile_end; tb += ags::kFinTilesPerChunk) {
+            ags::FinChunk ch;
+            ch.layer = l;
+            ch.tile_begin = tb;
+            ch.tile_end = std::min<int32_t>(tb + ags::kFinTilesPerChunk, ldev[l].tile_end);
+            ch.pad_ = 0;
+            chunks.push_back(ch);
+        }
+        ldev[l].chunk_end = (int32_t)chunks.size();
         ldev[l].pad_ = 0;
     }
     int64_t extent = 0;
@@ -466,7 +498,7 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         extent = std::max<int64_t>(extent, cfg->layers[l].offset + cfg->layers[l].numel);
 
     // Workspace size and the byte cap, still before any HIP call.
-    const WsLayout wl = ws_layout(*cfg, n_tiles);
+    const WsLayout wl = ws_layout(*cfg, n_tiles, count_chunks(*cfg));
     const size_t cap = workspace_cap();
     if (wl.end > cap) {
         char buf[200];
@@ -504,6 +536,7 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
     h->device = dev;
     h->lr = cfg->lr;
     h->n_tiles = n_tiles;
+    h->n_chunks = (int64_t)chunks.size();
     h->grad_extent = extent;
     h->materialize = materialize_gbar(*cfg);
     h->wl = wl;
@@ -536,11 +569,14 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
     } up[] = {
         {h->wl.tiles, tiles.data(), tiles.size() * sizeof(Tile)},
         {h->wl.ldev, ldev.data(), ldev.size() * sizeof(LayerDev)},
+        {h->wl.chunks, chunks.data(), chunks.size() * sizeof(ags::FinChunk)},
         {h->wl.gradscale, ones.data(), ones.size() * sizeof(double)},
         {h->wl.state, &ds, sizeof ds},
     };
     e = hipMemsetAsync(h->ws + h->wl.lstats, 0, h->wl.rec_bytes, s);
     if (e == hipSuccess) e = hipMemsetAsync(h->ws + h->wl.counters, 0, h->wl.counters_bytes, s);
+    if (e == hipSuccess)
+        e = hipMemsetAsync(h->ws + h->wl.chunk_count, 0, (size_t)cfg->n_layers * sizeof(unsigned), s);
     for (const auto& u : up) {
         if (e != hipSuccess) break;
         e = hipMemcpyAsync(h->ws + u.off, u.src, u.bytes, hipMemcpyHostToDevice, s);

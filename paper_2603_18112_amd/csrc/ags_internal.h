@@ -24,9 +24,15 @@ constexpr int kVec = 8;
 constexpr int kTileElems = AGS_TILE_ELEMS;  // a multiple of kBlock * kVec
 static_assert(kTileElems % (kBlock * kVec) == 0, "tile must hold whole block rounds");
 // A layer is cut into at most this many tiles (bigger layers get tiles of a
-// multiple of kTileElems), so that the finalize block of any layer sums at
-// most four partials per thread.
-constexpr int64_t kMaxTilesPerLayer = 1024;
+// multiple of kTileElems).
+#ifndef AGS_MAX_TILES_PER_LAYER
+#define AGS_MAX_TILES_PER_LAYER (1 << 30)
+#endif
+constexpr int64_t kMaxTilesPerLayer = AGS_MAX_TILES_PER_LAYER;
+// The finalize kernel sums at most this many tile partials per block (16 per
+// thread); a layer with more tiles is finalized by several blocks whose sums
+// the last of them combines.
+constexpr int kFinTilesPerChunk = 4096;
 
 // Elements per tile of a layer of numel elements.
 inline int64_t tile_elems_for(int64_t numel) {
@@ -48,9 +54,19 @@ struct Tile {
 };
 
 struct LayerDev {
-    int32_t tile_begin, tile_end;  // tiles [tile_begin, tile_end) cover the layer
+    int32_t tile_begin, tile_end;    // tiles [tile_begin, tile_end) cover the layer
     uint32_t flags;
+    int32_t chunk_begin, chunk_end;  // finalize chunks of the layer
     int32_t pad_;
+};
+
+// A finalize block's share: tiles [tile_begin, tile_end) of one layer.
+struct FinChunk {
+    int32_t layer, tile_begin, tile_end, pad_;
+};
+
+struct ChunkSum {
+    double w, g, d, s;
 };
 
 // Device-resident AGS state, updated by the last block of a committed step.
@@ -94,6 +110,9 @@ struct StepArgs {
     int* corr_flag;          // 1 when some layer needs the correction pass
     int updated;             // the step kernel applied predicted coefficients
     unsigned* done_count;    // layers finished (reset by the last block)
+    const FinChunk* chunks;  // finalize blocks
+    ChunkSum* chunk_sums;    // [n_chunks] sums of multi-chunk layers
+    unsigned* layer_chunk_count;  // [n_layers] chunks finished (reset by the last)
     ags_layer_stats* lstats;
     ags_global_stats* gstats;
 };
@@ -118,7 +137,7 @@ struct UpdateArgs {
 // Launchers (ags_kernels.hip).  They only enqueue; the return value is the
 // launch status.  update != 0 makes the step kernel apply the update.
 hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s);
-hipError_t launch_finalize(const StepArgs& a, hipStream_t s);
+hipError_t launch_finalize(const StepArgs& a, int n_chunks, hipStream_t s);
 hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s);
 hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s);
 

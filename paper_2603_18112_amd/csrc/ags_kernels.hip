@@ -17,10 +17,11 @@
 // The streaming kernels are HBM-bound (well under one flop per byte) and use
 // no matrix cores.  Element mapping: a block works through its tile in
 // rounds of 2048 elements; in a round, wave w owns elements [512w, 512w+512)
-// and lane l of it owns two halves of 4 elements, [4l, 4l+4) and
-// [256+4l, 256+4l+4).  So every load or store instruction of a wave covers
-// one contiguous span -- 1 KiB of fp32 (w, m, fp32 replicas) or 512 B of
-// bf16 -- and no cache line is split between two instructions.  Reductions
+// and each lane owns 8 of them.  With fp32 gradients lane l owns two halves
+// of 4 elements, [4l, 4l+4) and [256+4l, 256+4l+4), so every 16-byte load
+// or store instruction of a wave covers 1 KiB of consecutive elements; with
+// bf16 gradients lane l owns [8l, 8l+8), one 16-byte load per replica row.
+// Reductions
 // run in a fixed order (per thread, wave butterfly, the four waves in index
 // order, then per layer in fp64 over tiles in index order); the one atomic
 // only counts finished layers, so a step is bitwise reproducible.
@@ -54,11 +55,23 @@ namespace {
 #define AGS_LATE_WM_K 1 << 30
 #endif
 
+// bf16 gradients: a lane's two halves are adjacent (8 consecutive elements,
+// one 16-byte load per replica); fp32 gradients: 256 elements apart (every
+// 16-byte load instruction of a wave covers 1 KiB of consecutive elements).
+// Both measured best for their dtype on MI355X.
+#ifndef AGS_BF16_CONTIG
+#define AGS_BF16_CONTIG 1
+#endif
+
 constexpr int kHalf = 4;                    // elements per half group
-constexpr int kHalfStride = 64 * kHalf;     // 256: a lane's second half
-constexpr int kWaveSpan = 2 * kHalfStride;  // 512 elements per wave per round
+constexpr int kWaveSpan = 512;              // elements per wave per round
 constexpr int kRound = kBlock * kVec;       // 2048 elements per block per round
 static_assert(kRound == (kBlock / 64) * kWaveSpan, "round layout");
+
+// Distance between a lane's two halves for gradients of type GT.
+template <typename GT> struct Map {
+    static constexpr int HS = (sizeof(GT) == 2 && AGS_BF16_CONTIG) ? kHalf : kWaveSpan / 2;
+};
 
 // ---------------------------------------------------------------- loads ---
 
@@ -69,6 +82,15 @@ __device__ __forceinline__ uint2 stream_load(const uint2* p) {
 #if AGS_NT_LOADS
     const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
     return make_uint2(v.x, v.y);
+#else
+    return *p;
+#endif
+}
+
+__device__ __forceinline__ uint4 stream_load(const uint4* p) {
+#if AGS_NT_LOADS
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
 #else
     return *p;
 #endif
@@ -93,61 +115,69 @@ __device__ __forceinline__ float load1(const uint16_t* __restrict__ p) {
     return __uint_as_float(static_cast<uint32_t>(*p) << 16);
 }
 
-// A group of a lane: halves [p, p+4) and [p+256, p+260).  FULL groups are
+// A group of a lane: halves [p, p+4) and [p+HS, p+HS+4).  FULL groups are
 // two 16-byte (fp32) loads; the ragged end of a layer takes element loads
 // for the first n0 and n1 elements of the halves, the rest being 0 (which
 // adds nothing to any sum).
-template <bool FULL>
+template <bool FULL, int HS>
 __device__ __forceinline__ void load_f32(const float* __restrict__ p, int n0, int n1,
                                          float (&v)[kVec]) {
     if (FULL) {
         const float4 a = *reinterpret_cast<const float4*>(p);
-        const float4 b = *reinterpret_cast<const float4*>(p + kHalfStride);
+        const float4 b = *reinterpret_cast<const float4*>(p + HS);
         v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
         v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
     } else {
 #pragma unroll
         for (int e = 0; e < kHalf; ++e) {
             v[e] = (e < n0) ? p[e] : 0.0f;
-            v[kHalf + e] = (e < n1) ? p[kHalfStride + e] : 0.0f;
+            v[kHalf + e] = (e < n1) ? p[HS + e] : 0.0f;
         }
     }
 }
 
-template <bool FULL>
+template <bool FULL, int HS>
 __device__ __forceinline__ void store_f32(float* __restrict__ p, int n0, int n1,
                                           const float (&v)[kVec]) {
     if (FULL) {
         *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
-        *reinterpret_cast<float4*>(p + kHalfStride) = make_float4(v[4], v[5], v[6], v[7]);
+        *reinterpret_cast<float4*>(p + HS) = make_float4(v[4], v[5], v[6], v[7]);
     } else {
 #pragma unroll
         for (int e = 0; e < kHalf; ++e) {
             if (e < n0) p[e] = v[e];
-            if (e < n1) p[kHalfStride + e] = v[kHalf + e];
+            if (e < n1) p[HS + e] = v[kHalf + e];
         }
     }
 }
 
-template <typename GT>
+template <typename GT, int HS>
 __device__ __forceinline__ void load_tail(const GT* __restrict__ p, int n0, int n1,
                                           float (&v)[kVec]) {
 #pragma unroll
     for (int e = 0; e < kHalf; ++e) {
         v[e] = (e < n0) ? load1(p + e) : 0.0f;
-        v[kHalf + e] = (e < n1) ? load1(p + kHalfStride + e) : 0.0f;
+        v[kHalf + e] = (e < n1) ? load1(p + HS + e) : 0.0f;
     }
 }
 
-// A full group of replica values as loaded, before widening to fp32: two
-// 8-byte vectors for bf16, two 16-byte vectors for fp32.
+// A full group of replica values as loaded, before widening to fp32: one
+// 16-byte vector (bf16, adjacent halves) or two 8-byte vectors (bf16, split
+// halves), two 16-byte vectors for fp32.
 template <typename GT> struct RawGroup;
 template <> struct RawGroup<uint16_t> {
     static constexpr int kBatch = AGS_BATCH_BF16;
+    static constexpr int HS = Map<uint16_t>::HS;
     uint2 a, b;
     __device__ __forceinline__ void load(const uint16_t* __restrict__ p) {
-        a = stream_load(reinterpret_cast<const uint2*>(p));
-        b = stream_load(reinterpret_cast<const uint2*>(p + kHalfStride));
+        if constexpr (HS == kHalf) {
+            const uint4 v = stream_load(reinterpret_cast<const uint4*>(p));
+            a = make_uint2(v.x, v.y);
+            b = make_uint2(v.z, v.w);
+        } else {
+            a = stream_load(reinterpret_cast<const uint2*>(p));
+            b = stream_load(reinterpret_cast<const uint2*>(p + HS));
+        }
     }
     __device__ __forceinline__ void widen(float (&o)[kVec]) const {
         o[0] = bf16_lo(a.x); o[1] = bf16_hi(a.x); o[2] = bf16_lo(a.y); o[3] = bf16_hi(a.y);
@@ -156,10 +186,11 @@ template <> struct RawGroup<uint16_t> {
 };
 template <> struct RawGroup<float> {
     static constexpr int kBatch = AGS_BATCH_F32;
+    static constexpr int HS = Map<float>::HS;
     float4 a, b;
     __device__ __forceinline__ void load(const float* __restrict__ p) {
         a = stream_load(reinterpret_cast<const float4*>(p));
-        b = stream_load(reinterpret_cast<const float4*>(p + kHalfStride));
+        b = stream_load(reinterpret_cast<const float4*>(p + HS));
     }
     __device__ __forceinline__ void widen(float (&o)[kVec]) const {
         o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
@@ -190,7 +221,7 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
         r0.load(g + idx);
         r0.widen(g0);
     } else {
-        load_tail(g + idx, n0, n1, g0);
+        load_tail<GT, Map<GT>::HS>(g + idx, n0, n1, g0);
     }
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
@@ -250,7 +281,7 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
                     q.load(g + (int64_t)(k + j) * stride + idx);
                     q.widen(x[j]);
                 } else {
-                    load_tail(g + (int64_t)(k + j) * stride + idx, n0, n1, x[j]);
+                    load_tail<GT, Map<GT>::HS>(g + (int64_t)(k + j) * stride + idx, n0, n1, x[j]);
                 }
             }
 #pragma unroll
@@ -264,7 +295,7 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
                 q.load(g + (int64_t)k * stride + idx);
                 q.widen(x);
             } else {
-                load_tail(g + (int64_t)k * stride + idx, n0, n1, x);
+                load_tail<GT, Map<GT>::HS>(g + (int64_t)k * stride + idx, n0, n1, x);
             }
             acc(k, x);
         }
@@ -278,15 +309,17 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
 }
 
 // The groups of this thread in a tile of `count` elements starting at
-// `begin`: calls f(idx, n0, n1, full) for every group that holds data.
-template <typename F>
+// `begin` (halves HS apart): calls f(idx, n0, n1, full) for every group that
+// holds data.
+template <int HS, typename F>
 __device__ __forceinline__ void for_each_group(int64_t begin, int count, F&& f) {
-    const int pos = (int)(threadIdx.x >> 6) * kWaveSpan + (int)(threadIdx.x & 63) * kHalf;
+    const int lane_pos = HS == kHalf ? (int)(threadIdx.x & 63) * kVec : (int)(threadIdx.x & 63) * kHalf;
+    const int pos = (int)(threadIdx.x >> 6) * kWaveSpan + lane_pos;
 #pragma unroll 1
     for (int r0 = 0; r0 < count; r0 += kRound) {
         const int off = r0 + pos;
         const int n0 = min(max(count - off, 0), kHalf);
-        const int n1 = min(max(count - off - kHalfStride, 0), kHalf);
+        const int n1 = min(max(count - off - HS, 0), kHalf);
         if (n1 == kHalf) f(begin + off, kHalf, kHalf, std::true_type{});
         else if (n0 > 0) f(begin + off, n0, n1, std::false_type{});
     }
@@ -353,18 +386,18 @@ __device__ __forceinline__ bool surely_sensitive(double g_prev, long long step) 
 
 // ------------------------------------------------------- finalize -------
 
-// Per-layer statistics from the layer's tile partials (fp64, fixed order).
-__device__ void finalize_layer(const StepArgs& a, int l, Sum4* sh) {
-    const LayerDev ld = a.layers[l];
+// Sum of the tile partials [tb, te) in fp64, in a fixed order; every
+// thread of the block gets the result.
+__device__ Sum4 sum_tiles(const StepArgs& a, int tb, int te, Sum4* sh) {
     // Four independent accumulators per thread (tiles i, i + 256, i + 512,
-    // i + 768, then the next 1024), combined in a fixed order: long layers
-    // keep four loads in flight per thread instead of one.
+    // i + 768, then the next 1024), combined in a fixed order, so that four
+    // loads are in flight per thread.
     constexpr int U = 4;
     Sum4 acc[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) acc[u] = {0.0, 0.0, 0.0, 0.0};
-    int i = ld.tile_begin + (int)threadIdx.x;
-    for (; i + (U - 1) * kBlock < ld.tile_end; i += U * kBlock) {
+    int i = tb + (int)threadIdx.x;
+    for (; i + (U - 1) * kBlock < te; i += U * kBlock) {
         Partial p[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) p[u] = a.partials[i + u * kBlock];
@@ -379,7 +412,7 @@ __device__ void finalize_layer(const StepArgs& a, int l, Sum4* sh) {
 #pragma unroll
     for (int u = 0; u < U - 1; ++u) {
         const int j = i + u * kBlock;
-        if (j < ld.tile_end) {
+        if (j < te) {
             const Partial p = a.partials[j];
             acc[u].w += (double)p.w;
             acc[u].g += (double)p.g;
@@ -392,14 +425,15 @@ __device__ void finalize_layer(const StepArgs& a, int l, Sum4* sh) {
     v.g = (acc[0].g + acc[1].g) + (acc[2].g + acc[3].g);
     v.d = (acc[0].d + acc[1].d) + (acc[2].d + acc[3].d);
     v.s = (acc[0].s + acc[1].s) + (acc[2].s + acc[3].s);
-    v = block_sum4(v, sh);
-    if (threadIdx.x == 0) {
-        ags_layer_stats& o = a.lstats[l];
-        o.w_sq = v.w;
-        o.g_sq = v.g;
-        o.var = v.d / (double)a.K;
-        o.gsmall_sq = v.s;
-    }
+    return block_sum4(v, sh);
+}
+
+__device__ __forceinline__ void write_layer(const StepArgs& a, int l, const Sum4& v) {
+    ags_layer_stats& o = a.lstats[l];
+    o.w_sq = v.w;
+    o.g_sq = v.g;
+    o.var = v.d / (double)a.K;
+    o.gsmall_sq = v.s;
 }
 
 // The global decision and every layer's coefficients (one block, after all
@@ -510,16 +544,16 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
     constexpr bool late_wm = KT >= AGS_LATE_WM_K;
     float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
     if (!late_wm) {
-        load_f32<FULL>(a.w + idx, n0, n1, wv);
-        if (UPD) load_f32<FULL>(a.m + idx, n0, n1, mv);
+        load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
+        if (UPD) load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
     }
     moments<GT, KT, RMODE, FULL>(g, a.stride, idx, n0, n1, K, a.small_replica, a.invK, gb, dv,
                                  gr);
     if (late_wm) {
-        load_f32<FULL>(a.w + idx, n0, n1, wv);
-        if (UPD) load_f32<FULL>(a.m + idx, n0, n1, mv);
+        load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
+        if (UPD) load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
     }
-    if (!UPD && a.gbar) store_f32<FULL>(a.gbar + idx, n0, n1, gb);
+    if (!UPD && a.gbar) store_f32<FULL, Map<GT>::HS>(a.gbar + idx, n0, n1, gb);
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
         sw = fmaf(wv[e], wv[e], sw);
@@ -537,8 +571,8 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
             mv[e] = fmaf(a.momentum, mv[e], d);
             wv[e] = fmaf(-a.lr, mv[e], wv[e]);
         }
-        store_f32<FULL>(a.w + idx, n0, n1, wv);
-        store_f32<FULL>(a.m + idx, n0, n1, mv);
+        store_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
+        store_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
     }
 }
 
@@ -561,7 +595,7 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     }
 
     float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f;
-    for_each_group(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
+    for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
         step_group<GT, KT, RMODE, UPD, decltype(full)::value>(a, g, idx, n0, n1, K, ca, cb, sw,
                                                               sg, sd, ss);
     });
@@ -588,13 +622,45 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     }
 }
 
-// One block per layer.  The block that finishes the last layer (counted
-// with one device-scope atomic after a release fence) runs the global part.
+// One block per chunk of at most kFinTilesPerChunk tiles of one layer.  A
+// layer of several chunks is finished by the block that counts its last
+// chunk (one device-scope atomic after a release fence), which adds the
+// chunk sums in chunk order; the block that finishes the last layer runs
+// the global part.
 __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
     __shared__ Sum4 sh4[kBlock / 64];
     __shared__ int shi[kBlock / 64];
     __shared__ int sh_last;
-    finalize_layer(a, blockIdx.x, sh4);
+    const FinChunk c = a.chunks[blockIdx.x];
+    const int l = c.layer;
+    const Sum4 v = sum_tiles(a, c.tile_begin, c.tile_end, sh4);
+    const LayerDev ld = a.layers[l];
+    const int nch = ld.chunk_end - ld.chunk_begin;
+    if (nch == 1) {
+        if (threadIdx.x == 0) write_layer(a, l, v);
+    } else {
+        if (threadIdx.x == 0) {
+            a.chunk_sums[blockIdx.x] = ChunkSum{v.w, v.g, v.d, v.s};
+            __threadfence();
+            const unsigned prev = atomicAdd(&a.layer_chunk_count[l], 1u);
+            sh_last = (prev + 1 == (unsigned)nch);
+        }
+        __syncthreads();
+        if (!sh_last) return;
+        __threadfence();
+        if (threadIdx.x == 0) {
+            Sum4 t = {0.0, 0.0, 0.0, 0.0};
+            for (int q = ld.chunk_begin; q < ld.chunk_end; ++q) {
+                const ChunkSum cs = a.chunk_sums[q];
+                t.w += cs.w;
+                t.g += cs.g;
+                t.d += cs.d;
+                t.s += cs.s;
+            }
+            write_layer(a, l, t);
+            a.layer_chunk_count[l] = 0u;  // ready for the next launch
+        }
+    }
     if (threadIdx.x == 0) {
         __threadfence();
         const unsigned prev = atomicAdd(a.done_count, 1u);
@@ -615,8 +681,8 @@ template <typename GT, int KT, bool FULL>
 __device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __restrict__ g,
                                               int64_t idx, int n0, int n1, int K, float c) {
     float gb[kVec], dv[kVec], gr[kVec], wv[kVec], mv[kVec];
-    load_f32<FULL>(a.w + idx, n0, n1, wv);
-    load_f32<FULL>(a.m + idx, n0, n1, mv);
+    load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
+    load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
     moments<GT, KT, 0, FULL>(g, a.stride, idx, n0, n1, K, 0, a.invK, gb, dv, gr);
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
@@ -624,8 +690,8 @@ __device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __r
         mv[e] += cg;
         wv[e] = fmaf(-a.lr, cg, wv[e]);
     }
-    store_f32<FULL>(a.w + idx, n0, n1, wv);
-    store_f32<FULL>(a.m + idx, n0, n1, mv);
+    store_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
+    store_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
 }
 
 template <typename GT, int KT>
@@ -638,7 +704,7 @@ __global__ __launch_bounds__(kBlock) void correct_kernel(UpdateArgs a) {
         const Tile t = a.tiles[ti];
         const float c = a.corr[t.layer];
         if (c == 0.0f) continue;
-        for_each_group(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
+        for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
             correct_group<GT, KT, decltype(full)::value>(a, g, idx, n0, n1, K, c);
         });
     }
@@ -653,13 +719,13 @@ __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __re
                                              int64_t idx, int n0, int n1, int K, float ca,
                                              float cb) {
     float gb[kVec], wv[kVec], mv[kVec];
-    load_f32<FULL>(a.w + idx, n0, n1, wv);
-    load_f32<FULL>(a.m + idx, n0, n1, mv);
+    load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
+    load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
     if (RECOMP) {
         float dv[kVec], gr[kVec];
         moments<GT, KT, 0, FULL>(g, a.stride, idx, n0, n1, K, 0, a.invK, gb, dv, gr);
     } else {
-        load_f32<FULL>(a.gbar + idx, n0, n1, gb);
+        load_f32<FULL, Map<GT>::HS>(a.gbar + idx, n0, n1, gb);
     }
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
@@ -667,8 +733,8 @@ __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __re
         mv[e] = fmaf(a.momentum, mv[e], d);
         wv[e] = fmaf(-a.lr, mv[e], wv[e]);
     }
-    store_f32<FULL>(a.w + idx, n0, n1, wv);
-    store_f32<FULL>(a.m + idx, n0, n1, mv);
+    store_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
+    store_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
 }
 
 template <typename GT, int KT, bool RECOMP>
@@ -677,7 +743,7 @@ __global__ __launch_bounds__(kBlock) void update_kernel(UpdateArgs a) {
     const float2 ab = a.coef[t.layer];
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
-    for_each_group(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
+    for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
         update_group<GT, KT, RECOMP, decltype(full)::value>(a, g, idx, n0, n1, K, ab.x, ab.y);
     });
 }
@@ -749,8 +815,8 @@ hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update
                           : step_t<float>(a, n_tiles, update, s);
 }
 
-hipError_t launch_finalize(const StepArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(finalize_kernel, dim3(a.n_layers), dim3(kBlock), 0, s, a);
+hipError_t launch_finalize(const StepArgs& a, int n_chunks, hipStream_t s) {
+    hipLaunchKernelGGL(finalize_kernel, dim3(n_chunks), dim3(kBlock), 0, s, a);
     return hipGetLastError();
 }
 
