@@ -185,7 +185,8 @@ def main():
     N = lay.n_params
     t0 = time.time()
     w0 = synth.init_weights(lay, 0)
-    g_np = synth.replica_grads(lay, K, 0, 0, dtype=gdt)
+    stride = layouts.replica_stride(lay)
+    g_np = synth.replica_grads(lay, K, 0, 0, dtype=gdt, stride=stride)
     log(f"inputs generated in {time.time() - t0:.1f}s: {desc} "
         f"({g_np.nbytes / 1e9:.2f} GB of gradients)")
 
@@ -223,6 +224,24 @@ def main():
     h.set_profiling(False)
     log("per kernel (us): " + ", ".join(f"{n} {kms[i] / ncalls * 1e3:.1f}"
                                          for i, n in enumerate(ags.KERNEL_NAMES)))
+
+    # Cold-cache steps: a 1 GiB read evicts the caches (L2 and the 256 MB
+    # Infinity Cache) between steps, as the forward and backward passes of a
+    # training step would; each step is timed on its own with two events.
+    flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    cold_ms = []
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(min(args.steps, 100))]
+    for a0, a1 in ev:
+        flush.sum()
+        a0.record(stream)
+        h.step(g, stream)
+        a1.record(stream)
+    torch.cuda.synchronize()
+    cold_ms = sorted(a0.elapsed_time(a1) for a0, a1 in ev)
+    cold_step = cold_ms[len(cold_ms) // 2]
+    del flush
+    log(f"cold-cache steps: median {cold_step * 1e3:.1f} us")
     s = h.read_stats()
 
     ab = algorithmic_bytes(N, args.mode)
@@ -269,6 +288,10 @@ def main():
                    "mode": args.mode, "algorithmic_bytes_per_step": ab["whole_step"],
                    "parallelism": "single GPU (K replicas stand in for K data-parallel workers)"},
         "kernel_us": {n: round(v * 1e3, 2) for n, v in avg_ms.items()},
+        "cold_cache": {"ms_per_step": round(cold_step, 5),
+                       "value": round(ab["whole_step"] / (cold_step * 1e-3) / 1e9, 1),
+                       "note": "median of single steps after a 1 GiB read evicts the caches"},
+        "replica_stride": stride,
         "device_copy_GBps": round(copy_bw, 1),
         "roofline": roofline,
         "cpu_baseline": cpu,

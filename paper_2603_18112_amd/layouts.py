@@ -71,6 +71,19 @@ def round_up(x: int, a: int) -> int:
     return (x + a - 1) // a * a
 
 
+#: Gap, in elements, left between consecutive replica rows of a gradient
+#: stack.  The K replica streams of a step are read at the same offset at the
+#: same time; staggering their start addresses spreads them over more HBM
+#: channels (measured on MI355X: 2.5% faster ResNet-50 K=16 steps, no change
+#: for the fp32 layouts).
+REPLICA_GAP = 2048
+
+
+def replica_stride(layout: "Layout") -> int:
+    """Row stride (elements) of a [K, stride] replica-gradient stack."""
+    return round_up(layout.n_flat, 8) + REPLICA_GAP
+
+
 def _flags_for(t: Tensor, policy: str) -> int:
     if policy == "all":
         return LAYER_SCALE | LAYER_DECAY

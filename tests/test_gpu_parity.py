@@ -44,8 +44,11 @@ def test_resnet18_cifar_k8_one_step():
 
 
 def test_resnet50_k16_bf16_ten_steps():
+    # The benchmark's launch configuration: the same layout, K, dtype and
+    # replica stride as bench.py's default workload.
     lay = layouts.get_layout("resnet50")
-    w = run_steps(lay, 16, 10, dtype="bf16", check_each=False, label="r50")
+    w = run_steps(lay, 16, 10, dtype="bf16", check_each=False, label="r50",
+                  stride=layouts.replica_stride(lay))
     log(f"  r50 worst param error / tolerance scale: w {w[0]:.2e} m {w[1]:.2e}")
 
 
