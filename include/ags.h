@@ -3,11 +3,11 @@
  * gradient statistics, for one data-parallel training step on one MI355X
  * (gfx950) GPU.
  *
- * Source of the method: Tula (arXiv 2603.18112), Sec. IV-B "Statistical
- * Performance Model", Eq. (5)-(8) and Algorithm 1 "Adaptive Gradient
- * Scaling"; synchronous data-parallel averaging of Eq. (1c); the wrapped
- * momentum SGD with weight decay of Sec. V-A/V-B; the LARS baseline of
- * Sec. V-D.
+ * Source of the method: Tula (arXiv 2603.18112): the gradient-variability
+ * metric of Sec. III-B, Eq. (5); the statistical performance model of
+ * Sec. III-C, Eq. (6)-(8) and Algorithm 1 "Adaptive Gradient Scaling";
+ * synchronous data-parallel averaging, Eq. (1c); the wrapped momentum SGD
+ * with weight decay of Sec. IV-A/IV-B; the LARS baseline of Sec. IV-D.
  *
  * One step, for a model whose parameter tensors ("layers") are laid end to
  * end in one flat fp32 buffer w with momentum m of the same layout, given K

@@ -23,7 +23,7 @@
  *   3. Global squared norm G = sum_l G_l, gradient variability
  *        Delta = |G - G_prev| / G_prev                   (Eq. (5))
  *      sensitive = !(Delta < delta)                      (Algorithm 1 branch,
- *                                                         Sec. IV-B)
+ *                                                         Sec. III-C)
  *      On the first step (no G_prev), G_prev <= 0 or a non-finite value,
  *      Delta = +inf, i.e. the step is treated as sensitive.
  *   4. Per-layer coefficients of the update d = a_l * gbar + b_l * w:
@@ -33,11 +33,11 @@
  *                                              momentum-SGD adding decay)
  *        LARS: a_l = tau ||w|| / (||gbar|| + lambda_l ||w||) if scaled
  *              (1 when ||w|| = 0 or ||gbar|| = 0), b_l = a_l * lambda_l
- *              (LARS baseline, Sec. V-D: learning rate scaled by
+ *              (LARS baseline, Sec. IV-D: learning rate scaled by
  *               ||w|| / ||grad w|| per layer)
  *        SGD : a_l = 1, b_l = lambda_l        (vanilla large-batch baseline)
  *      lambda_l = weight_decay if the layer is decayed, else 0.
- *   5. Wrapped momentum SGD (Sec. V-A, V-B: SGD, momentum 0.9, weight decay;
+ *   5. Wrapped momentum SGD (Sec. IV-A, IV-B: SGD, momentum 0.9, weight decay;
  *      PyTorch semantics, no dampening, no Nesterov):
  *        m_j <- mu m_j + d_j ;  w_j <- w_j - eta m_j     (Eq. (7b))
  *   6. UpdateGradScale after the update when a refresh is due

@@ -13,7 +13,7 @@ Only shapes live here: this module holds no part of the method's arithmetic.
 The tensor lists follow the public architecture definitions (ResNet: He et
 al. 2016; VGG: Simonyan & Zisserman 2015), in the order a PyTorch module
 lists its parameters.  The paper evaluates its method on CNNs of these
-families (Sec. V-B, experimental setup).
+families (Sec. IV-B, experimental setup).
 """
 from __future__ import annotations
 

@@ -4,7 +4,7 @@ This module only *draws* inputs; it holds none of the method's arithmetic and
 is shared by the GPU path's tests/bench and by the float64 oracle's tests, so
 that both sides read the very same bytes.
 
-Recipe (the paper trains CNNs on ImageNet-1K / CIFAR100 / CalTech, Sec. V-B;
+Recipe (the paper trains CNNs on ImageNet-1K / CIFAR100 / CalTech, Sec. IV-B;
 neither the datasets nor trained weights are needed, only the parameter
 shapes and gradients of a realistic scale):
 
