@@ -154,6 +154,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default=WORKLOAD, choices=sorted(WORKLOADS))
     ap.add_argument("--mode", default="ags", choices=["ags", "sgd", "lars"])
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step captured once in a HIP graph and replayed")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -242,6 +244,25 @@ def main():
     cold_step = cold_ms[len(cold_ms) // 2]
     del flush
     log(f"cold-cache steps: median {cold_step * 1e3:.1f} us")
+    graph_ms = None
+    if args.graph:
+        # One step captured in a HIP graph (kernels only), replayed K times.
+        cap = torch.cuda.Stream()
+        graph = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap):
+            h.step(g)
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        graph_ms = e0.elapsed_time(e1) / args.steps
+        log(f"graph replay: {graph_ms * 1e3:.1f} us/step")
     s = h.read_stats()
 
     ab = algorithmic_bytes(N, args.mode)
@@ -292,6 +313,7 @@ def main():
                        "value": round(ab["whole_step"] / (cold_step * 1e-3) / 1e9, 1),
                        "note": "median of single steps after a 1 GiB read evicts the caches"},
         "replica_stride": stride,
+        "graph_replay_ms_per_step": None if graph_ms is None else round(graph_ms, 5),
         "device_copy_GBps": round(copy_bw, 1),
         "roofline": roofline,
         "cpu_baseline": cpu,

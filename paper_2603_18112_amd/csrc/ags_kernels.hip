@@ -576,10 +576,27 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
     }
 }
 
+// Workgroups are dispatched round-robin over the 8 XCDs; with AGS_XCD_MAP
+// each XCD walks a contiguous range of tiles instead of every 8th tile.
+#ifndef AGS_XCD_MAP
+#define AGS_XCD_MAP 0
+#endif
+__device__ __forceinline__ int tile_of_block(int b, int n) {
+#if AGS_XCD_MAP
+    constexpr int nx = 8;
+    const int q = n / nx, r = n % nx, x = b % nx, i = b / nx;
+    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
+#else
+    (void)n;
+    return b;
+#endif
+}
+
 template <typename GT, int KT, int RMODE, bool UPD>
 __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     __shared__ float red[4][kBlock / 64];
-    const Tile t = a.tiles[blockIdx.x];
+    const int ti = tile_of_block(blockIdx.x, gridDim.x);
+    const Tile t = a.tiles[ti];
     const int l = t.layer;
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
@@ -618,7 +635,7 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
         p.g = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
         p.d = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
         p.s = (red[3][0] + red[3][1]) + (red[3][2] + red[3][3]);
-        a.partials[blockIdx.x] = p;
+        a.partials[ti] = p;
     }
 }
 
