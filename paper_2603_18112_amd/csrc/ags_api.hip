@@ -358,6 +358,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.corr = h->corr();
     sa.corr_flag = h->corr_flag();
     sa.updated = fused ? 1 : 0;
+    sa.xcd_map = h->n_tiles >= ags::kXcdMapMinTiles ? 1 : 0;
     sa.done_count = h->done_count();
     sa.chunks = reinterpret_cast<const ags::FinChunk*>(h->ws + h->wl.chunks);
     sa.chunk_sums = reinterpret_cast<ags::ChunkSum*>(h->ws + h->wl.chunk_sums);

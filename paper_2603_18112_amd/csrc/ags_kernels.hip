@@ -576,26 +576,20 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
     }
 }
 
-// Workgroups are dispatched round-robin over the 8 XCDs; with AGS_XCD_MAP
-// each XCD walks a contiguous range of tiles instead of every 8th tile.
-#ifndef AGS_XCD_MAP
-#define AGS_XCD_MAP 0
-#endif
-__device__ __forceinline__ int tile_of_block(int b, int n) {
-#if AGS_XCD_MAP
+// Workgroups are dispatched round-robin over the 8 XCDs.  With xcd_map each
+// XCD walks a contiguous range of tiles instead of every 8th tile (a
+// bijection of block indices onto tiles).
+__device__ __forceinline__ int tile_of_block(int b, int n, int xcd_map) {
+    if (!xcd_map) return b;
     constexpr int nx = 8;
     const int q = n / nx, r = n % nx, x = b % nx, i = b / nx;
     return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
-#else
-    (void)n;
-    return b;
-#endif
 }
 
 template <typename GT, int KT, int RMODE, bool UPD>
 __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     __shared__ float red[4][kBlock / 64];
-    const int ti = tile_of_block(blockIdx.x, gridDim.x);
+    const int ti = tile_of_block(blockIdx.x, gridDim.x, a.xcd_map);
     const Tile t = a.tiles[ti];
     const int l = t.layer;
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
