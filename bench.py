@@ -244,6 +244,22 @@ def main():
     cold_step = cold_ms[len(cold_ms) // 2]
     del flush
     log(f"cold-cache steps: median {cold_step * 1e3:.1f} us")
+    # Worst case of the coefficient prediction: gradient sets g and 2g in
+    # turn make every step sensitive (Delta = 3, then 0.75), so every AGS
+    # step is applied scaled and then corrected by the second pass.
+    g2 = g.view(torch.bfloat16).mul(2).view(g.dtype) if gdt == "bf16" else g * 2
+    torch.cuda.synchronize()
+    nmis = min(args.steps, 100)
+    e0.record(stream)
+    for i in range(nmis):
+        h.step(g2 if i % 2 == 0 else g, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    mis_ms = e0.elapsed_time(e1) / nmis
+    mis_sens = h.read_stats().glob["sensitive"]
+    del g2
+    log(f"mispredicted steps: {mis_ms * 1e3:.1f} us/step (last step sensitive={mis_sens})")
+
     graph_ms = None
     if args.graph:
         # One step captured in a HIP graph (kernels only), replayed K times.
@@ -313,6 +329,9 @@ def main():
                        "value": round(ab["whole_step"] / (cold_step * 1e-3) / 1e9, 1),
                        "note": "median of single steps after a 1 GiB read evicts the caches"},
         "replica_stride": stride,
+        "mispredicted_steps": {"ms_per_step": round(mis_ms, 5), "last_sensitive": mis_sens,
+                               "note": "every step sensitive: applied with the predicted "
+                                       "coefficients, then corrected (AGS); SGD never corrects"},
         "graph_replay_ms_per_step": None if graph_ms is None else round(graph_ms, 5),
         "device_copy_GBps": round(copy_bw, 1),
         "roofline": roofline,

@@ -366,3 +366,30 @@ def test_hip_graph_capture_replays_match_eager(lay_name, K, dtype):
         assert se.glob == sg.glob
     eager.close()
     graphed.close()
+
+
+def test_matches_golden_oracle_fixture():
+    """The HIP path against the stored oracle output of the tiny CNN layout
+    (tests/golden/tiny_cnn_ags_k4.json, written by a script that calls only
+    the oracle), at the sampled elements and for every statistic."""
+    import json
+    import os
+    import torch
+    from ags_parity import PARAM_RTOL, STAT_RTOL
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "tiny_cnn_ags_k4.json")))
+    lay = layouts.get_layout(gold["layout"])
+    w = torch.from_numpy(synth.init_weights(lay, gold["seed"])).cuda()
+    m = torch.zeros_like(w)
+    h = ags.AGS(lay.table(), w, m, gold["K"], **gold["hyper"])
+    idx = gold["index"]
+    for t, step in enumerate(gold["steps"]):
+        h.step(to_device(synth.replica_grads(lay, gold["K"], t, gold["seed"])))
+        s = h.read_stats()
+        for k, v in step["layer"].items():
+            np.testing.assert_allclose(s.layer[k], v, rtol=STAT_RTOL)
+        assert s.glob["sensitive"] == step["global"]["sensitive"]
+        wv, mv = w.cpu().numpy()[idx], m.cpu().numpy()[idx]
+        for got, ref in ((wv, np.array(step["w"])), (mv, np.array(step["m"]))):
+            scale = np.maximum(np.abs(ref), np.sqrt(np.mean(ref * ref)))
+            assert np.all(np.abs(got - ref) <= PARAM_RTOL * scale)
+    h.close()

@@ -544,3 +544,27 @@ def test_unscaled_layer_ignores_gradscale_state():
     st, gl = o.step(g)
     assert gl["sensitive"] == 0
     assert st["coef_a"][0] == 1.5 and st["coef_a"][1] == 1.0
+
+
+# --------------------------------------------------------------------------
+# frozen oracle output (tests/golden/make_golden.py, which calls only the
+# oracle): guards the oracle against unintended changes of its arithmetic
+
+
+def test_oracle_reproduces_golden_fixture():
+    import json
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "tiny_cnn_ags_k4.json")
+    gold = json.load(open(path))
+    lay = layouts.get_layout(gold["layout"])
+    o = OracleAGS(lay.table(), lay.n_flat, gold["K"], synth.init_weights(lay, gold["seed"]),
+                  **gold["hyper"])
+    idx = gold["index"]
+    for t, step in enumerate(gold["steps"]):
+        st, gl = o.step(synth.replica_grads(lay, gold["K"], t, gold["seed"]))
+        for k, v in step["layer"].items():
+            np.testing.assert_allclose(st[k], v, rtol=1e-14, atol=0)
+        for k, v in step["global"].items():
+            assert (gl[k] == v) or abs(gl[k] - v) <= 1e-14 * abs(v), (t, k)
+        np.testing.assert_allclose(o.w[idx], step["w"], rtol=1e-14, atol=0)
+        np.testing.assert_allclose(o.m[idx], step["m"], rtol=1e-14, atol=0)
