@@ -153,7 +153,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default=WORKLOAD, choices=sorted(WORKLOADS))
-    ap.add_argument("--mode", default="ags", choices=["ags", "sgd", "lars"])
+    ap.add_argument("--mode", default="ags", choices=["ags", "sgd", "lars", "static"])
     ap.add_argument("--graph", action="store_true",
                     help="also time the step captured once in a HIP graph and replayed")
     ap.add_argument("--copy-probe", action="store_true",

@@ -29,6 +29,9 @@
  *              sensitive, else 1; b_l = lambda_l.
  *        LARS  a_l = tau ||w_l|| / (||gbar_l|| + lambda_l ||w_l||) on scaled
  *              layers (1 if either norm is 0); b_l = a_l lambda_l.
+ *        STATIC a_l = s (static_scale) if the layer is scaled and the step
+ *              is not sensitive, else 1; b_l = lambda_l (the static mapping
+ *              U(s) of Eq. (8a), (8b), Sec. III-C).
  *        SGD   a_l = 1; b_l = lambda_l.
  * lambda_l is weight_decay on layers with AGS_LAYER_DECAY, else 0.
  *
@@ -69,7 +72,7 @@ typedef enum {
 
 typedef enum { AGS_F32 = 0, AGS_BF16 = 1 } ags_dtype;
 
-typedef enum { AGS_MODE_SGD = 0, AGS_MODE_AGS = 1, AGS_MODE_LARS = 2 } ags_mode;
+typedef enum { AGS_MODE_SGD = 0, AGS_MODE_AGS = 1, AGS_MODE_LARS = 2, AGS_MODE_STATIC = 3 } ags_mode;
 
 #define AGS_LAYER_SCALE 1u /* the layer takes part in AGS / LARS scaling  */
 #define AGS_LAYER_DECAY 2u /* the layer receives weight decay             */
@@ -108,6 +111,7 @@ typedef struct {
     int32_t refresh_every;   /* refresh gradscale every n steps; 0 = never  */
     int32_t small_replica;   /* replica r taken as the small-batch gradient;
                                 -1 = mean over replicas of ||g_k||^2        */
+    double static_scale;     /* s of AGS_MODE_STATIC (> 0)                 */
 } ags_config;
 
 /* Per-layer record of the last ags_stats / ags_step.  var is V_l (the 1/K

@@ -21,7 +21,7 @@ _LIB = os.path.join(_HERE, "liboracle_ags.so")
 _lock = threading.Lock()
 _lib = None
 
-MODES = {"sgd": 0, "ags": 1, "lars": 2}
+MODES = {"sgd": 0, "ags": 1, "lars": 2, "static": 3}
 LAYER_FIELDS = ("w_sq", "g_sq", "var", "gsmall_sq", "noise_ratio", "coef_a",
                 "coef_b", "gradscale")
 GLOBAL_FIELDS = ("g_sq", "g_sq_prev", "delta", "sensitive", "nonfinite")
@@ -40,7 +40,7 @@ class _Config(ctypes.Structure):
                 ("lr", ctypes.c_double), ("momentum", ctypes.c_double),
                 ("weight_decay", ctypes.c_double), ("delta", ctypes.c_double),
                 ("eps", ctypes.c_double), ("s_max", ctypes.c_double),
-                ("trust_coef", ctypes.c_double)]
+                ("trust_coef", ctypes.c_double), ("static_scale", ctypes.c_double)]
 
 
 def build(force: bool = False) -> str:
@@ -78,7 +78,7 @@ class OracleAGS:
 
     def __init__(self, layers, n_flat, K, w0, m0=None, *, mode="ags",
                  grad_dtype="f32", lr=0.1, momentum=0.9, weight_decay=5e-4,
-                 delta=0.5, eps=1e-8, s_max=0.0, trust_coef=1e-3,
+                 delta=0.5, eps=1e-8, s_max=0.0, trust_coef=1e-3, static_scale=2.0,
                  refresh_every=1, small_replica=0):
         self.lib = _load()
         self.layers = [(int(o), int(n), int(f)) for o, n, f in layers]
@@ -88,6 +88,7 @@ class OracleAGS:
         self.grad_dtype = grad_dtype
         self.cfg = dict(mode=mode, lr=lr, momentum=momentum, weight_decay=weight_decay,
                         delta=delta, eps=eps, s_max=s_max, trust_coef=trust_coef,
+                        static_scale=static_scale,
                         refresh_every=refresh_every, small_replica=small_replica)
         self.w = np.array(w0, dtype=np.float64, copy=True).reshape(-1)
         self.m = (np.zeros(self.n_flat) if m0 is None
@@ -131,7 +132,8 @@ class OracleAGS:
                       lr=float(c["lr"] if lr is None else lr), momentum=float(c["momentum"]),
                       weight_decay=float(c["weight_decay"]), delta=float(c["delta"]),
                       eps=float(c["eps"]), s_max=float(c["s_max"]),
-                      trust_coef=float(c["trust_coef"]))
+                      trust_coef=float(c["trust_coef"]),
+                      static_scale=float(c["static_scale"]))
         out_l = np.zeros((self.L, len(LAYER_FIELDS)))
         out_g = np.zeros(len(GLOBAL_FIELDS))
         rc = self.lib.oracle_ags_step(

@@ -35,6 +35,9 @@
  *              (1 when ||w|| = 0 or ||gbar|| = 0), b_l = a_l * lambda_l
  *              (LARS baseline, Sec. IV-D: learning rate scaled by
  *               ||w|| / ||grad w|| per layer)
+ *        STATIC: a_l = s if (layer scaled and not sensitive) else 1,
+ *              b_l = lambda_l                 (static gradient scaling U(s),
+ *                                              Eq. (8a), (8b), Sec. III-C)
  *        SGD : a_l = 1, b_l = lambda_l        (vanilla large-batch baseline)
  *      lambda_l = weight_decay if the layer is decayed, else 0.
  *   5. Wrapped momentum SGD (Sec. IV-A, IV-B: SGD, momentum 0.9, weight decay;
@@ -59,7 +62,7 @@
 #define ORACLE_SCALE 1u
 #define ORACLE_DECAY 2u
 
-enum { ORACLE_SGD = 0, ORACLE_AGS = 1, ORACLE_LARS = 2 };
+enum { ORACLE_SGD = 0, ORACLE_AGS = 1, ORACLE_LARS = 2, ORACLE_STATIC = 3 };
 
 typedef struct {
     int64_t offset;
@@ -78,6 +81,7 @@ typedef struct {
     int64_t n_flat;
     int64_t replica_stride;
     double lr, momentum, weight_decay, delta, eps, s_max, trust_coef;
+    double static_scale; /* s of the static mapping U(s) */
 } oracle_config;
 
 /* Per-layer output record: W, G, V, S, rho, a, b, gradscale (after refresh). */
@@ -197,6 +201,9 @@ int oracle_ags_step(const oracle_config *c, double *w, double *m, const void *gr
         double a = 1.0, b = lam;
         if (c->mode == ORACLE_AGS) {
             a = (scaled && !sensitive) ? gradscale[l] : 1.0;
+            b = lam;
+        } else if (c->mode == ORACLE_STATIC) {
+            a = (scaled && !sensitive) ? c->static_scale : 1.0;
             b = lam;
         } else if (c->mode == ORACLE_LARS) {
             if (scaled) {

@@ -26,13 +26,14 @@ AGS_OK, AGS_E_ARG, AGS_E_LAYOUT, AGS_E_ALIGN, AGS_E_NOMEM, AGS_E_DEVICE, AGS_E_S
 STATUS_NAMES = {0: "AGS_OK", 1: "AGS_E_ARG", 2: "AGS_E_LAYOUT", 3: "AGS_E_ALIGN",
                 4: "AGS_E_NOMEM", 5: "AGS_E_DEVICE", 6: "AGS_E_STATE"}
 AGS_F32, AGS_BF16 = 0, 1
-AGS_MODE_SGD, AGS_MODE_AGS, AGS_MODE_LARS = 0, 1, 2
+AGS_MODE_SGD, AGS_MODE_AGS, AGS_MODE_LARS, AGS_MODE_STATIC = 0, 1, 2, 3
 AGS_LAYER_SCALE, AGS_LAYER_DECAY = 1, 2
 AGS_ALIGN_ELEMS = 8
 AGS_MAX_K = 1024
 AGS_N_KERNELS = 3
 KERNEL_NAMES = ("step", "finalize", "second_pass")
-MODES = {"sgd": AGS_MODE_SGD, "ags": AGS_MODE_AGS, "lars": AGS_MODE_LARS}
+MODES = {"sgd": AGS_MODE_SGD, "ags": AGS_MODE_AGS, "lars": AGS_MODE_LARS,
+         "static": AGS_MODE_STATIC}
 DTYPES = {"f32": AGS_F32, "bf16": AGS_BF16}
 
 
@@ -49,7 +50,7 @@ class ags_config(ctypes.Structure):
                 ("weight_decay", ctypes.c_double), ("delta", ctypes.c_double),
                 ("eps", ctypes.c_double), ("s_max", ctypes.c_double),
                 ("trust_coef", ctypes.c_double), ("refresh_every", ctypes.c_int32),
-                ("small_replica", ctypes.c_int32)]
+                ("small_replica", ctypes.c_int32), ("static_scale", ctypes.c_double)]
 
 
 class ags_layer_stats(ctypes.Structure):
@@ -136,7 +137,7 @@ def _check(status: int, handle=None):
 
 def make_config(layers, n_flat, K, *, grad_dtype="f32", mode="ags", lr=0.1, momentum=0.9,
                 weight_decay=5e-4, delta=0.5, eps=1e-8, s_max=0.0, trust_coef=1e-3,
-                refresh_every=1, small_replica=0):
+                refresh_every=1, small_replica=0, static_scale=2.0):
     """An ags_config (plus the layer array it points to, kept alive on it)."""
     arr = (ags_layer * max(len(layers), 1))()
     for i, (o, n, f) in enumerate(layers):
@@ -146,7 +147,7 @@ def make_config(layers, n_flat, K, *, grad_dtype="f32", mode="ags", lr=0.1, mome
                      lr=float(lr), momentum=float(momentum), weight_decay=float(weight_decay),
                      delta=float(delta), eps=float(eps), s_max=float(s_max),
                      trust_coef=float(trust_coef), refresh_every=int(refresh_every),
-                     small_replica=int(small_replica))
+                     small_replica=int(small_replica), static_scale=float(static_scale))
     cfg._layers_keepalive = arr
     return cfg
 

@@ -98,7 +98,8 @@ ags_status check_config(const ags_config* c, std::string& why) {
     if (c->n_flat < 1) { why = "n_flat must be >= 1"; return AGS_E_LAYOUT; }
     if (c->K < 1 || c->K > AGS_MAX_K) { why = "K out of range 1..AGS_MAX_K"; return AGS_E_ARG; }
     if (c->grad_dtype != AGS_F32 && c->grad_dtype != AGS_BF16) { why = "bad grad_dtype"; return AGS_E_ARG; }
-    if (c->mode != AGS_MODE_SGD && c->mode != AGS_MODE_AGS && c->mode != AGS_MODE_LARS) {
+    if (c->mode != AGS_MODE_SGD && c->mode != AGS_MODE_AGS && c->mode != AGS_MODE_LARS &&
+        c->mode != AGS_MODE_STATIC) {
         why = "bad mode";
         return AGS_E_ARG;
     }
@@ -113,6 +114,10 @@ ags_status check_config(const ags_config* c, std::string& why) {
     if (!finite(c->s_max)) { why = "s_max must be finite"; return AGS_E_ARG; }
     if (c->mode == AGS_MODE_LARS && !(finite(c->trust_coef) && c->trust_coef > 0)) {
         why = "trust_coef must be > 0 in LARS mode";
+        return AGS_E_ARG;
+    }
+    if (c->mode == AGS_MODE_STATIC && !(finite(c->static_scale) && c->static_scale > 0)) {
+        why = "static_scale must be finite and > 0 in STATIC mode";
         return AGS_E_ARG;
     }
     if (c->refresh_every < 0) { why = "refresh_every must be >= 0"; return AGS_E_ARG; }
@@ -351,6 +356,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.eps = c.eps;
     sa.s_max = c.s_max;
     sa.trust_coef = c.trust_coef;
+    sa.static_scale = c.static_scale;
     sa.weight_decay = c.weight_decay;
     sa.gradscale = h->gradscale();
     sa.state = h->state();

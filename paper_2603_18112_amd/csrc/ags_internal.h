@@ -106,7 +106,7 @@ struct StepArgs {
     int commit;              // 1: a step (state advances), 0: statistics only
     int refresh_every;
     float lr, momentum;      // used when the kernel updates w and m
-    double delta, eps, s_max, trust_coef, weight_decay;
+    double delta, eps, s_max, trust_coef, weight_decay, static_scale;
     double* gradscale;       // [n_layers]
     DevState* state;
     float2* coef;            // [n_layers] (a_l, b_l) as applied, fp32

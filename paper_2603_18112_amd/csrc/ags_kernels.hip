@@ -440,7 +440,8 @@ __device__ __forceinline__ void write_layer(const StepArgs& a, int l, const Sum4
 // layers are final).  Delta = |G - G_prev| / G_prev, infinite on a first
 // step, when G_prev <= 0 or when a value is not finite; sensitive =
 // !(Delta < delta).  AGS: a_l = gradscale_l on scaled layers of a
-// non-sensitive step, else 1; LARS: a_l = tau ||w|| / (||g|| + lambda ||w||);
+// non-sensitive step, else 1; STATIC: a_l = s likewise (U(s), Eq. (8));
+// LARS: a_l = tau ||w|| / (||g|| + lambda ||w||);
 // b_l = lambda_l (AGS, SGD) or a_l lambda_l (LARS).  When the refresh is due,
 // gradscale_l = min(sqrt(S_l) / (sqrt(G_l) + eps), s_max) (1 if a norm is 0)
 // for the steps that follow.  updated: the step kernel has already applied
@@ -500,6 +501,8 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         double ca = 1.0, cb = lam;
         if (a.mode == AGS_MODE_AGS) {
             ca = (scaled && !sens) ? gs_old : 1.0;
+        } else if (a.mode == AGS_MODE_STATIC) {
+            ca = (scaled && !sens) ? a.static_scale : 1.0;
         } else if (a.mode == AGS_MODE_LARS) {
             if (scaled) {
                 const double wn = sqrt(o.w_sq), gn = sqrt(o.g_sq);
@@ -512,7 +515,11 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         o.coef_b = cb;
         a.coef[l] = make_float2((float)ca, (float)cb);
         if (updated) {
-            const double ap = (a.mode == AGS_MODE_AGS && scaled && !pred) ? gs_old : 1.0;
+            double ap = 1.0;
+            if (scaled && !pred) {
+                if (a.mode == AGS_MODE_AGS) ap = gs_old;
+                else if (a.mode == AGS_MODE_STATIC) ap = a.static_scale;
+            }
             const float c = (float)ca - (float)ap;
             a.corr[l] = c;
             need |= (c != 0.0f);
@@ -601,7 +608,10 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     if (UPD) {
         const uint32_t f = a.layers[l].flags;
         const bool pred = surely_sensitive(a.state->g_prev, a.state->step);
-        if (a.mode == AGS_MODE_AGS && (f & AGS_LAYER_SCALE) && !pred) ca = (float)a.gradscale[l];
+        if ((f & AGS_LAYER_SCALE) && !pred) {
+            if (a.mode == AGS_MODE_AGS) ca = (float)a.gradscale[l];
+            else if (a.mode == AGS_MODE_STATIC) ca = (float)a.static_scale;
+        }
         cb = (f & AGS_LAYER_DECAY) ? (float)a.weight_decay : 0.0f;
     }
 

@@ -46,7 +46,7 @@ def test_struct_sizes_match_the_header():
     assert ctypes.sizeof(ags.ags_layer) == 24
     assert ctypes.sizeof(ags.ags_layer_stats) == 64
     assert ctypes.sizeof(ags.ags_global_stats) == 40
-    assert ctypes.sizeof(ags.ags_config) == 4 + 4 + 8 + 8 + 4 + 4 + 4 + 4 + 7 * 8 + 4 + 4
+    assert ctypes.sizeof(ags.ags_config) == 4 + 4 + 8 + 8 + 4 + 4 + 4 + 4 + 7 * 8 + 4 + 4 + 8
 
 
 def test_status_strings(lib):
@@ -106,6 +106,8 @@ def test_valid_config_workspace_size(lib):
     (dict(eps=-1e-8), ags.AGS_E_ARG),
     (dict(s_max=float("nan")), ags.AGS_E_ARG),
     (dict(mode="lars", trust_coef=0.0), ags.AGS_E_ARG),
+    (dict(mode="static", static_scale=0.0), ags.AGS_E_ARG),
+    (dict(mode="static", static_scale=float("inf")), ags.AGS_E_ARG),
     (dict(refresh_every=-1), ags.AGS_E_ARG),
     (dict(small_replica=4), ags.AGS_E_ARG),
     (dict(small_replica=-2), ags.AGS_E_ARG),

@@ -32,7 +32,7 @@ def gpu():
 # ------------------------------------------------------------ the configs --
 
 
-@pytest.mark.parametrize("mode", ["ags", "lars", "sgd"])
+@pytest.mark.parametrize("mode", ["ags", "lars", "sgd", "static"])
 def test_tiny_cnn_k4_three_steps(mode):
     lay = layouts.get_layout("tiny_cnn")
     run_steps(lay, 4, 3, mode=mode, label=f"tiny {mode}")
@@ -41,6 +41,12 @@ def test_tiny_cnn_k4_three_steps(mode):
 def test_resnet18_cifar_k8_one_step():
     lay = layouts.get_layout("resnet18_cifar")
     run_steps(lay, 8, 1, label="r18")
+
+
+def test_resnet18_cifar_static_scaling_three_steps():
+    # Static mapping U(s), s = 4 (one of the paper's s in {2, 4, 8, 16}).
+    lay = layouts.get_layout("resnet18_cifar")
+    run_steps(lay, 8, 3, mode="static", static_scale=4.0, label="r18 static")
 
 
 def test_resnet50_k16_bf16_ten_steps():
@@ -160,15 +166,16 @@ def test_forced_spike_takes_unscaled_branch():
     p.close()
 
 
-@pytest.mark.parametrize("K,dtype", [(4, "f32"), (16, "bf16"), (3, "bf16")])
-def test_mispredicted_steps_are_corrected(K, dtype):
+@pytest.mark.parametrize("K,dtype,mode", [(4, "f32", "ags"), (16, "bf16", "ags"),
+                                          (3, "bf16", "ags"), (8, "f32", "static")])
+def test_mispredicted_steps_are_corrected(K, dtype, mode):
     """AGS steps are applied with the coefficients predicted before the step
     (scaled unless Delta is infinite by definition); a sensitive step then
     takes the correction pass.  Gradient scales 1, 1, 2, 2, 0.25, 0.25, 1, 1
     make steps 1, 3, 5 and 7 sensitive (Delta = inf, 3, 0.9375, 15)."""
     lay = layouts.custom_layout(RAGGED, pad=8)
     base = synth.replica_grads(lay, K, 0, 4, dtype="f32")
-    p = Pair(lay, K, dtype=dtype, seed=4)
+    p = Pair(lay, K, dtype=dtype, seed=4, mode=mode, static_scale=3.0)
     sens = []
     for t, c in enumerate([1, 1, 2, 2, 0.25, 0.25, 1, 1]):
         g = (base * np.float32(c)).astype(np.float32)

@@ -568,3 +568,34 @@ def test_oracle_reproduces_golden_fixture():
             assert (gl[k] == v) or abs(gl[k] - v) <= 1e-14 * abs(v), (t, k)
         np.testing.assert_allclose(o.w[idx], step["w"], rtol=1e-14, atol=0)
         np.testing.assert_allclose(o.m[idx], step["m"], rtol=1e-14, atol=0)
+
+
+def test_static_scaling_matches_torch_with_prescaled_gradients():
+    """Static mapping U(s) (Eq. (8a), (8b)): gradients scaled by s on the
+    non-sensitive steps of scaled layers, 1 otherwise.  Step scales
+    1, 1.125, 2, 2 give Delta = inf, 0.265625, 2.16, 0 (sensitive, scaled,
+    sensitive, scaled), so torch.optim.SGD sees s * G on steps 2 and 4."""
+    rng = np.random.default_rng(21)
+    K, s_fixed = 3, 4.0
+    flags = [SD, layouts.LAYER_DECAY, SD, layouts.LAYER_SCALE]
+    lay, table = _layers([40, 24, 64, 9], flags)
+    w0 = np.zeros(lay.n_flat, np.float32)
+    base = np.zeros((K, lay.n_flat), np.float32)
+    for o, n, _ in table:
+        w0[o:o + n] = rng.standard_normal(n)
+        base[:, o:o + n] = _coarse(rng.standard_normal((K, n)))
+    grads = [(np.float32(c) * base).astype(np.float32) for c in (1.0, 1.125, 2.0, 2.0)]
+    o = OracleAGS(table, lay.n_flat, K, w0, mode="static", static_scale=s_fixed, lr=0.05,
+                  momentum=0.9, weight_decay=5e-4)
+    sens, scales = [], []
+    for g in grads:
+        st, gl = o.step(g)
+        sens.append(gl["sensitive"])
+        scales.append([s_fixed if (not gl["sensitive"] and f & layouts.LAYER_SCALE) else 1.0
+                       for _, _, f in table])
+        np.testing.assert_array_equal(st["coef_a"], scales[-1])
+        np.testing.assert_array_equal(st["gradscale"], 1.0)   # no refresh in this mode
+    assert sens == [1, 0, 1, 0]
+    w_ref, m_ref = _torch_sgd_run(w0, lay, grads, 0.05, 0.9, 5e-4, scales)
+    np.testing.assert_allclose(o.w, w_ref, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(o.m, m_ref, rtol=1e-12, atol=1e-14)
