@@ -705,11 +705,14 @@ __device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __r
     load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
     load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
     moments<GT, KT, 0, FULL>(g, a.stride, idx, n0, n1, K, 0, a.invK, gb, dv, gr);
+    // One rounding each: m + c gbar and w - (eta c) gbar as fused
+    // multiply-adds (the applied m already carries the rounding of the
+    // predicted step; a second rounding of c gbar would double it).
+    const float lc = -a.lr * c;
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
-        const float cg = c * gb[e];
-        mv[e] += cg;
-        wv[e] = fmaf(-a.lr, cg, wv[e]);
+        mv[e] = fmaf(c, gb[e], mv[e]);
+        wv[e] = fmaf(lc, gb[e], wv[e]);
     }
     store_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
     store_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
