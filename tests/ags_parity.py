@@ -3,8 +3,12 @@ oracle on the same seeded input bytes.  Test infrastructure only.
 
 Tolerances:
 * parameters and momentum, per element:
-    |x - y| <= 1e-5 * max(|y|, rms_l(y)),  rms_l = oracle RMS of layer l
-  (relative error of fp32 parameters, guarded near zero by the layer scale);
+    |x - y| <= 1e-5 * max(|y|, rms_l(y), |y_prev|)
+  with rms_l the oracle RMS of layer l and y_prev the oracle's value before
+  the step (relative error of fp32 state, guarded near zero by the layer
+  scale; a new w or m is a sum whose largest term has the size of the
+  previous value, and an fp32 sum's rounding is relative to that term, which
+  matters where the terms cancel in a layer of one or a few elements);
 * statistics (W, G, V, S, rho, a, b, gradscale, global G and Delta):
     |x - y| <= 1e-4 * |y|, and exact where the oracle's value is exactly 0
   (the spread of identical replicas, a single replica) or infinite;
@@ -39,14 +43,18 @@ def to_device(arr: np.ndarray):
     return torch.from_numpy(np.ascontiguousarray(arr)).cuda()
 
 
-def check_params(x: np.ndarray, y: np.ndarray, table, what: str, rtol: float = PARAM_RTOL):
-    """Per-element check with the layer-RMS guard; returns the worst ratio."""
+def check_params(x: np.ndarray, y: np.ndarray, table, what: str, rtol: float = PARAM_RTOL,
+                 y_prev: np.ndarray | None = None):
+    """Per-element check with the layer-RMS and previous-value guards;
+    returns the worst error over tolerance scale."""
     worst = 0.0
     for l, (o, n, _) in enumerate(table):
         yy = y[o:o + n]
         xx = x[o:o + n].astype(np.float64)
         rms = math.sqrt(float(np.mean(yy * yy)))
         scale = np.maximum(np.abs(yy), rms)
+        if y_prev is not None:
+            scale = np.maximum(scale, np.abs(y_prev[o:o + n]))
         err = np.abs(xx - yy)
         bad = err > rtol * scale
         if np.any(~np.isfinite(xx)) or np.any(bad):
@@ -108,6 +116,7 @@ class Pair:
 
     def step(self, grads: np.ndarray, commit=True, check=True, what=""):
         g = to_device(grads)
+        self.prev_w, self.prev_m = self.ora.w.copy(), self.ora.m.copy()
         if commit:
             self.gpu.step(g)
             ol, og = self.ora.step(grads)
@@ -123,8 +132,9 @@ class Pair:
         self.torch.cuda.synchronize()
         w = self.w.cpu().numpy()
         m = self.m.cpu().numpy()
-        rw = check_params(w, self.ora.w, self.table, what + " w")
-        rm = check_params(m, self.ora.m, self.table, what + " m")
+        pw, pm = getattr(self, "prev_w", None), getattr(self, "prev_m", None)
+        rw = check_params(w, self.ora.w, self.table, what + " w", y_prev=pw)
+        rm = check_params(m, self.ora.m, self.table, what + " m", y_prev=pm)
         gs, gp, st = self.gpu.get_state()
         ogs, ogp, ost = self.ora.get_state()
         assert st == ost
