@@ -40,7 +40,8 @@ class _Config(ctypes.Structure):
                 ("lr", ctypes.c_double), ("momentum", ctypes.c_double),
                 ("weight_decay", ctypes.c_double), ("delta", ctypes.c_double),
                 ("eps", ctypes.c_double), ("s_max", ctypes.c_double),
-                ("trust_coef", ctypes.c_double), ("static_scale", ctypes.c_double)]
+                ("trust_coef", ctypes.c_double), ("static_scale", ctypes.c_double),
+                ("elementwise", ctypes.c_int32), ("pad_", ctypes.c_int32)]
 
 
 def build(force: bool = False) -> str:
@@ -79,7 +80,7 @@ class OracleAGS:
     def __init__(self, layers, n_flat, K, w0, m0=None, *, mode="ags",
                  grad_dtype="f32", lr=0.1, momentum=0.9, weight_decay=5e-4,
                  delta=0.5, eps=1e-8, s_max=0.0, trust_coef=1e-3, static_scale=2.0,
-                 refresh_every=1, small_replica=0):
+                 refresh_every=1, small_replica=0, elementwise=False):
         self.lib = _load()
         self.layers = [(int(o), int(n), int(f)) for o, n, f in layers]
         self.L = len(self.layers)
@@ -88,14 +89,15 @@ class OracleAGS:
         self.grad_dtype = grad_dtype
         self.cfg = dict(mode=mode, lr=lr, momentum=momentum, weight_decay=weight_decay,
                         delta=delta, eps=eps, s_max=s_max, trust_coef=trust_coef,
-                        static_scale=static_scale,
+                        static_scale=static_scale, elementwise=bool(elementwise),
                         refresh_every=refresh_every, small_replica=small_replica)
         self.w = np.array(w0, dtype=np.float64, copy=True).reshape(-1)
         self.m = (np.zeros(self.n_flat) if m0 is None
                   else np.array(m0, dtype=np.float64, copy=True).reshape(-1))
         if self.w.size != self.n_flat or self.m.size != self.n_flat:
             raise ValueError("w/m size does not match n_flat")
-        self.gradscale = np.ones(self.L)
+        # one scale per layer, or per element of the flat buffer
+        self.gradscale = np.ones(self.n_flat if elementwise else self.L)
         self.g_prev = ctypes.c_double(0.0)
         self.step_count = ctypes.c_int64(0)
         arr = (_Layer * max(self.L, 1))()
@@ -133,7 +135,8 @@ class OracleAGS:
                       weight_decay=float(c["weight_decay"]), delta=float(c["delta"]),
                       eps=float(c["eps"]), s_max=float(c["s_max"]),
                       trust_coef=float(c["trust_coef"]),
-                      static_scale=float(c["static_scale"]))
+                      static_scale=float(c["static_scale"]),
+                      elementwise=int(c["elementwise"]))
         out_l = np.zeros((self.L, len(LAYER_FIELDS)))
         out_g = np.zeros(len(GLOBAL_FIELDS))
         rc = self.lib.oracle_ags_step(

@@ -82,9 +82,13 @@ typedef struct {
     int64_t replica_stride;
     double lr, momentum, weight_decay, delta, eps, s_max, trust_coef;
     double static_scale; /* s of the static mapping U(s) */
+    int32_t elementwise; /* AGS scale per element instead of per layer */
+    int32_t pad_;
 } oracle_config;
 
-/* Per-layer output record: W, G, V, S, rho, a, b, gradscale (after refresh). */
+/* Per-layer output record: W, G, V, S, rho, a, b, gradscale (after refresh).
+ * With elementwise scales, a is the layer mean of the coefficients applied
+ * to its elements and gradscale the layer mean of its scales. */
 enum { OUT_W = 0, OUT_G, OUT_V, OUT_S, OUT_RHO, OUT_A, OUT_B, OUT_GRADSCALE, OUT_N };
 /* Global output record: G, G_prev (value used), Delta, sensitive, nonfinite. */
 enum { GOUT_G = 0, GOUT_GPREV, GOUT_DELTA, GOUT_SENSITIVE, GOUT_NONFINITE, GOUT_N };
@@ -103,7 +107,8 @@ static double grad_at(const oracle_config *c, const void *grads, int k, int64_t 
 
 /*
  * One step.  w, m: float64 state [n_flat], updated in place when commit != 0.
- * gradscale [n_layers], *g_prev, *step: AGS state, updated when commit != 0.
+ * gradscale [n_layers] (or [n_flat] with elementwise scales), *g_prev, *step:
+ * AGS state, updated when commit != 0.
  * out_layers [n_layers][OUT_N], out_global [GOUT_N].
  * Returns 0, or -1 on a bad argument, -2 when out of memory.
  */
@@ -218,12 +223,28 @@ int oracle_ags_step(const oracle_config *c, double *w, double *m, const void *gr
         out[OUT_B] = b;
     }
 
+    /* Elementwise AGS (Algorithm 1 read per element): element j of a scaled
+     * layer takes gradscale_j on a non-sensitive step.  The layer record
+     * gets the mean of the coefficients applied. */
+    const int ew = c->mode == ORACLE_AGS && c->elementwise;
+    if (ew) {
+        for (int l = 0; l < L; ++l) {
+            const int64_t o = layers[l].offset, n = layers[l].numel;
+            const int scaled = (layers[l].flags & ORACLE_SCALE) != 0;
+            double sum = 0.0;
+            for (int64_t j = 0; j < n; ++j) sum += (scaled && !sensitive) ? gradscale[o + j] : 1.0;
+            out_layers[(size_t)l * OUT_N + OUT_A] = sum / (double)n;
+        }
+    }
+
     /* Step 5: momentum SGD on d = a gbar + b w. */
     if (commit) {
         for (int l = 0; l < L; ++l) {
             const int64_t o = layers[l].offset, n = layers[l].numel;
+            const int scaled = (layers[l].flags & ORACLE_SCALE) != 0;
             for (int64_t j = 0; j < n; ++j) {
-                const double d = a_l[l] * gbar_keep[l][j] + b_l[l] * w[o + j];
+                const double a = ew ? ((scaled && !sensitive) ? gradscale[o + j] : 1.0) : a_l[l];
+                const double d = a * gbar_keep[l][j] + b_l[l] * w[o + j];
                 m[o + j] = c->momentum * m[o + j] + d;
                 w[o + j] = w[o + j] - c->lr * m[o + j];
             }
@@ -236,6 +257,35 @@ int oracle_ags_step(const oracle_config *c, double *w, double *m, const void *gr
                         (t % c->refresh_every) == 0;
     for (int l = 0; l < L; ++l) {
         double *out = out_layers + (size_t)l * OUT_N;
+        if (ew) {
+            /* Per element: s_j = min(|g_small,j / (gbar_j + eps)|, s_max), with
+             * g_small = replica r, or the root mean square over replicas
+             * (r = -1); a 0/0 ratio gives 1. */
+            const int64_t o = layers[l].offset, n = layers[l].numel;
+            if (refresh && (layers[l].flags & ORACLE_SCALE)) {
+                for (int64_t j = 0; j < n; ++j) {
+                    double gs;
+                    if (c->small_replica >= 0) {
+                        gs = grad_at(c, grads, c->small_replica, o + j);
+                    } else {
+                        double q = 0.0;
+                        for (int k = 0; k < K; ++k) {
+                            const double g = grad_at(c, grads, k, o + j);
+                            q += g * g;
+                        }
+                        gs = sqrt(q / K);
+                    }
+                    double s = fabs(gs / (gbar_keep[l][j] + c->eps));
+                    if (isnan(s)) s = 1.0;
+                    if (s > smax) s = smax;
+                    gradscale[o + j] = s;
+                }
+            }
+            double sum = 0.0;
+            for (int64_t j = 0; j < n; ++j) sum += gradscale[o + j];
+            out[OUT_GRADSCALE] = sum / (double)n;
+            continue;
+        }
         if (refresh && (layers[l].flags & ORACLE_SCALE)) {
             const double S = out[OUT_S], Gl = out[OUT_G];
             double s;

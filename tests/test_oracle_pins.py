@@ -599,3 +599,124 @@ def test_static_scaling_matches_torch_with_prescaled_gradients():
     w_ref, m_ref = _torch_sgd_run(w0, lay, grads, 0.05, 0.9, 5e-4, scales)
     np.testing.assert_allclose(o.w, w_ref, rtol=1e-12, atol=1e-14)
     np.testing.assert_allclose(o.m, m_ref, rtol=1e-12, atol=1e-14)
+
+
+# --------------------------------------------------------------------------
+# elementwise AGS: one scale per element, min(|g_small,j / (gbar_j + eps)|, s_max)
+
+
+def _brute_elementwise(w, grads_steps, lr, mu, lam, delta, s_max):
+    """Exact rational AGS with one scale per element (K = 2, eps = 0, r = 0)."""
+    w = [_q(x) for x in w]
+    n = len(w)
+    m = [Fraction(0)] * n
+    scale = [Fraction(1)] * n
+    g_prev = None
+    for t, g in enumerate(grads_steps, start=1):
+        gb = [(_q(g[0][j]) + _q(g[1][j])) / 2 for j in range(n)]
+        G = sum(x * x for x in gb)
+        sens = True
+        if t > 1 and g_prev > 0:
+            sens = not (abs((G - g_prev) / g_prev) < delta)
+        for j in range(n):
+            a = scale[j] if not sens else Fraction(1)
+            d = a * gb[j] + lam * w[j]
+            m[j] = mu * m[j] + d
+            w[j] = w[j] - lr * m[j]
+        scale = [min(abs(_q(g[0][j]) / gb[j]), s_max) for j in range(n)]
+        g_prev = G
+    return w, m, scale
+
+
+def test_elementwise_bruteforce_three_steps_exact():
+    # g0_j = alpha_j u_j, g1_j = beta_j u_j: the ratio |g0 / gbar| is
+    # 2 alpha / (alpha + beta) per element (0.5, 1.5, 1, 2.5 -> clipped to 2,
+    # 0 -> an element that scaled steps do not move, 0.25).
+    u = np.array([1, -2, 3, 0.5, -0.25, 4, -1, 2], np.float32)
+    alpha = np.array([1, 3, 1, 5, 0, 1, 3, 1], np.float32)
+    beta = np.array([3, 1, 1, -1, 2, 7, 1, 3], np.float32)
+    g = np.stack([alpha * u, beta * u]).astype(np.float32)
+    steps = [g, g, (2 * g).astype(np.float32)]
+    w0 = np.array([0.5, 1, -1, 2, 0.25, -0.5, 3, -2], np.float32)
+    lr, mu, lam, delta = Fraction(1, 10), Fraction(9, 10), Fraction(1, 2000), Fraction(1, 2)
+    wq, mq, sq = _brute_elementwise(w0, steps, lr, mu, lam, delta, Fraction(2))
+    o = OracleAGS([(0, 8, SD)], 8, 2, w0, lr=0.1, momentum=0.9, weight_decay=5e-4, delta=0.5,
+                  eps=0.0, s_max=2.0, refresh_every=1, elementwise=True)
+    sens = [o.step(gs)[1]["sensitive"] for gs in steps]
+    assert sens == [1, 0, 1]
+    np.testing.assert_allclose(o.gradscale, [float(x) for x in sq], rtol=1e-15)
+    np.testing.assert_allclose(o.w, [float(x) for x in wq], rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(o.m, [float(x) for x in mq], rtol=1e-14, atol=1e-15)
+
+
+def test_elementwise_matches_torch_with_prescaled_gradients():
+    """Non-sensitive steps feed torch.optim.SGD with s_j * gbar_j on scaled
+    layers, s_j refreshed from the previous step (numpy, float64)."""
+    rng = np.random.default_rng(31)
+    K, eps = 4, 1e-8
+    flags = [SD, layouts.LAYER_DECAY, SD, layouts.LAYER_SCALE]
+    lay, table = _layers([40, 24, 64, 9], flags)
+    w0 = np.zeros(lay.n_flat, np.float32)
+    base = np.zeros((K, lay.n_flat), np.float32)
+    for o, n, _ in table:
+        w0[o:o + n] = rng.standard_normal(n)
+        base[:, o:o + n] = _coarse(rng.standard_normal((K, n)))
+    grads = [(np.float32(c) * base).astype(np.float32) for c in (1.0, 1.125, 2.0, 2.0)]
+    o = OracleAGS(table, lay.n_flat, K, w0, lr=0.05, momentum=0.9, weight_decay=5e-4,
+                  eps=eps, refresh_every=1, small_replica=0, elementwise=True)
+    scale = np.ones(lay.n_flat)
+    scales_applied, sens = [], []
+    for g in grads:
+        st, gl = o.step(g)
+        sens.append(gl["sensitive"])
+        applied = np.ones(lay.n_flat)
+        if not gl["sensitive"]:
+            for oo, n, f in table:
+                if f & layouts.LAYER_SCALE:
+                    applied[oo:oo + n] = scale[oo:oo + n]
+        for l, (oo, n, f) in enumerate(table):
+            assert abs(st["coef_a"][l] - applied[oo:oo + n].mean()) < 1e-12
+        scales_applied.append(applied)
+        g64 = g.astype(np.float64)
+        gbar = g64.mean(axis=0)
+        new = scale.copy()
+        for oo, n, f in table:
+            if f & layouts.LAYER_SCALE:
+                r = np.abs(g64[0, oo:oo + n] / (gbar[oo:oo + n] + eps))
+                new[oo:oo + n] = np.minimum(r, math.sqrt(K))
+        scale = new
+        np.testing.assert_allclose(o.gradscale, scale, rtol=1e-12)
+        for l, (oo, n, _) in enumerate(table):
+            assert abs(st["gradscale"][l] - scale[oo:oo + n].mean()) < 1e-12
+    assert sens == [1, 0, 1, 0]
+    # torch.optim.SGD with the per-element scales folded into the gradient
+    params, groups = [], []
+    for oo, n, f in table:
+        p = torch.tensor(np.asarray(w0[oo:oo + n], np.float64), requires_grad=True)
+        params.append(p)
+        groups.append({"params": [p], "weight_decay": 5e-4 if f & layouts.LAYER_DECAY else 0.0})
+    opt = torch.optim.SGD(groups, lr=0.05, momentum=0.9)
+    for g, sc in zip(grads, scales_applied):
+        gm = g.astype(np.float64).mean(axis=0) * sc
+        for l, (oo, n, _) in enumerate(table):
+            params[l].grad = torch.tensor(gm[oo:oo + n])
+        opt.step()
+    for l, (oo, n, _) in enumerate(table):
+        np.testing.assert_allclose(o.w[oo:oo + n], params[l].detach().numpy(), rtol=1e-12,
+                                   atol=1e-14)
+
+
+def test_elementwise_rms_small_batch_and_zero_rules():
+    # r = -1: g_small,j = sqrt(mean_k g_kj^2).  All-zero replicas: 0/0 -> 1
+    # with eps = 0, and 0/eps = 0 with eps > 0.
+    g = np.zeros((3, 8), np.float32)
+    g[:, 0] = [1.0, 2.0, 3.0]
+    g[:, 1] = [1.0, -1.0, 0.5]
+    for eps, zero_scale in ((0.0, 1.0), (1e-8, 0.0)):
+        o = OracleAGS([(0, 8, SD)], 8, 3, np.ones(8), eps=eps, s_max=10.0, small_replica=-1,
+                      elementwise=True)
+        o.step(g)
+        rms0, rms1 = math.sqrt(14 / 3), math.sqrt(2.25 / 3)
+        assert abs(o.gradscale[0] - rms0 / (2.0 + eps)) < 1e-12
+        assert abs(o.gradscale[1] - rms1 / (0.5 / 3 + eps)) < 1e-9
+        assert np.all(o.gradscale[2:] == zero_scale)
