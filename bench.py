@@ -21,8 +21,12 @@ Prints one JSON line (last line of stdout):
   cpu_baseline   the float64 oracle on the host on whole steps of the same
                  workload (a reported baseline, not a target)
 
+With --elementwise the scale of Algorithm 1 is kept per parameter element
+(AGS mode): a step also reads the scales in force and writes the refreshed
+ones, (K*2 + 24) bytes per parameter.
+
 Usage: python bench.py [--gpus 1] [--steps 200] [--warmup 20]
-                       [--no-cpu-baseline] [--copy-probe]
+                       [--no-cpu-baseline] [--copy-probe] [--elementwise]
 """
 from __future__ import annotations
 
@@ -70,7 +74,7 @@ def kernel_source_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(n_params: int, mode: str = "ags"):
+def algorithmic_bytes(n_params: int, mode: str = "ags", elementwise: bool = False):
     """Per-launch algorithmic bytes of each kernel and of the whole step.
 
     A step reads every replica once and reads and writes w and m once:
@@ -80,8 +84,10 @@ def algorithmic_bytes(n_params: int, mode: str = "ags"):
     sensitive bit is predicted right.  A LARS step reads the replicas and w
     in the step kernel (and writes the replica mean when K * e_g > 8), then
     reads w, m and the mean (or the replicas again) and writes w, m in the
-    update pass."""
-    step = n_params * (K * E_G + 16)
+    update pass.  Element scales add a 4-byte read of the scale in force and
+    a 4-byte write of the refreshed one per parameter (refresh every step,
+    scales applied: the steps timed here)."""
+    step = n_params * (K * E_G + 16 + (8 if elementwise else 0))
     if mode != "lars":
         return {"step": step, "finalize": 0, "second_pass": 0, "whole_step": step}
     mat = K * E_G > 8
@@ -92,6 +98,10 @@ def algorithmic_bytes(n_params: int, mode: str = "ags"):
 
 def traffic_file(workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+
+
+def workload_key(workload: str, elementwise: bool) -> str:
+    return workload + ("_elementwise" if elementwise else "")
 
 
 def read_traffic(workload: str, kernel: str):
@@ -158,7 +168,12 @@ def main():
                     help="also time the step captured once in a HIP graph and replayed")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB device copy (counter calibration)")
+    ap.add_argument("--elementwise", action="store_true",
+                    help="AGS with one scale per parameter element")
     args = ap.parse_args()
+    if args.elementwise and args.mode != "ags":
+        print("--elementwise needs --mode ags", file=sys.stderr)
+        sys.exit(2)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the hot path measured here is the "
               f"single-GPU AGS step (got --gpus {args.gpus}).", file=sys.stderr)
@@ -181,6 +196,8 @@ def main():
     global K, E_G
     layout_name, K, gdt, desc = WORKLOADS[args.workload]
     E_G = 2 if gdt == "bf16" else 4
+    HYPER["elementwise"] = bool(args.elementwise)
+    wkey = workload_key(args.workload, args.elementwise)
     lib = ags.load_library()
     log(f"libags: {ags.library_path()}")
     lay = layouts.get_layout(layout_name)
@@ -281,14 +298,14 @@ def main():
         log(f"graph replay: {graph_ms * 1e3:.1f} us/step")
     s = h.read_stats()
 
-    ab = algorithmic_bytes(N, args.mode)
+    ab = algorithmic_bytes(N, args.mode, args.elementwise)
     value = ab["whole_step"] / (ms_step * 1e-3) / 1e9
     avg_ms = {n: kms[i] / ncalls for i, n in enumerate(ags.KERNEL_NAMES)}
     dom = max(avg_ms, key=avg_ms.get)
     achieved = ab[dom] / (avg_ms[dom] * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                "traffic": read_traffic(args.workload, dom),
+                "traffic": read_traffic(wkey, dom),
                 "algorithmic_bytes_per_launch": ab[dom],
                 "avg_launch_us": round(avg_ms[dom] * 1e3, 2)}
 
@@ -301,12 +318,13 @@ def main():
         sec, n = cpu_baseline(lay, w0, g_np)
         cpu = {"value": round(ab["whole_step"] / sec / 1e9, 3), "unit": "GB/s", "cores": 1,
                "kind": "oracle", "sec_per_step": round(sec, 3),
-               "sample": f"median of {n} whole steps of {args.workload}, float64, 1 thread"}
+               "sample": f"median of {n} whole steps of {wkey}, float64, 1 thread"}
         log(f"cpu baseline: {sec:.2f} s/step")
 
     out = {
         "metric": ("AGS step+stats GB/s & % HBM peak (ResNet-50 layout, K=16); steps/s"
-                   if args.workload == WORKLOAD else f"AGS step+stats GB/s ({desc})"),
+                   if wkey == WORKLOAD else
+                   f"AGS step+stats GB/s ({desc}{', elementwise scales' if args.elementwise else ''})"),
         "value": round(value, 1),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -320,9 +338,10 @@ def main():
         "vs_baseline": None,
         "dtype": gdt,
         "data": "synthetic",
-        "config": {"workload": args.workload, "layout": layout_name, "tensors": lay.n_layers,
+        "config": {"workload": wkey, "layout": layout_name, "tensors": lay.n_layers,
                    "params": N, "K": K, "grad_dtype": gdt, "param_dtype": "f32",
-                   "mode": args.mode, "algorithmic_bytes_per_step": ab["whole_step"],
+                   "mode": args.mode, "elementwise": bool(args.elementwise),
+                   "algorithmic_bytes_per_step": ab["whole_step"],
                    "parallelism": "single GPU (K replicas stand in for K data-parallel workers)"},
         "kernel_us": {n: round(v * 1e3, 2) for n, v in avg_ms.items()},
         "cold_cache": {"ms_per_step": round(cold_step, 5),

@@ -35,6 +35,17 @@
  *        SGD   a_l = 1; b_l = lambda_l.
  * lambda_l is weight_decay on layers with AGS_LAYER_DECAY, else 0.
  *
+ * Elementwise AGS (cfg.elementwise = 1, AGS mode only) reads the scale of
+ * Algorithm 1 per parameter element instead of per tensor: element j of a
+ * scaled layer gets a_j = gradscale_j on a non-sensitive step (else 1), and
+ * the refresh sets gradscale_j = min(|g_small,j / (gbar_j + eps)|, s_max),
+ * where g_small,j is replica r's element (or, with small_replica = -1, the
+ * root mean square of the K replicas' elements) and a 0/0 ratio gives 1.
+ * The denominator gbar_j + eps is formed from an fp64 sum of the replicas,
+ * so that its cancellation does not decide the ratio.  The per-layer records
+ * then hold layer means: coef_a the mean coefficient applied, gradscale the
+ * mean scale after the call.
+ *
  * Conventions for every function:
  *  - C linkage; every function returns an ags_status (0 = AGS_OK) except
  *    where noted; nothing throws across the ABI.
@@ -46,8 +57,9 @@
  *    not), so that a bad pointer is an error, not a GPU fault.
  *  - Work is enqueued on hip_stream (a hipStream_t; NULL is the default
  *    stream) and the call returns without waiting, except ags_read_stats,
- *    ags_get_state, ags_set_state and ags_get_kernel_times, which wait for
- *    the handle's last stream.
+ *    ags_get_state, ags_set_state, ags_get_elementwise_scale,
+ *    ags_set_elementwise_scale and ags_get_kernel_times, which wait for the
+ *    handle's last stream.
  *  - A handle is not thread-safe: one thread at a time.
  */
 #ifndef AGS_H
@@ -112,6 +124,8 @@ typedef struct {
     int32_t small_replica;   /* replica r taken as the small-batch gradient;
                                 -1 = mean over replicas of ||g_k||^2        */
     double static_scale;     /* s of AGS_MODE_STATIC (> 0)                 */
+    int32_t elementwise;     /* 1: AGS scale per element (AGS mode only)    */
+    int32_t reserved;        /* must be 0                                   */
 } ags_config;
 
 /* Per-layer record of the last ags_stats / ags_step.  var is V_l (the 1/K
@@ -176,11 +190,25 @@ ags_status ags_read_stats(ags_handle *h, ags_layer_stats *out_layers,
 ags_status ags_set_lr(ags_handle *h, double lr);
 
 /* Checkpoint / resume of the AGS state (w and m are the caller's).
- * gradscale_L: host [n_layers]. */
+ * gradscale_L: host [n_layers].  With elementwise scales, ags_get_state
+ * writes the layer means of the element scales to gradscale_L, and
+ * ags_set_state sets G_prev and the step count only (gradscale_L may be
+ * NULL and is not read): the element scales are restored with
+ * ags_set_elementwise_scale. */
 ags_status ags_get_state(ags_handle *h, double *gradscale_L, double *g_sq_prev,
                          int64_t *step);
 ags_status ags_set_state(ags_handle *h, const double *gradscale_L, double g_sq_prev,
                          int64_t step);
+
+/* Elementwise scales gradscale_j (Algorithm 1 read per element; handles
+ * created with cfg.elementwise = 1, else AGS_E_STATE).  scale: host fp32
+ * [n], n == n_flat (AGS_E_ARG otherwise); entries outside every layer are
+ * carried but never used.  Get waits for the handle's last stream.  Set
+ * checks every value is finite and >= 0 (AGS_E_ARG, nothing changed),
+ * waits for the last stream, copies the array and recomputes the layer
+ * means in fp64. */
+ags_status ags_get_elementwise_scale(ags_handle *h, float *scale, int64_t n);
+ags_status ags_set_elementwise_scale(ags_handle *h, const float *scale, int64_t n);
 
 /* Per-kernel timing with HIP events on the launch stream: enable, then
  * read the summed milliseconds per kernel (out_ms [AGS_N_KERNELS]) and the

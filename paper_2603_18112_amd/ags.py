@@ -50,7 +50,8 @@ class ags_config(ctypes.Structure):
                 ("weight_decay", ctypes.c_double), ("delta", ctypes.c_double),
                 ("eps", ctypes.c_double), ("s_max", ctypes.c_double),
                 ("trust_coef", ctypes.c_double), ("refresh_every", ctypes.c_int32),
-                ("small_replica", ctypes.c_int32), ("static_scale", ctypes.c_double)]
+                ("small_replica", ctypes.c_int32), ("static_scale", ctypes.c_double),
+                ("elementwise", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class ags_layer_stats(ctypes.Structure):
@@ -67,7 +68,8 @@ class ags_global_stats(ctypes.Structure):
 LAYER_STATS_FIELDS = tuple(n for n, _ in ags_layer_stats._fields_)
 #: every function the header declares
 EXPORTS = ("ags_workspace_bytes", "ags_init", "ags_stats", "ags_step", "ags_read_stats",
-           "ags_set_lr", "ags_get_state", "ags_set_state", "ags_set_profiling",
+           "ags_set_lr", "ags_get_state", "ags_set_state", "ags_get_elementwise_scale",
+           "ags_set_elementwise_scale", "ags_set_profiling",
            "ags_get_kernel_times", "ags_status_string", "ags_last_error", "ags_destroy")
 
 _lib = None
@@ -111,6 +113,8 @@ def load_library(path: str | None = None):
         "ags_set_lr": (c_int, [h, c_dbl]),
         "ags_get_state": (c_int, [h, vp, P(c_dbl), P(c_i64)]),
         "ags_set_state": (c_int, [h, vp, c_dbl, c_i64]),
+        "ags_get_elementwise_scale": (c_int, [h, vp, c_i64]),
+        "ags_set_elementwise_scale": (c_int, [h, vp, c_i64]),
         "ags_set_profiling": (c_int, [h, c_int]),
         "ags_get_kernel_times": (c_int, [h, vp, P(c_i64)]),
         "ags_status_string": (ctypes.c_char_p, [c_int]),
@@ -137,7 +141,7 @@ def _check(status: int, handle=None):
 
 def make_config(layers, n_flat, K, *, grad_dtype="f32", mode="ags", lr=0.1, momentum=0.9,
                 weight_decay=5e-4, delta=0.5, eps=1e-8, s_max=0.0, trust_coef=1e-3,
-                refresh_every=1, small_replica=0, static_scale=2.0):
+                refresh_every=1, small_replica=0, static_scale=2.0, elementwise=False):
     """An ags_config (plus the layer array it points to, kept alive on it)."""
     arr = (ags_layer * max(len(layers), 1))()
     for i, (o, n, f) in enumerate(layers):
@@ -147,7 +151,8 @@ def make_config(layers, n_flat, K, *, grad_dtype="f32", mode="ags", lr=0.1, mome
                      lr=float(lr), momentum=float(momentum), weight_decay=float(weight_decay),
                      delta=float(delta), eps=float(eps), s_max=float(s_max),
                      trust_coef=float(trust_coef), refresh_every=int(refresh_every),
-                     small_replica=int(small_replica), static_scale=float(static_scale))
+                     small_replica=int(small_replica), static_scale=float(static_scale),
+                     elementwise=int(bool(elementwise)), reserved=0)
     cfg._layers_keepalive = arr
     return cfg
 
@@ -204,8 +209,23 @@ def ags_get_state(handle, n_layers: int):
 
 
 def ags_set_state(handle, gradscale, g_sq_prev: float, step: int):
-    gs = np.ascontiguousarray(gradscale, dtype=np.float64)
-    _check(load_library().ags_set_state(handle, gs.ctypes.data, float(g_sq_prev), int(step)), handle)
+    if gradscale is None:
+        ptr = None
+    else:
+        gs = np.ascontiguousarray(gradscale, dtype=np.float64)
+        ptr = gs.ctypes.data
+    _check(load_library().ags_set_state(handle, ptr, float(g_sq_prev), int(step)), handle)
+
+
+def ags_get_elementwise_scale(handle, n: int):
+    out = np.empty(max(int(n), 1), np.float32)
+    _check(load_library().ags_get_elementwise_scale(handle, out.ctypes.data, int(n)), handle)
+    return out[:int(n)].copy()
+
+
+def ags_set_elementwise_scale(handle, scale):
+    a = np.ascontiguousarray(scale, dtype=np.float32).reshape(-1)
+    _check(load_library().ags_set_elementwise_scale(handle, a.ctypes.data, int(a.size)), handle)
 
 
 def ags_set_profiling(handle, enable: bool):
@@ -292,6 +312,12 @@ class AGS:
 
     def set_state(self, gradscale, g_sq_prev, step):
         ags_set_state(self.handle, gradscale, g_sq_prev, step)
+
+    def get_elementwise_scale(self):
+        return ags_get_elementwise_scale(self.handle, self.w.numel())
+
+    def set_elementwise_scale(self, scale):
+        ags_set_elementwise_scale(self.handle, scale)
 
     def set_profiling(self, enable=True):
         ags_set_profiling(self.handle, enable)

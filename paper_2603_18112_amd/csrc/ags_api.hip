@@ -32,6 +32,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // that a read-back is one copy.
 struct WsLayout {
     size_t gbar = 0, tiles = 0, partials = 0, ldev = 0, coef = 0, corr = 0, counters = 0;
+    size_t ew_buf = 0, ew_partials = 0;  // element scales: two [n_flat] fp32 buffers
     size_t chunks = 0, chunk_sums = 0, chunk_count = 0;
     size_t counters_bytes = 0;  // finished-layer counter, correction flag
     size_t lstats = 0, gstats = 0, gradscale = 0, state = 0, end = 0;
@@ -54,6 +55,13 @@ WsLayout ws_layout(const ags_config& c, int64_t n_tiles, int64_t n_chunks) {
     const size_t L = (size_t)c.n_layers;
     w.gbar = p;
     if (materialize_gbar(c)) p = align_up(p + (size_t)c.n_flat * sizeof(float));
+    w.ew_buf = p;
+    w.ew_partials = p;
+    if (c.elementwise) {
+        p = align_up(p + 2 * (size_t)c.n_flat * sizeof(float));
+        w.ew_partials = p;
+        p = align_up(p + (size_t)n_tiles * sizeof(float));
+    }
     w.tiles = p;
     p = align_up(p + (size_t)n_tiles * sizeof(Tile));
     w.partials = p;
@@ -69,7 +77,7 @@ WsLayout ws_layout(const ags_config& c, int64_t n_tiles, int64_t n_chunks) {
     w.chunk_count = p;
     p = align_up(p + L * sizeof(unsigned));
     w.corr = p;
-    p = align_up(p + L * sizeof(float));
+    p = align_up(p + L * sizeof(float2));
     w.counters = p;
     w.counters_bytes = 2 * sizeof(unsigned);
     p = align_up(p + w.counters_bytes);
@@ -120,6 +128,12 @@ ags_status check_config(const ags_config* c, std::string& why) {
         why = "static_scale must be finite and > 0 in STATIC mode";
         return AGS_E_ARG;
     }
+    if (c->elementwise != 0 && c->elementwise != 1) { why = "elementwise must be 0 or 1"; return AGS_E_ARG; }
+    if (c->elementwise && c->mode != AGS_MODE_AGS) {
+        why = "elementwise scales need AGS_MODE_AGS";
+        return AGS_E_ARG;
+    }
+    if (c->reserved != 0) { why = "reserved must be 0"; return AGS_E_ARG; }
     if (c->refresh_every < 0) { why = "refresh_every must be >= 0"; return AGS_E_ARG; }
     if (c->small_replica < -1 || c->small_replica >= c->K) {
         why = "small_replica must be -1 or in 0..K-1";
@@ -244,6 +258,10 @@ struct ags_handle {
     char* pinned = nullptr;
     hipStream_t last_stream = nullptr;
     bool has_stats = false;
+    // Host mirror of the device step count (only ags_step advances it and
+    // ags_set_state sets it) and the element-scale buffer in force.
+    int64_t step_host = 0;
+    int ew_cur = 0;
     std::string err;
     bool profiling = false;
     std::vector<std::array<hipEvent_t, AGS_N_KERNELS + 1>> ev_pending, ev_free;
@@ -252,7 +270,13 @@ struct ags_handle {
     Partial* partials() const { return reinterpret_cast<Partial*>(ws + wl.partials); }
     LayerDev* ldev() const { return reinterpret_cast<LayerDev*>(ws + wl.ldev); }
     float2* coef() const { return reinterpret_cast<float2*>(ws + wl.coef); }
-    float* corr() const { return reinterpret_cast<float*>(ws + wl.corr); }
+    float2* corr() const { return reinterpret_cast<float2*>(ws + wl.corr); }
+    float* ew_buf(int i) const {
+        return cfg.elementwise ? reinterpret_cast<float*>(ws + wl.ew_buf) + (size_t)i * cfg.n_flat : nullptr;
+    }
+    float* ew_partials() const {
+        return cfg.elementwise ? reinterpret_cast<float*>(ws + wl.ew_partials) : nullptr;
+    }
     unsigned* done_count() const { return reinterpret_cast<unsigned*>(ws + wl.counters); }
     int* corr_flag() const { return reinterpret_cast<int*>(done_count() + 1); }
     float* gbar() const { return materialize ? reinterpret_cast<float*>(ws + wl.gbar) : nullptr; }
@@ -333,6 +357,12 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     // AGS and SGD steps update w and m in the statistics pass with the
     // predicted coefficients; a LARS step needs its layer norms first.
     const bool fused = commit && c.mode != AGS_MODE_LARS;
+    // Element scales: the step reads the buffer in force and, when the
+    // refresh is due, writes the other one, which is in force afterwards;
+    // the old one stays intact for the correction pass.
+    const bool ew = c.elementwise != 0;
+    const bool ew_refresh = ew && commit && c.refresh_every > 0 &&
+                            (h->step_host + 1) % c.refresh_every == 0;
 
     ags::StepArgs sa{};
     sa.grads = d_grads;
@@ -371,6 +401,11 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.layer_chunk_count = reinterpret_cast<unsigned*>(h->ws + h->wl.chunk_count);
     sa.lstats = h->lstats();
     sa.gstats = h->gstats();
+    sa.ew = ew ? 1 : 0;
+    sa.ew_refresh = ew_refresh ? 1 : 0;
+    sa.gs_old = h->ew_buf(h->ew_cur);
+    sa.gs_new = ew_refresh ? h->ew_buf(1 - h->ew_cur) : nullptr;
+    sa.ew_partials = h->ew_partials();
     hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s);
     if (e != hipSuccess) return h->hip_fail(e, "step kernel launch");
     if (prof) (void)hipEventRecord(ev[1], s);
@@ -391,6 +426,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         ua.m = h->d_m;
         ua.coef = h->coef();
         ua.corr = h->corr();
+        ua.gs_old = h->ew_buf(h->ew_cur);
         ua.corr_flag = h->corr_flag();
         ua.lr = (float)h->lr;
         ua.momentum = (float)c.momentum;
@@ -402,6 +438,8 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         (void)hipEventRecord(ev[3], s);
         h->ev_pending.push_back(ev);
     }
+    if (commit) ++h->step_host;
+    if (ew_refresh) h->ew_cur ^= 1;
     h->last_stream = s;
     h->has_stats = true;
     return AGS_OK;
@@ -499,6 +537,7 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         }
         ldev[l].chunk_end = (int32_t)chunks.size();
         ldev[l].pad_ = 0;
+        ldev[l].numel = L.numel;
     }
     int64_t extent = 0;
     for (int32_t l = 0; l < cfg->n_layers; ++l)
@@ -584,6 +623,9 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
     if (e == hipSuccess) e = hipMemsetAsync(h->ws + h->wl.counters, 0, h->wl.counters_bytes, s);
     if (e == hipSuccess)
         e = hipMemsetAsync(h->ws + h->wl.chunk_count, 0, (size_t)cfg->n_layers * sizeof(unsigned), s);
+    if (e == hipSuccess && cfg->elementwise)  // element scales start at 1.0f
+        e = hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(h->ew_buf(0)), 0x3f800000,
+                              2 * (size_t)cfg->n_flat, s);
     for (const auto& u : up) {
         if (e != hipSuccess) break;
         e = hipMemcpyAsync(h->ws + u.off, u.src, u.bytes, hipMemcpyHostToDevice, s);
@@ -651,24 +693,72 @@ ags_status ags_get_state(ags_handle* h, double* gradscale_L, double* g_sq_prev, 
 
 ags_status ags_set_state(ags_handle* h, const double* gradscale_L, double g_sq_prev, int64_t step) {
     if (!h) return AGS_E_ARG;
-    if (!gradscale_L) return h->fail(AGS_E_ARG, "gradscale_L is NULL");
+    const bool ew = h->cfg.elementwise != 0;
+    if (!gradscale_L && !ew) return h->fail(AGS_E_ARG, "gradscale_L is NULL");
     if (!std::isfinite(g_sq_prev) || g_sq_prev < 0) return h->fail(AGS_E_ARG, "g_sq_prev must be finite and >= 0");
     if (step < 0) return h->fail(AGS_E_ARG, "step must be >= 0");
     const size_t L = (size_t)h->cfg.n_layers;
-    for (size_t l = 0; l < L; ++l)
-        if (!std::isfinite(gradscale_L[l]) || !(gradscale_L[l] > 0))
-            return h->fail(AGS_E_ARG, "gradscale values must be finite and > 0");
+    if (!ew)
+        for (size_t l = 0; l < L; ++l)
+            if (!std::isfinite(gradscale_L[l]) || !(gradscale_L[l] > 0))
+                return h->fail(AGS_E_ARG, "gradscale values must be finite and > 0");
     // Wait for queued steps first: the staging buffer and the state are
     // shared with them.
     hipError_t e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "waiting for the last stream");
-    std::memcpy(h->pinned, gradscale_L, L * sizeof(double));
     DevState ds{g_sq_prev, step};
-    std::memcpy(h->pinned + (h->wl.state - h->wl.gradscale), &ds, sizeof ds);
-    e = hipMemcpyAsync(h->ws + h->wl.gradscale, h->pinned, h->wl.state_bytes,
-                       hipMemcpyHostToDevice, h->last_stream);
+    const size_t soff = h->wl.state - h->wl.gradscale;
+    std::memcpy(h->pinned + soff, &ds, sizeof ds);
+    if (ew) {
+        // The layer means belong to the element scales; only the state moves.
+        e = hipMemcpyAsync(h->ws + h->wl.state, h->pinned + soff, sizeof ds,
+                           hipMemcpyHostToDevice, h->last_stream);
+    } else {
+        std::memcpy(h->pinned, gradscale_L, L * sizeof(double));
+        e = hipMemcpyAsync(h->ws + h->wl.gradscale, h->pinned, h->wl.state_bytes,
+                           hipMemcpyHostToDevice, h->last_stream);
+    }
     if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "writing state");
+    h->step_host = step;
+    return AGS_OK;
+}
+
+ags_status ags_get_elementwise_scale(ags_handle* h, float* scale, int64_t n) {
+    if (!h) return AGS_E_ARG;
+    if (!h->cfg.elementwise) return h->fail(AGS_E_STATE, "the handle has no element scales");
+    if (!scale) return h->fail(AGS_E_ARG, "scale is NULL");
+    if (n != h->cfg.n_flat) return h->fail(AGS_E_ARG, "n must equal n_flat");
+    hipError_t e = hipMemcpyAsync(scale, h->ew_buf(h->ew_cur), (size_t)n * sizeof(float),
+                                  hipMemcpyDeviceToHost, h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "reading element scales");
+    return AGS_OK;
+}
+
+ags_status ags_set_elementwise_scale(ags_handle* h, const float* scale, int64_t n) {
+    if (!h) return AGS_E_ARG;
+    if (!h->cfg.elementwise) return h->fail(AGS_E_STATE, "the handle has no element scales");
+    if (!scale) return h->fail(AGS_E_ARG, "scale is NULL");
+    if (n != h->cfg.n_flat) return h->fail(AGS_E_ARG, "n must equal n_flat");
+    for (int64_t j = 0; j < n; ++j)
+        if (!std::isfinite(scale[j]) || scale[j] < 0.0f)
+            return h->fail(AGS_E_ARG, "element scales must be finite and >= 0");
+    const size_t L = (size_t)h->cfg.n_layers;
+    std::vector<double> mean(L);
+    for (size_t l = 0; l < L; ++l) {
+        const ags_layer& ly = h->layers[l];
+        double sum = 0.0;
+        for (int64_t j = 0; j < ly.numel; ++j) sum += (double)scale[ly.offset + j];
+        mean[l] = sum / (double)ly.numel;
+    }
+    hipError_t e = hipMemcpyAsync(h->ew_buf(h->ew_cur), scale, (size_t)n * sizeof(float),
+                                  hipMemcpyHostToDevice, h->last_stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(h->ws + h->wl.gradscale, mean.data(), L * sizeof(double),
+                           hipMemcpyHostToDevice, h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "writing element scales");
     return AGS_OK;
 }
 

@@ -62,6 +62,7 @@ struct LayerDev {
     uint32_t flags;
     int32_t chunk_begin, chunk_end;  // finalize chunks of the layer
     int32_t pad_;
+    int64_t numel;
 };
 
 // A finalize block's share: tiles [tile_begin, tile_end) of one layer.
@@ -70,7 +71,7 @@ struct FinChunk {
 };
 
 struct ChunkSum {
-    double w, g, d, s;
+    double w, g, d, s, x;  // x: sum of the refreshed element scales
 };
 
 // Device-resident AGS state, updated by the last block of a committed step.
@@ -107,10 +108,10 @@ struct StepArgs {
     int refresh_every;
     float lr, momentum;      // used when the kernel updates w and m
     double delta, eps, s_max, trust_coef, weight_decay, static_scale;
-    double* gradscale;       // [n_layers]
+    double* gradscale;       // [n_layers]; with element scales, their layer means
     DevState* state;
     float2* coef;            // [n_layers] (a_l, b_l) as applied, fp32
-    float* corr;             // [n_layers] a_true - a_predicted (fp32)
+    float2* corr;            // [n_layers] correction c = x + y * scale_j (fp32)
     int* corr_flag;          // 1 when some layer needs the correction pass
     int updated;             // the step kernel applied predicted coefficients
     int xcd_map;             // step kernel: contiguous tile ranges per XCD
@@ -120,6 +121,12 @@ struct StepArgs {
     unsigned* layer_chunk_count;  // [n_layers] chunks finished (reset by the last)
     ags_layer_stats* lstats;
     ags_global_stats* gstats;
+    // Element scales (elementwise AGS; all null / 0 otherwise).
+    int ew;                  // the scale is per element
+    int ew_refresh;          // this step refreshes the element scales
+    const float* gs_old;     // [n_flat] scales in force before the step
+    float* gs_new;           // [n_flat] refreshed scales (refresh steps)
+    float* ew_partials;      // [n_tiles] per-tile sums of the refreshed scales
 };
 
 struct UpdateArgs {
@@ -133,7 +140,8 @@ struct UpdateArgs {
     float* w;
     float* m;
     const float2* coef;   // LARS update: (a_l, b_l)
-    const float* corr;    // correction pass: a_true - a_predicted
+    const float2* corr;   // correction pass: c = x + y * gs_old_j per layer
+    const float* gs_old;  // element scales in force before the step (or null)
     const int* corr_flag;
     float lr;
     float momentum;

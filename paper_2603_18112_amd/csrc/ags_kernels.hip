@@ -49,10 +49,30 @@ namespace {
 #ifndef AGS_BATCH_F32
 #define AGS_BATCH_F32 2
 #endif
+// Batches of the element-scale kernels, which hold more per-element state
+// (the fp64 replica sums, the scales): with 8 bf16 replicas per batch the
+// refresh kernel needs 319 VGPRs (one wave per SIMD), with 4 it needs 121.
+#ifndef AGS_BATCH_BF16_EW
+#define AGS_BATCH_BF16_EW 4
+#endif
+#ifndef AGS_BATCH_F32_EW
+#define AGS_BATCH_F32_EW 2
+#endif
 // From this many replicas on, w and m are loaded after the replica loop
 // rather than before it, so that they do not hold registers through it.
 #ifndef AGS_LATE_WM_K
 #define AGS_LATE_WM_K 1 << 30
+#endif
+
+// Element-scale kernels with bf16 gradients: the scale loads, the refreshed
+// scale stores and the w and m stores are non-temporal (measured on MI355X,
+// ResNet-50 layout K = 16: step kernel 262 -> 221 us); with fp32 gradients
+// ordinary accesses measured faster (ResNet-18 K = 8: 97 against 101 us).
+#ifndef AGS_EW_NT_BF16
+#define AGS_EW_NT_BF16 1
+#endif
+#ifndef AGS_EW_NT_F32
+#define AGS_EW_NT_F32 0
 #endif
 
 // bf16 gradients: a lane's two halves are adjacent (8 consecutive elements,
@@ -151,6 +171,50 @@ __device__ __forceinline__ void store_f32(float* __restrict__ p, int n0, int n1,
     }
 }
 
+// Non-temporal variants of load_f32 / store_f32 (the ragged end keeps
+// element accesses).
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+template <bool FULL, int HS>
+__device__ __forceinline__ void load_f32_nt(const float* __restrict__ p, int n0, int n1,
+                                            float (&v)[kVec]) {
+    if (FULL) {
+        const float4 a = stream_load(reinterpret_cast<const float4*>(p));
+        const float4 b = stream_load(reinterpret_cast<const float4*>(p + HS));
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    } else {
+        load_f32<false, HS>(p, n0, n1, v);
+    }
+}
+
+template <bool FULL, int HS>
+__device__ __forceinline__ void store_f32_nt(float* __restrict__ p, int n0, int n1,
+                                             const float (&v)[kVec]) {
+    if (FULL) {
+        const f32x4_t a = {v[0], v[1], v[2], v[3]};
+        const f32x4_t b = {v[4], v[5], v[6], v[7]};
+        __builtin_nontemporal_store(a, reinterpret_cast<f32x4_t*>(p));
+        __builtin_nontemporal_store(b, reinterpret_cast<f32x4_t*>(p + HS));
+    } else {
+        store_f32<false, HS>(p, n0, n1, v);
+    }
+}
+
+template <bool NT, bool FULL, int HS>
+__device__ __forceinline__ void load_f32_as(const float* __restrict__ p, int n0, int n1,
+                                            float (&v)[kVec]) {
+    if (NT) load_f32_nt<FULL, HS>(p, n0, n1, v);
+    else load_f32<FULL, HS>(p, n0, n1, v);
+}
+
+template <bool NT, bool FULL, int HS>
+__device__ __forceinline__ void store_f32_as(float* __restrict__ p, int n0, int n1,
+                                             const float (&v)[kVec]) {
+    if (NT) store_f32_nt<FULL, HS>(p, n0, n1, v);
+    else store_f32<FULL, HS>(p, n0, n1, v);
+}
+
 template <typename GT, int HS>
 __device__ __forceinline__ void load_tail(const GT* __restrict__ p, int n0, int n1,
                                           float (&v)[kVec]) {
@@ -167,6 +231,7 @@ __device__ __forceinline__ void load_tail(const GT* __restrict__ p, int n0, int 
 template <typename GT> struct RawGroup;
 template <> struct RawGroup<uint16_t> {
     static constexpr int kBatch = AGS_BATCH_BF16;
+    static constexpr int kBatchEw = AGS_BATCH_BF16_EW;
     static constexpr int HS = Map<uint16_t>::HS;
     uint2 a, b;
     __device__ __forceinline__ void load(const uint16_t* __restrict__ p) {
@@ -186,6 +251,7 @@ template <> struct RawGroup<uint16_t> {
 };
 template <> struct RawGroup<float> {
     static constexpr int kBatch = AGS_BATCH_F32;
+    static constexpr int kBatchEw = AGS_BATCH_F32_EW;
     static constexpr int HS = Map<float>::HS;
     float4 a, b;
     __device__ __forceinline__ void load(const float* __restrict__ p) {
@@ -209,12 +275,16 @@ template <> struct RawGroup<float> {
 //
 // RMODE selects the small-batch gradient: 0 = replica 0, 1 = mean over
 // replicas (no per-replica value needed), 2 = replica r (runtime).
+// EX: also return q = sum_k g_k in fp64 (exact for bf16 replicas and, in
+// practice, for fp32 ones), from which an element scale's denominator
+// gbar + eps is formed without the cancellation of the fp32 sums.
 
-template <typename GT, int KT, int RMODE, bool FULL>
+template <typename GT, int KT, int RMODE, bool FULL, bool EX = false,
+          int BATCH = RawGroup<GT>::kBatch>
 __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride, int64_t idx,
                                         int n0, int n1, int K, int r, float invK,
                                         float (&gbar)[kVec], float (&dev)[kVec],
-                                        float (&gr)[kVec]) {
+                                        float (&gr)[kVec], double (&q)[kVec]) {
     float g0[kVec], s1[kVec], s2[kVec];
     if (FULL) {
         RawGroup<GT> r0;
@@ -228,6 +298,7 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
         s1[e] = 0.0f;
         s2[e] = 0.0f;
         gr[e] = g0[e];
+        if (EX) q[e] = (double)g0[e];
     }
     auto acc = [&](int k, const float (&x)[kVec]) {
 #pragma unroll
@@ -236,13 +307,14 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
             s1[e] += d;
             s2[e] = fmaf(d, d, s2[e]);
             if (RMODE == 2) gr[e] = (k == r) ? x[e] : gr[e];
+            if (EX) q[e] += (double)x[e];
         }
     };
     if constexpr (KT > 0 && FULL) {
         // Every load of a batch is issued before any of its values is used.
         // The first batch holds replicas 1..KB-1 (replica 0 is the shift);
         // later batches run as a loop, one batch in registers at a time.
-        constexpr int KB = KT < RawGroup<GT>::kBatch ? KT : RawGroup<GT>::kBatch;
+        constexpr int KB = KT < BATCH ? KT : BATCH;
         static_assert(KT % KB == 0, "K must be a multiple of the batch");
         {
             RawGroup<GT> x[KB];
@@ -358,15 +430,17 @@ __device__ __forceinline__ T block_sum(T v, T* sh /* [kBlock / 64] */) {
 
 struct Sum4 {
     double w, g, d, s;
+    double x;  // refreshed element scales (elementwise AGS), else 0
 };
 
-// Componentwise block sum of four values with one pair of barriers.
+// Componentwise block sum with one pair of barriers.
 __device__ __forceinline__ Sum4 block_sum4(Sum4 v, Sum4* sh /* [kBlock / 64] */) {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
     v.w = wave_sum(v.w);
     v.g = wave_sum(v.g);
     v.d = wave_sum(v.d);
     v.s = wave_sum(v.s);
+    v.x = wave_sum(v.x);
     __syncthreads();
     if (lane == 0) sh[wid] = v;
     __syncthreads();
@@ -375,6 +449,7 @@ __device__ __forceinline__ Sum4 block_sum4(Sum4 v, Sum4* sh /* [kBlock / 64] */)
     r.g = (sh[0].g + sh[1].g) + (sh[2].g + sh[3].g);
     r.d = (sh[0].d + sh[1].d) + (sh[2].d + sh[3].d);
     r.s = (sh[0].s + sh[1].s) + (sh[2].s + sh[3].s);
+    r.x = (sh[0].x + sh[1].x) + (sh[2].x + sh[3].x);
     return r;
 }
 
@@ -393,20 +468,26 @@ __device__ Sum4 sum_tiles(const StepArgs& a, int tb, int te, Sum4* sh) {
     // i + 768, then the next 1024), combined in a fixed order, so that four
     // loads are in flight per thread.
     constexpr int U = 4;
+    const bool ex = a.ew_refresh != 0;
     Sum4 acc[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) acc[u] = {0.0, 0.0, 0.0, 0.0};
+    for (int u = 0; u < U; ++u) acc[u] = {0.0, 0.0, 0.0, 0.0, 0.0};
     int i = tb + (int)threadIdx.x;
     for (; i + (U - 1) * kBlock < te; i += U * kBlock) {
         Partial p[U];
+        float x[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) p[u] = a.partials[i + u * kBlock];
+        for (int u = 0; u < U; ++u) {
+            p[u] = a.partials[i + u * kBlock];
+            x[u] = ex ? a.ew_partials[i + u * kBlock] : 0.0f;
+        }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             acc[u].w += (double)p[u].w;
             acc[u].g += (double)p[u].g;
             acc[u].d += (double)p[u].d;
             acc[u].s += (double)p[u].s;
+            acc[u].x += (double)x[u];
         }
     }
 #pragma unroll
@@ -418,6 +499,7 @@ __device__ Sum4 sum_tiles(const StepArgs& a, int tb, int te, Sum4* sh) {
             acc[u].g += (double)p.g;
             acc[u].d += (double)p.d;
             acc[u].s += (double)p.s;
+            if (ex) acc[u].x += (double)a.ew_partials[j];
         }
     }
     Sum4 v;
@@ -425,6 +507,7 @@ __device__ Sum4 sum_tiles(const StepArgs& a, int tb, int te, Sum4* sh) {
     v.g = (acc[0].g + acc[1].g) + (acc[2].g + acc[3].g);
     v.d = (acc[0].d + acc[1].d) + (acc[2].d + acc[3].d);
     v.s = (acc[0].s + acc[1].s) + (acc[2].s + acc[3].s);
+    v.x = (acc[0].x + acc[1].x) + (acc[2].x + acc[3].x);
     return block_sum4(v, sh);
 }
 
@@ -434,6 +517,8 @@ __device__ __forceinline__ void write_layer(const StepArgs& a, int l, const Sum4
     o.g_sq = v.g;
     o.var = v.d / (double)a.K;
     o.gsmall_sq = v.s;
+    // Mean of the refreshed element scales, taken over by finalize_global.
+    if (a.ew_refresh) o.gradscale = v.x / (double)a.layers[l].numel;
 }
 
 // The global decision and every layer's coefficients (one block, after all
@@ -446,10 +531,14 @@ __device__ __forceinline__ void write_layer(const StepArgs& a, int l, const Sum4
 // gradscale_l = min(sqrt(S_l) / (sqrt(G_l) + eps), s_max) (1 if a norm is 0)
 // for the steps that follow.  updated: the step kernel has already applied
 // the predicted coefficients, so record their difference for the correction.
+// With element scales gradscale_l is the layer mean of the element scales
+// (so a_l above is the mean coefficient applied), the step kernel has
+// refreshed the elements, and a mispredicted scaled layer is corrected per
+// element by c_j = 1 - gradscale_j (x = 1, y = -1).
 __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* shi) {
     __shared__ int sh_sens, sh_pred;
     __shared__ long long sh_t;
-    Sum4 v = {0.0, 0.0, 0.0, 0.0};
+    Sum4 v = {0.0, 0.0, 0.0, 0.0, 0.0};
     for (int l = threadIdx.x; l < a.n_layers; l += kBlock) {
         const ags_layer_stats& o = a.lstats[l];
         v.g += o.g_sq;
@@ -515,17 +604,27 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         o.coef_b = cb;
         a.coef[l] = make_float2((float)ca, (float)cb);
         if (updated) {
-            double ap = 1.0;
-            if (scaled && !pred) {
-                if (a.mode == AGS_MODE_AGS) ap = gs_old;
-                else if (a.mode == AGS_MODE_STATIC) ap = a.static_scale;
+            float2 c = make_float2(0.0f, 0.0f);
+            if (a.ew) {
+                if (scaled && !pred && sens) c = make_float2(1.0f, -1.0f);
+            } else {
+                double ap = 1.0;
+                if (scaled && !pred) {
+                    if (a.mode == AGS_MODE_AGS) ap = gs_old;
+                    else if (a.mode == AGS_MODE_STATIC) ap = a.static_scale;
+                }
+                c.x = (float)ca - (float)ap;
             }
-            const float c = (float)ca - (float)ap;
             a.corr[l] = c;
-            need |= (c != 0.0f);
+            need |= (c.x != 0.0f || c.y != 0.0f);
         }
         double gsc = gs_old;
-        if (refresh && scaled) {
+        if (a.ew) {
+            if (a.ew_refresh) {
+                gsc = o.gradscale;
+                a.gradscale[l] = gsc;
+            }
+        } else if (refresh && scaled) {
             const double S = o.gsmall_sq, Gl = o.g_sq;
             if (S > 0.0 && Gl > 0.0) {
                 gsc = sqrt(S) / (sqrt(Gl) + a.eps);
@@ -543,24 +642,66 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
 
 // ------------------------------------------------- the fused step kernel ---
 
-template <typename GT, int KT, int RMODE, bool UPD, bool FULL>
+// Element scale of elementwise AGS (Algorithm 1 read per element):
+// |g_small / (gbar + eps)| clipped at smax, 1 for a 0/0 ratio.  q is the
+// fp64 replica sum of the element: the denominator q / K + eps is formed in
+// fp64 and rounded once, after which the quotient is well conditioned and
+// an fp32 division (two roundings in all, 1.2e-7 relative) suffices.
+#ifndef AGS_EW_F64_DIV
+#define AGS_EW_F64_DIV 0
+#endif
+__device__ __forceinline__ float element_scale(float gsmall, double q, double invK, double eps,
+                                               float smax) {
+#if AGS_EW_F64_DIV
+    double r = fabs((double)gsmall / fma(q, invK, eps));
+    if (isnan(r)) r = 1.0;
+    if (r > (double)smax) r = smax;
+    return (float)r;
+#else
+    const float den = (float)fma(q, invK, eps);
+    float r = fabsf(gsmall / den);
+    if (isnan(r)) r = 1.0f;
+    return r > smax ? smax : r;
+#endif
+}
+
+// One group of a tile.  EW: 0 per-layer coefficients; 1 element scales
+// applied (use_gs: the layer is scaled and the step is predicted not
+// sensitive); 2 applied and refreshed into a.gs_new, whose sum over the
+// group's elements goes to sx.
+template <typename GT, int KT, int RMODE, bool UPD, int EW, bool FULL>
 __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restrict__ g,
                                            int64_t idx, int n0, int n1, int K, float ca,
-                                           float cb, float& sw, float& sg, float& sd,
-                                           float& ss) {
+                                           float cb, bool use_gs, bool scaled, float smax,
+                                           float& sw, float& sg, float& sd, float& ss,
+                                           float& sx) {
     constexpr bool late_wm = KT >= AGS_LATE_WM_K;
+    constexpr int HS = Map<GT>::HS;
+    constexpr bool NT = EW > 0 && (sizeof(GT) == 2 ? AGS_EW_NT_BF16 : AGS_EW_NT_F32);
     float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
+    double q[kVec];
     if (!late_wm) {
-        load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
-        if (UPD) load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
+        load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
+        if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
     }
-    moments<GT, KT, RMODE, FULL>(g, a.stride, idx, n0, n1, K, a.small_replica, a.invK, gb, dv,
-                                 gr);
+    constexpr int kb = EW > 0 ? RawGroup<GT>::kBatchEw : RawGroup<GT>::kBatch;
+    moments<GT, KT, RMODE, FULL, EW == 2, kb>(g, a.stride, idx, n0, n1, K, a.small_replica,
+                                              a.invK, gb, dv, gr, q);
     if (late_wm) {
-        load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
-        if (UPD) load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
+        load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
+        if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
     }
-    if (!UPD && a.gbar) store_f32<FULL, Map<GT>::HS>(a.gbar + idx, n0, n1, gb);
+    float gsv[kVec];
+    if (EW > 0) {
+        // Old scales: applied on scaled layers, carried over on the others.
+        if (use_gs || (EW == 2 && !scaled)) {
+            load_f32_as<NT, FULL, HS>(a.gs_old + idx, n0, n1, gsv);
+        } else {
+#pragma unroll
+            for (int e = 0; e < kVec; ++e) gsv[e] = 1.0f;
+        }
+    }
+    if (!UPD && a.gbar) store_f32<FULL, HS>(a.gbar + idx, n0, n1, gb);
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
         sw = fmaf(wv[e], wv[e], sw);
@@ -574,12 +715,33 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
         // d = a gbar + b w ; m <- mu m + d ; w <- w - eta m
 #pragma unroll
         for (int e = 0; e < kVec; ++e) {
-            const float d = fmaf(ca, gb[e], cb * wv[e]);
+            const float ae = (EW > 0 && use_gs) ? gsv[e] : ca;
+            const float d = fmaf(ae, gb[e], cb * wv[e]);
             mv[e] = fmaf(a.momentum, mv[e], d);
             wv[e] = fmaf(-a.lr, mv[e], wv[e]);
         }
-        store_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
-        store_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
+        store_f32_as<NT, FULL, HS>(a.w + idx, n0, n1, wv);
+        store_f32_as<NT, FULL, HS>(a.m + idx, n0, n1, mv);
+    }
+    if (EW == 2) {
+        float sn[kVec];
+        if (scaled) {
+            const double invK = 1.0 / (double)K;
+#pragma unroll
+            for (int e = 0; e < kVec; ++e) {
+                const float gs = RMODE == 1 ? sqrtf(fmaf(gb[e], gb[e], dv[e] * a.invK)) : gr[e];
+                sn[e] = element_scale(gs, q[e], invK, a.eps, smax);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < kVec; ++e) sn[e] = gsv[e];
+        }
+        store_f32_as<NT, FULL, HS>(a.gs_new + idx, n0, n1, sn);
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) {
+            const bool valid = FULL || (e < kHalf ? e < n0 : e - kHalf < n1);
+            sx += valid ? sn[e] : 0.0f;
+        }
     }
 }
 
@@ -593,9 +755,9 @@ __device__ __forceinline__ int tile_of_block(int b, int n, int xcd_map) {
     return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
 }
 
-template <typename GT, int KT, int RMODE, bool UPD>
+template <typename GT, int KT, int RMODE, bool UPD, int EW>
 __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
-    __shared__ float red[4][kBlock / 64];
+    __shared__ float red[5][kBlock / 64];
     const int ti = tile_of_block(blockIdx.x, gridDim.x, a.xcd_map);
     const Tile t = a.tiles[ti];
     const int l = t.layer;
@@ -605,20 +767,24 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     // Coefficients predicted before the step: on a step whose Delta is
     // infinite by definition the unscaled ones, otherwise the scaled ones.
     float ca = 1.0f, cb = 0.0f;
+    bool use_gs = false, scaled = false;
     if (UPD) {
         const uint32_t f = a.layers[l].flags;
         const bool pred = surely_sensitive(a.state->g_prev, a.state->step);
-        if ((f & AGS_LAYER_SCALE) && !pred) {
-            if (a.mode == AGS_MODE_AGS) ca = (float)a.gradscale[l];
+        scaled = (f & AGS_LAYER_SCALE) != 0;
+        if (scaled && !pred) {
+            if (EW > 0) use_gs = true;
+            else if (a.mode == AGS_MODE_AGS) ca = (float)a.gradscale[l];
             else if (a.mode == AGS_MODE_STATIC) ca = (float)a.static_scale;
         }
         cb = (f & AGS_LAYER_DECAY) ? (float)a.weight_decay : 0.0f;
     }
+    const float smax = (float)(a.s_max > 0.0 ? a.s_max : sqrt((double)K));
 
-    float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f;
+    float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f, sx = 0.0f;
     for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
-        step_group<GT, KT, RMODE, UPD, decltype(full)::value>(a, g, idx, n0, n1, K, ca, cb, sw,
-                                                              sg, sd, ss);
+        step_group<GT, KT, RMODE, UPD, EW, decltype(full)::value>(
+            a, g, idx, n0, n1, K, ca, cb, use_gs, scaled, smax, sw, sg, sd, ss, sx);
     });
 
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -626,11 +792,13 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     sg = wave_sum(sg);
     sd = wave_sum(sd);
     ss = wave_sum(ss);
+    if (EW == 2) sx = wave_sum(sx);
     if (lane == 0) {
         red[0][wid] = sw;
         red[1][wid] = sg;
         red[2][wid] = sd;
         red[3][wid] = ss;
+        red[4][wid] = sx;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -640,6 +808,7 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
         p.d = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
         p.s = (red[3][0] + red[3][1]) + (red[3][2] + red[3][3]);
         a.partials[ti] = p;
+        if (EW == 2) a.ew_partials[ti] = (red[4][0] + red[4][1]) + (red[4][2] + red[4][3]);
     }
 }
 
@@ -661,7 +830,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
         if (threadIdx.x == 0) write_layer(a, l, v);
     } else {
         if (threadIdx.x == 0) {
-            a.chunk_sums[blockIdx.x] = ChunkSum{v.w, v.g, v.d, v.s};
+            a.chunk_sums[blockIdx.x] = ChunkSum{v.w, v.g, v.d, v.s, v.x};
             __threadfence();
             const unsigned prev = atomicAdd(&a.layer_chunk_count[l], 1u);
             sh_last = (prev + 1 == (unsigned)nch);
@@ -670,13 +839,14 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
         if (!sh_last) return;
         __threadfence();
         if (threadIdx.x == 0) {
-            Sum4 t = {0.0, 0.0, 0.0, 0.0};
+            Sum4 t = {0.0, 0.0, 0.0, 0.0, 0.0};
             for (int q = ld.chunk_begin; q < ld.chunk_end; ++q) {
                 const ChunkSum cs = a.chunk_sums[q];
                 t.w += cs.w;
                 t.g += cs.g;
                 t.d += cs.d;
                 t.s += cs.s;
+                t.x += cs.x;
             }
             write_layer(a, l, t);
             a.layer_chunk_count[l] = 0u;  // ready for the next launch
@@ -697,25 +867,35 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
 // ----------------------------------------- correction and LARS update ---
 
 // Correction of a mispredicted AGS step: m += c gbar, w -= eta c gbar with
-// c = a_true - a_predicted of the layer (0 for most layers).
-template <typename GT, int KT, bool FULL>
+// c = a_true - a_predicted of the layer (0 for most layers); with element
+// scales (PE) c_j = x + y * gs_old_j.
+template <typename GT, int KT, bool PE, bool FULL>
 __device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __restrict__ g,
-                                              int64_t idx, int n0, int n1, int K, float c) {
-    float gb[kVec], dv[kVec], gr[kVec], wv[kVec], mv[kVec];
-    load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
-    load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
-    moments<GT, KT, 0, FULL>(g, a.stride, idx, n0, n1, K, 0, a.invK, gb, dv, gr);
+                                              int64_t idx, int n0, int n1, int K, float2 c) {
+    constexpr int HS = Map<GT>::HS;
+    float gb[kVec], dv[kVec], gr[kVec], wv[kVec], mv[kVec], cv[kVec];
+    double q[kVec];
+    load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
+    load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
+    if (PE) {
+        load_f32<FULL, HS>(a.gs_old + idx, n0, n1, cv);
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) cv[e] = fmaf(c.y, cv[e], c.x);
+    } else {
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) cv[e] = c.x;
+    }
+    moments<GT, KT, 0, FULL>(g, a.stride, idx, n0, n1, K, 0, a.invK, gb, dv, gr, q);
     // One rounding each: m + c gbar and w - (eta c) gbar as fused
     // multiply-adds (the applied m already carries the rounding of the
     // predicted step; a second rounding of c gbar would double it).
-    const float lc = -a.lr * c;
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
-        mv[e] = fmaf(c, gb[e], mv[e]);
-        wv[e] = fmaf(lc, gb[e], wv[e]);
+        mv[e] = fmaf(cv[e], gb[e], mv[e]);
+        wv[e] = fmaf(-a.lr * cv[e], gb[e], wv[e]);
     }
-    store_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
-    store_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
+    store_f32<FULL, HS>(a.w + idx, n0, n1, wv);
+    store_f32<FULL, HS>(a.m + idx, n0, n1, mv);
 }
 
 template <typename GT, int KT>
@@ -726,11 +906,17 @@ __global__ __launch_bounds__(kBlock) void correct_kernel(UpdateArgs a) {
 #pragma unroll 1
     for (int ti = blockIdx.x; ti < a.n_tiles; ti += gridDim.x) {
         const Tile t = a.tiles[ti];
-        const float c = a.corr[t.layer];
-        if (c == 0.0f) continue;
-        for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
-            correct_group<GT, KT, decltype(full)::value>(a, g, idx, n0, n1, K, c);
-        });
+        const float2 c = a.corr[t.layer];
+        if (c.x == 0.0f && c.y == 0.0f) continue;
+        if (c.y == 0.0f) {
+            for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
+                correct_group<GT, KT, false, decltype(full)::value>(a, g, idx, n0, n1, K, c);
+            });
+        } else {
+            for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
+                correct_group<GT, KT, true, decltype(full)::value>(a, g, idx, n0, n1, K, c);
+            });
+        }
     }
 }
 
@@ -747,7 +933,8 @@ __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __re
     load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
     if (RECOMP) {
         float dv[kVec], gr[kVec];
-        moments<GT, KT, 0, FULL>(g, a.stride, idx, n0, n1, K, 0, a.invK, gb, dv, gr);
+        double q[kVec];
+        moments<GT, KT, 0, FULL>(g, a.stride, idx, n0, n1, K, 0, a.invK, gb, dv, gr, q);
     } else {
         load_f32<FULL, Map<GT>::HS>(a.gbar + idx, n0, n1, gb);
     }
@@ -774,19 +961,25 @@ __global__ __launch_bounds__(kBlock) void update_kernel(UpdateArgs a) {
 
 // ----------------------------------------------------------- dispatch ---
 
+template <typename GT, int KT, int RMODE>
+void step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
+    const dim3 grid(n_tiles), block(kBlock);
+    if (!update)
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, false, 0>), grid, block, 0, s, a);
+    else if (a.ew_refresh)
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 2>), grid, block, 0, s, a);
+    else if (a.ew)
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 1>), grid, block, 0, s, a);
+    else
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 0>), grid, block, 0, s, a);
+}
+
 template <typename GT, int KT>
 hipError_t step_k(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
-    const dim3 grid(n_tiles), block(kBlock);
     const int rm = a.small_replica == 0 ? 0 : (a.small_replica < 0 ? 1 : 2);
-    if (update) {
-        if (rm == 0) hipLaunchKernelGGL((step_kernel<GT, KT, 0, true>), grid, block, 0, s, a);
-        else if (rm == 1) hipLaunchKernelGGL((step_kernel<GT, KT, 1, true>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((step_kernel<GT, KT, 2, true>), grid, block, 0, s, a);
-    } else {
-        if (rm == 0) hipLaunchKernelGGL((step_kernel<GT, KT, 0, false>), grid, block, 0, s, a);
-        else if (rm == 1) hipLaunchKernelGGL((step_kernel<GT, KT, 1, false>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((step_kernel<GT, KT, 2, false>), grid, block, 0, s, a);
-    }
+    if (rm == 0) step_r<GT, KT, 0>(a, n_tiles, update, s);
+    else if (rm == 1) step_r<GT, KT, 1>(a, n_tiles, update, s);
+    else step_r<GT, KT, 2>(a, n_tiles, update, s);
     return hipGetLastError();
 }
 

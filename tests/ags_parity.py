@@ -14,7 +14,12 @@ Tolerances:
   (the spread of identical replicas, a single replica) or infinite;
 * the sensitive bit is compared exactly, and the harness asserts that the
   oracle's Delta is not within 1e-6 * delta of the threshold, where fp32
-  and fp64 sums could legitimately take different branches.
+  and fp64 sums could legitimately take different branches;
+* element scales (elementwise AGS), per element: |x - y| <= 1e-5 * |y|,
+  exact where the oracle's scale is 0.  The GPU forms each scale's
+  denominator from an fp64 replica sum and rounds it once, then divides in
+  fp32, so the scale carries about two fp32 roundings (1.2e-7 relative;
+  3e-7 with the root-mean-square numerator) however close gbar_j is to 0.
 """
 from __future__ import annotations
 
@@ -29,6 +34,7 @@ from paper_2603_18112_amd import ags, layouts, synth
 
 PARAM_RTOL = 1e-5
 STAT_RTOL = 1e-4
+SCALE_RTOL = 1e-5
 
 
 def log(*a):
@@ -66,6 +72,19 @@ def check_params(x: np.ndarray, y: np.ndarray, table, what: str, rtol: float = P
             r = float(np.max(err / np.maximum(scale, 1e-300)))
             worst = max(worst, r)
     return worst
+
+
+def check_scales(x: np.ndarray, y: np.ndarray, table, what: str, rtol: float = SCALE_RTOL):
+    """Element scales of every layer (elements outside the layers are not
+    compared: the kernels never read or write them)."""
+    for l, (o, n, _) in enumerate(table):
+        xx = x[o:o + n].astype(np.float64)
+        yy = y[o:o + n]
+        bad = ~(np.abs(xx - yy) <= rtol * np.abs(yy))
+        if np.any(bad):
+            i = int(np.argmax(bad))
+            raise AssertionError(f"{what}: layer {l} element {i}: scale {xx[i]!r}, oracle {yy[i]!r}, "
+                                 f"{int(bad.sum())} of {n} out of tolerance")
 
 
 def _close(x, y, rtol):
@@ -107,6 +126,7 @@ class Pair:
         self.hyper = dict(lr=0.1, momentum=0.9, weight_decay=5e-4, delta=0.5, eps=1e-8,
                           s_max=0.0, trust_coef=1e-3, refresh_every=1, small_replica=0)
         self.hyper.update(hyper)
+        self.ew = bool(self.hyper.get("elementwise", False))
         self.w0 = synth.init_weights(layout, seed) if w0 is None else np.asarray(w0, np.float32)
         self.w = torch.from_numpy(self.w0.copy()).cuda()
         self.m = torch.zeros_like(self.w)
@@ -138,6 +158,9 @@ class Pair:
         gs, gp, st = self.gpu.get_state()
         ogs, ogp, ost = self.ora.get_state()
         assert st == ost
+        if self.ew:
+            check_scales(self.gpu.get_elementwise_scale(), ogs, self.table, what + " scales")
+            ogs = np.array([np.mean(ogs[o:o + n]) for o, n, _ in self.table])
         for x, y in zip(gs, ogs):
             assert _close(float(x), float(y), STAT_RTOL), (x, y)
         assert _close(gp, ogp, STAT_RTOL)

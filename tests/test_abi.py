@@ -46,7 +46,7 @@ def test_struct_sizes_match_the_header():
     assert ctypes.sizeof(ags.ags_layer) == 24
     assert ctypes.sizeof(ags.ags_layer_stats) == 64
     assert ctypes.sizeof(ags.ags_global_stats) == 40
-    assert ctypes.sizeof(ags.ags_config) == 4 + 4 + 8 + 8 + 4 + 4 + 4 + 4 + 7 * 8 + 4 + 4 + 8
+    assert ctypes.sizeof(ags.ags_config) == 4 + 4 + 8 + 8 + 4 + 4 + 4 + 4 + 7 * 8 + 4 + 4 + 8 + 4 + 4
 
 
 def test_status_strings(lib):
@@ -83,6 +83,11 @@ def test_valid_config_workspace_size(lib):
     # ... unless re-reading the replicas is as cheap (K = 4 bf16: 8 bytes).
     cfg = ags.make_config(lay.table(), lay.n_flat, 4, grad_dtype="bf16", mode="lars")
     assert ags.ags_workspace_bytes(cfg) < 2_000_000
+    # Element scales: two fp32 buffers of n_flat (the scales in force and the
+    # refreshed ones) plus a per-tile sum.
+    cfg = ags.make_config(lay.table(), lay.n_flat, 16, grad_dtype="bf16", elementwise=True)
+    n = ags.ags_workspace_bytes(cfg)
+    assert 2 * lay.n_flat * 4 <= n < 2 * lay.n_flat * 4 + 2_000_000
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -111,6 +116,9 @@ def test_valid_config_workspace_size(lib):
     (dict(refresh_every=-1), ags.AGS_E_ARG),
     (dict(small_replica=4), ags.AGS_E_ARG),
     (dict(small_replica=-2), ags.AGS_E_ARG),
+    (dict(mode="sgd", elementwise=True), ags.AGS_E_ARG),     # element scales: AGS only
+    (dict(mode="lars", elementwise=True), ags.AGS_E_ARG),
+    (dict(mode="static", elementwise=True), ags.AGS_E_ARG),
 ])
 def test_config_validation(lib, kw, status):
     st, msg = _ws(**kw)
@@ -129,6 +137,15 @@ def test_bad_enum_values(lib):
     with pytest.raises(ags.AGSError) as e:
         ags.ags_workspace_bytes(cfg)
     assert e.value.status == ags.AGS_E_ARG
+
+
+def test_bad_elementwise_and_reserved_fields(lib):
+    for field, value in (("elementwise", 2), ("elementwise", -1), ("reserved", 1)):
+        cfg = ags.make_config(_table(), 136, 4)
+        setattr(cfg, field, value)
+        with pytest.raises(ags.AGSError) as e:
+            ags.ags_workspace_bytes(cfg)
+        assert e.value.status == ags.AGS_E_ARG, field
 
 
 def test_init_rejects_null_and_misaligned_pointers_before_any_device_call(lib):
@@ -163,6 +180,8 @@ def test_null_handle_calls_are_errors(lib):
     assert lib.ags_read_stats(None, None, None) == ags.AGS_E_ARG
     assert lib.ags_set_lr(None, 0.1) == ags.AGS_E_ARG
     assert lib.ags_set_profiling(None, 1) == ags.AGS_E_ARG
+    assert lib.ags_get_elementwise_scale(None, None, 0) == ags.AGS_E_ARG
+    assert lib.ags_set_elementwise_scale(None, None, 0) == ags.AGS_E_ARG
     lib.ags_destroy(None)
 
 
