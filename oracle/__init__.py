@@ -23,7 +23,8 @@ _lib = None
 
 MODES = {"sgd": 0, "ags": 1, "lars": 2, "static": 3}
 LAYER_FIELDS = ("w_sq", "g_sq", "var", "gsmall_sq", "noise_ratio", "coef_a",
-                "coef_b", "gradscale")
+                "coef_b", "gradscale", "delta", "sensitive")
+DELTA_SCOPES = {"global": 0, "layer": 1}
 GLOBAL_FIELDS = ("g_sq", "g_sq_prev", "delta", "sensitive", "nonfinite")
 
 
@@ -41,7 +42,7 @@ class _Config(ctypes.Structure):
                 ("weight_decay", ctypes.c_double), ("delta", ctypes.c_double),
                 ("eps", ctypes.c_double), ("s_max", ctypes.c_double),
                 ("trust_coef", ctypes.c_double), ("static_scale", ctypes.c_double),
-                ("elementwise", ctypes.c_int32), ("pad_", ctypes.c_int32)]
+                ("elementwise", ctypes.c_int32), ("delta_scope", ctypes.c_int32)]
 
 
 def build(force: bool = False) -> str:
@@ -64,8 +65,9 @@ def _load():
         lib.oracle_ags_step.restype = ctypes.c_int
         lib.oracle_ags_step.argtypes = [
             ctypes.POINTER(_Config), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-            ctypes.c_void_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64),
-            ctypes.c_int, ctypes.POINTER(_Layer), ctypes.c_void_p, ctypes.c_void_p]
+            ctypes.c_void_p, ctypes.POINTER(ctypes.c_double), ctypes.c_void_p,
+            ctypes.POINTER(ctypes.c_int64), ctypes.c_int, ctypes.POINTER(_Layer), ctypes.c_void_p,
+            ctypes.c_void_p]
         _lib = lib
     return _lib
 
@@ -80,7 +82,7 @@ class OracleAGS:
     def __init__(self, layers, n_flat, K, w0, m0=None, *, mode="ags",
                  grad_dtype="f32", lr=0.1, momentum=0.9, weight_decay=5e-4,
                  delta=0.5, eps=1e-8, s_max=0.0, trust_coef=1e-3, static_scale=2.0,
-                 refresh_every=1, small_replica=0, elementwise=False):
+                 refresh_every=1, small_replica=0, elementwise=False, delta_scope="global"):
         self.lib = _load()
         self.layers = [(int(o), int(n), int(f)) for o, n, f in layers]
         self.L = len(self.layers)
@@ -90,7 +92,8 @@ class OracleAGS:
         self.cfg = dict(mode=mode, lr=lr, momentum=momentum, weight_decay=weight_decay,
                         delta=delta, eps=eps, s_max=s_max, trust_coef=trust_coef,
                         static_scale=static_scale, elementwise=bool(elementwise),
-                        refresh_every=refresh_every, small_replica=small_replica)
+                        refresh_every=refresh_every, small_replica=small_replica,
+                        delta_scope=DELTA_SCOPES[delta_scope])
         self.w = np.array(w0, dtype=np.float64, copy=True).reshape(-1)
         self.m = (np.zeros(self.n_flat) if m0 is None
                   else np.array(m0, dtype=np.float64, copy=True).reshape(-1))
@@ -99,6 +102,7 @@ class OracleAGS:
         # one scale per layer, or per element of the flat buffer
         self.gradscale = np.ones(self.n_flat if elementwise else self.L)
         self.g_prev = ctypes.c_double(0.0)
+        self.g_prev_layers = np.zeros(max(self.L, 1))
         self.step_count = ctypes.c_int64(0)
         arr = (_Layer * max(self.L, 1))()
         for i, (o, n, f) in enumerate(self.layers):
@@ -116,6 +120,13 @@ class OracleAGS:
         self.gradscale[:] = np.asarray(gradscale, dtype=np.float64)
         self.g_prev.value = float(g_prev)
         self.step_count.value = int(step)
+
+    def get_layer_state(self):
+        """Per-layer ||gbar_l||^2 of the last committed step."""
+        return self.g_prev_layers[:self.L].copy()
+
+    def set_layer_state(self, g_prev_layers):
+        self.g_prev_layers[:self.L] = np.asarray(g_prev_layers, dtype=np.float64)
 
     def _run(self, grads, commit, lr=None):
         g = np.ascontiguousarray(grads)
@@ -136,18 +147,19 @@ class OracleAGS:
                       eps=float(c["eps"]), s_max=float(c["s_max"]),
                       trust_coef=float(c["trust_coef"]),
                       static_scale=float(c["static_scale"]),
-                      elementwise=int(c["elementwise"]))
+                      elementwise=int(c["elementwise"]), delta_scope=int(c["delta_scope"]))
         out_l = np.zeros((self.L, len(LAYER_FIELDS)))
         out_g = np.zeros(len(GLOBAL_FIELDS))
         rc = self.lib.oracle_ags_step(
             ctypes.byref(cfg), self.w.ctypes.data, self.m.ctypes.data, g.ctypes.data,
-            self.gradscale.ctypes.data, ctypes.byref(self.g_prev),
+            self.gradscale.ctypes.data, ctypes.byref(self.g_prev), self.g_prev_layers.ctypes.data,
             ctypes.byref(self.step_count), int(commit), self._layers_c,
             out_l.ctypes.data, out_g.ctypes.data)
         if rc != 0:
             raise RuntimeError(f"oracle_ags_step failed ({rc})")
         layer_stats = {k: out_l[:, i].copy() for i, k in enumerate(LAYER_FIELDS)}
         glob = {k: float(out_g[i]) for i, k in enumerate(GLOBAL_FIELDS)}
+        layer_stats["sensitive"] = layer_stats["sensitive"].astype(np.int64)
         glob["sensitive"] = int(glob["sensitive"])
         glob["nonfinite"] = int(glob["nonfinite"])
         return layer_stats, glob

@@ -26,6 +26,12 @@
  *                                                         Sec. III-C)
  *      On the first step (no G_prev), G_prev <= 0 or a non-finite value,
  *      Delta = +inf, i.e. the step is treated as sensitive.
+ *      Per layer, the same measure on the layer's own norm:
+ *        Delta_l = |G_l - G_l,prev| / G_l,prev   (+inf under the same rules)
+ *      It is always reported; with the per-layer scope (a variant of Eq. (5)
+ *      for the spatial side of the mapping M of Sec. III-C) layer l's
+ *      coefficient follows its own bit sensitive_l = !(Delta_l < delta)
+ *      instead of the global one.
  *   4. Per-layer coefficients of the update d = a_l * gbar + b_l * w:
  *        AGS : a_l = gradscale_l if (layer scaled and not sensitive) else 1,
  *              b_l = lambda_l                 (Algorithm 1; Eq. (8b) form
@@ -40,6 +46,8 @@
  *                                              Eq. (8a), (8b), Sec. III-C)
  *        SGD : a_l = 1, b_l = lambda_l        (vanilla large-batch baseline)
  *      lambda_l = weight_decay if the layer is decayed, else 0.
+ *      Elementwise AGS (Algorithm 1 read per element): element j of a scaled
+ *      layer takes a_j = gradscale_j on a non-sensitive step.
  *   5. Wrapped momentum SGD (Sec. IV-A, IV-B: SGD, momentum 0.9, weight decay;
  *      PyTorch semantics, no dampening, no Nesterov):
  *        m_j <- mu m_j + d_j ;  w_j <- w_j - eta m_j     (Eq. (7b))
@@ -83,13 +91,15 @@ typedef struct {
     double lr, momentum, weight_decay, delta, eps, s_max, trust_coef;
     double static_scale; /* s of the static mapping U(s) */
     int32_t elementwise; /* AGS scale per element instead of per layer */
-    int32_t pad_;
+    int32_t delta_scope; /* 0: one global Delta decides; 1: Delta_l per layer */
 } oracle_config;
 
-/* Per-layer output record: W, G, V, S, rho, a, b, gradscale (after refresh).
+/* Per-layer output record: W, G, V, S, rho, a, b, gradscale (after refresh),
+ * Delta_l and the sensitive bit that decided the layer's coefficient.
  * With elementwise scales, a is the layer mean of the coefficients applied
  * to its elements and gradscale the layer mean of its scales. */
-enum { OUT_W = 0, OUT_G, OUT_V, OUT_S, OUT_RHO, OUT_A, OUT_B, OUT_GRADSCALE, OUT_N };
+enum { OUT_W = 0, OUT_G, OUT_V, OUT_S, OUT_RHO, OUT_A, OUT_B, OUT_GRADSCALE, OUT_DELTA,
+       OUT_SENS, OUT_N };
 /* Global output record: G, G_prev (value used), Delta, sensitive, nonfinite. */
 enum { GOUT_G = 0, GOUT_GPREV, GOUT_DELTA, GOUT_SENSITIVE, GOUT_NONFINITE, GOUT_N };
 
@@ -107,17 +117,18 @@ static double grad_at(const oracle_config *c, const void *grads, int k, int64_t 
 
 /*
  * One step.  w, m: float64 state [n_flat], updated in place when commit != 0.
- * gradscale [n_layers] (or [n_flat] with elementwise scales), *g_prev, *step:
- * AGS state, updated when commit != 0.
+ * gradscale [n_layers] (or [n_flat] with elementwise scales), *g_prev,
+ * g_prev_layers [n_layers], *step: AGS state, updated when commit != 0.
  * out_layers [n_layers][OUT_N], out_global [GOUT_N].
  * Returns 0, or -1 on a bad argument, -2 when out of memory.
  */
 int oracle_ags_step(const oracle_config *c, double *w, double *m, const void *grads,
-                    double *gradscale, double *g_prev, int64_t *step, int commit,
-                    const oracle_layer *layers, double *out_layers, double *out_global)
+                    double *gradscale, double *g_prev, double *g_prev_layers, int64_t *step,
+                    int commit, const oracle_layer *layers, double *out_layers,
+                    double *out_global)
 {
-    if (!c || !w || !m || !grads || !gradscale || !g_prev || !step || !layers ||
-        !out_layers || !out_global || c->n_layers < 1 || c->K < 1)
+    if (!c || !w || !m || !grads || !gradscale || !g_prev || !g_prev_layers || !step ||
+        !layers || !out_layers || !out_global || c->n_layers < 1 || c->K < 1)
         return -1;
     const int L = c->n_layers, K = c->K;
     const int64_t t = *step + 1; /* the step being taken, 1-based */
@@ -198,6 +209,19 @@ int oracle_ags_step(const oracle_config *c, double *w, double *m, const void *gr
     if (!isfinite(G)) nonfinite = 1;
     const int sensitive = !(delta < c->delta);
 
+    /* Step 3b: per-layer variability, and the bit that decides each layer. */
+    for (int l = 0; l < L; ++l) {
+        const double Gpl = g_prev_layers[l];
+        double dl;
+        if (t == 1 || !(Gpl > 0.0) || !isfinite(Gpl) || !isfinite(G_l[l]))
+            dl = INFINITY;
+        else
+            dl = fabs((G_l[l] - Gpl) / Gpl);
+        double *out = out_layers + (size_t)l * OUT_N;
+        out[OUT_DELTA] = dl;
+        out[OUT_SENS] = c->delta_scope ? !(dl < c->delta) : sensitive;
+    }
+
     /* Step 4: coefficients. */
     for (int l = 0; l < L; ++l) {
         const int scaled = (layers[l].flags & ORACLE_SCALE) != 0;
@@ -205,10 +229,10 @@ int oracle_ags_step(const oracle_config *c, double *w, double *m, const void *gr
         double *out = out_layers + (size_t)l * OUT_N;
         double a = 1.0, b = lam;
         if (c->mode == ORACLE_AGS) {
-            a = (scaled && !sensitive) ? gradscale[l] : 1.0;
+            a = (scaled && !out[OUT_SENS]) ? gradscale[l] : 1.0;
             b = lam;
         } else if (c->mode == ORACLE_STATIC) {
-            a = (scaled && !sensitive) ? c->static_scale : 1.0;
+            a = (scaled && !out[OUT_SENS]) ? c->static_scale : 1.0;
             b = lam;
         } else if (c->mode == ORACLE_LARS) {
             if (scaled) {
@@ -232,7 +256,8 @@ int oracle_ags_step(const oracle_config *c, double *w, double *m, const void *gr
             const int64_t o = layers[l].offset, n = layers[l].numel;
             const int scaled = (layers[l].flags & ORACLE_SCALE) != 0;
             double sum = 0.0;
-            for (int64_t j = 0; j < n; ++j) sum += (scaled && !sensitive) ? gradscale[o + j] : 1.0;
+            const int sens_l = out_layers[(size_t)l * OUT_N + OUT_SENS] != 0.0;
+            for (int64_t j = 0; j < n; ++j) sum += (scaled && !sens_l) ? gradscale[o + j] : 1.0;
             out_layers[(size_t)l * OUT_N + OUT_A] = sum / (double)n;
         }
     }
@@ -243,7 +268,8 @@ int oracle_ags_step(const oracle_config *c, double *w, double *m, const void *gr
             const int64_t o = layers[l].offset, n = layers[l].numel;
             const int scaled = (layers[l].flags & ORACLE_SCALE) != 0;
             for (int64_t j = 0; j < n; ++j) {
-                const double a = ew ? ((scaled && !sensitive) ? gradscale[o + j] : 1.0) : a_l[l];
+                const int sens_l = out_layers[(size_t)l * OUT_N + OUT_SENS] != 0.0;
+                const double a = ew ? ((scaled && !sens_l) ? gradscale[o + j] : 1.0) : a_l[l];
                 const double d = a * gbar_keep[l][j] + b_l[l] * w[o + j];
                 m[o + j] = c->momentum * m[o + j] + d;
                 w[o + j] = w[o + j] - c->lr * m[o + j];
@@ -308,6 +334,7 @@ int oracle_ags_step(const oracle_config *c, double *w, double *m, const void *gr
 
     if (commit) {
         *g_prev = G;
+        for (int l = 0; l < L; ++l) g_prev_layers[l] = G_l[l];
         *step = t;
     }
 

@@ -720,3 +720,222 @@ def test_elementwise_rms_small_batch_and_zero_rules():
         assert abs(o.gradscale[0] - rms0 / (2.0 + eps)) < 1e-12
         assert abs(o.gradscale[1] - rms1 / (0.5 / 3 + eps)) < 1e-9
         assert np.all(o.gradscale[2:] == zero_scale)
+
+
+# --------------------------------------------------------------------------
+# per-layer variability: Delta_l = |G_l - G_l,prev| / G_l,prev decides layer l
+
+
+def _per_layer_setup(seed, K=3):
+    rng = np.random.default_rng(seed)
+    flags = [SD, SD, layouts.LAYER_DECAY, layouts.LAYER_SCALE]
+    lay, table = _layers([40, 24, 64, 9], flags)
+    w0 = np.zeros(lay.n_flat, np.float32)
+    base = np.zeros((K, lay.n_flat), np.float32)
+    for o, n, _ in table:
+        w0[o:o + n] = rng.standard_normal(n)
+        base[:, o:o + n] = _coarse(rng.standard_normal((K, n)))
+    return lay, table, w0, base
+
+
+def _rescale(base, table, factors):
+    g = base.copy()
+    for (o, n, _), c in zip(table, factors):
+        g[:, o:o + n] *= np.float32(c)
+    return g.astype(np.float32)
+
+
+def test_layer_delta_closed_forms_and_decisions_match_torch():
+    """Layer factors per step (relative to the base gradient):
+        step 1: 1, 1, 1, 1          Delta_l = inf for all (first step)
+        step 2: 1.125, 2, 1, 0.5    Delta_l = 0.265625, 3, 0, 0.75
+        step 3: 2.25, 2, 1, 0.5     Delta_l = 3, 0, 0, 0
+    so layer 0 is scaled on step 2 only, layer 1 on step 3 only, the decayed
+    unscaled layer never, layer 3 on step 3 only.  torch.optim.SGD fed with
+    per-layer pre-scaled gradients (scales from numpy norms) must agree."""
+    K = 3
+    lay, table, w0, base = _per_layer_setup(41, K)
+    factors = [(1, 1, 1, 1), (1.125, 2, 1, 0.5), (2.25, 2, 1, 0.5)]
+    grads = [_rescale(base, table, f) for f in factors]
+    expect_delta = [[math.inf] * 4, [0.265625, 3.0, 0.0, 0.75], [3.0, 0.0, 0.0, 0.0]]
+    expect_sens = [[1, 1, 1, 1], [0, 1, 0, 1], [1, 0, 0, 0]]
+    o = OracleAGS(table, lay.n_flat, K, w0, lr=0.05, momentum=0.9, weight_decay=5e-4,
+                  eps=0.0, refresh_every=1, small_replica=0, delta_scope="layer")
+    scale = np.ones(len(table))
+    applied = []
+    for t, g in enumerate(grads):
+        st, gl = o.step(g)
+        # (K = 3: the mean rounds, so G_l scales by c^2 up to 1e-15)
+        np.testing.assert_allclose(st["delta"], expect_delta[t], rtol=1e-13, atol=0)
+        np.testing.assert_array_equal(st["sensitive"], expect_sens[t])
+        # the global measure is still reported (the total norm's change)
+        g64 = g.astype(np.float64)
+        G = sum(float(np.sum(g64[:, o_:o_ + n].mean(axis=0) ** 2)) for o_, n, _ in table)
+        if t == 0:
+            assert math.isinf(gl["delta"])
+        else:
+            assert abs(gl["delta"] - abs(G - g_prev) / g_prev) < 1e-14
+        g_prev = G
+        a = [scale[l] if (f & layouts.LAYER_SCALE and not expect_sens[t][l]) else 1.0
+             for l, (_, _, f) in enumerate(table)]
+        np.testing.assert_allclose(st["coef_a"], a, rtol=1e-15)
+        applied.append(a)
+        gbar = g64.mean(axis=0)
+        for l, (o_, n, f) in enumerate(table):
+            if f & layouts.LAYER_SCALE:
+                scale[l] = min(np.linalg.norm(g64[0, o_:o_ + n]) / np.linalg.norm(gbar[o_:o_ + n]),
+                               math.sqrt(K))
+    w_ref, m_ref = _torch_sgd_run(w0, lay, grads, 0.05, 0.9, 5e-4, applied)
+    np.testing.assert_allclose(o.w, w_ref, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(o.m, m_ref, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("mode,kw", [("ags", {}), ("static", {"static_scale": 4.0}),
+                                     ("ags", {"elementwise": True})])
+def test_layer_delta_equals_global_under_uniform_rescaling(mode, kw):
+    # Every layer scaled by the same factor: Delta_l = Delta for all l, so
+    # both scopes take the same decisions and compute the same bits.
+    K = 3
+    lay, table, w0, base = _per_layer_setup(43, K)
+    grads = [(np.float32(c) * base).astype(np.float32) for c in (1.0, 1.125, 2.0, 2.0, 0.5)]
+    runs = []
+    for scope in ("global", "layer"):
+        o = OracleAGS(table, lay.n_flat, K, w0, mode=mode, delta_scope=scope, **kw)
+        recs = [o.step(g) for g in grads]
+        runs.append((o, recs))
+    (a, ra), (b, rb) = runs
+    np.testing.assert_array_equal(a.w, b.w)
+    np.testing.assert_array_equal(a.m, b.m)
+    for (sa, ga), (sb, gb) in zip(ra, rb):
+        for k in sa:
+            np.testing.assert_array_equal(sa[k], sb[k])
+        assert ga == gb
+        assert np.all(sb["sensitive"] == gb["sensitive"])
+
+
+def test_layer_delta_one_layer_is_the_global_measure():
+    K = 4
+    lay, table = _layers([300], [SD])
+    rng = np.random.default_rng(44)
+    w0 = rng.standard_normal(lay.n_flat).astype(np.float32)
+    o = OracleAGS(table, lay.n_flat, K, w0, delta_scope="layer")
+    for t in range(4):
+        g = rng.standard_normal((K, lay.n_flat)).astype(np.float32) * np.float32(1 + 0.3 * t)
+        st, gl = o.step(g)
+        assert st["delta"][0] == gl["delta"] and st["sensitive"][0] == gl["sensitive"]
+
+
+def test_layer_delta_zero_previous_norm_is_sensitive():
+    # Layer 1's gradient is zero on step 1: G_1,prev = 0, so Delta_1 = inf on
+    # step 2 while layer 0 (Delta_0 = 0) is scaled.
+    K = 2
+    lay, table = _layers([16, 16], [SD, SD])
+    rng = np.random.default_rng(45)
+    g1 = _coarse(rng.standard_normal((K, lay.n_flat)))
+    g0 = g1.copy()
+    g0[:, 16:32] = 0
+    o = OracleAGS(table, lay.n_flat, K, np.ones(lay.n_flat), delta_scope="layer")
+    o.step(g0)
+    st, gl = o.step(g1)
+    assert st["delta"][0] == 0.0 and math.isinf(st["delta"][1])
+    assert list(st["sensitive"]) == [0, 1]
+    assert st["coef_a"][1] == 1.0 and st["coef_a"][0] != 1.0
+
+
+def test_layer_state_checkpoint_resume_is_bitwise():
+    K = 3
+    lay, table, w0, base = _per_layer_setup(46, K)
+    rng = np.random.default_rng(47)
+    grads = [_rescale(base, table, rng.uniform(0.6, 1.4, len(table))) for _ in range(6)]
+    a = OracleAGS(table, lay.n_flat, K, w0, delta_scope="layer")
+    for g in grads:
+        a.step(g)
+    b = OracleAGS(table, lay.n_flat, K, w0, delta_scope="layer")
+    for g in grads[:3]:
+        b.step(g)
+    c = OracleAGS(table, lay.n_flat, K, b.w.astype(np.float64), m0=b.m, delta_scope="layer")
+    c.set_state(*b.get_state())
+    c.set_layer_state(b.get_layer_state())
+    for g in grads[3:]:
+        c.step(g)
+    np.testing.assert_array_equal(a.w, c.w)
+    np.testing.assert_array_equal(a.m, c.m)
+    np.testing.assert_array_equal(a.get_layer_state(), c.get_layer_state())
+
+
+def test_layer_delta_first_step_and_zero_norm_records():
+    # A first step is sensitive whatever G_prev the state holds; a layer
+    # whose norm is 0 on two steps in a row has Delta_l = +inf (not NaN).
+    K = 2
+    lay, table = _layers([16, 16], [SD, SD])
+    rng = np.random.default_rng(48)
+    g = _coarse(rng.standard_normal((K, lay.n_flat)))
+    g[:, 16:32] = 0
+    o = OracleAGS(table, lay.n_flat, K, np.ones(lay.n_flat), delta_scope="layer")
+    o.set_state(np.ones(2), 1.0, 0)
+    o.set_layer_state([1.0, 1.0])
+    st, gl = o.step(g)
+    assert np.all(np.isinf(st["delta"])) and list(st["sensitive"]) == [1, 1]
+    st, gl = o.step(g)
+    assert st["delta"][0] == 0.0 and math.isinf(st["delta"][1]) and st["delta"][1] > 0
+    assert list(st["sensitive"]) == [0, 1]
+
+
+def test_layer_delta_tie_is_sensitive():
+    # delta = 3 and a layer scaled by 2: Delta_l = 3 exactly, a tie.
+    K = 2
+    lay, table = _layers([16, 16], [SD, SD])
+    rng = np.random.default_rng(49)
+    g = _coarse(rng.standard_normal((K, lay.n_flat)))
+    o = OracleAGS(table, lay.n_flat, K, np.ones(lay.n_flat), delta=3.0, delta_scope="layer")
+    o.step(g)
+    st, _ = o.step(_rescale(g, table, [2.0, 1.0]))
+    assert list(st["delta"]) == [3.0, 0.0] and list(st["sensitive"]) == [1, 0]
+
+
+@pytest.mark.parametrize("mode", ["static", "elementwise"])
+def test_layer_delta_decides_static_and_elementwise_coefficients(mode):
+    """The schedule of the closed-form test under static U(s) and elementwise
+    AGS: layer l takes its scale iff it is scaled and not sensitive_l;
+    torch.optim.SGD fed with the pre-scaled gradients (per layer for U(s),
+    per element for elementwise scales) must agree."""
+    K, s_fixed, eps = 3, 4.0, 1e-8
+    lay, table, w0, base = _per_layer_setup(41, K)
+    factors = [(1, 1, 1, 1), (1.125, 2, 1, 0.5), (2.25, 2, 1, 0.5)]
+    grads = [_rescale(base, table, f) for f in factors]
+    expect_sens = [[1, 1, 1, 1], [0, 1, 0, 1], [1, 0, 0, 0]]
+    kw = dict(mode="static", static_scale=s_fixed) if mode == "static" else dict(elementwise=True)
+    o = OracleAGS(table, lay.n_flat, K, w0, lr=0.05, momentum=0.9, weight_decay=5e-4, eps=eps,
+                  refresh_every=1, small_replica=0, delta_scope="layer", **kw)
+    scale = np.ones(lay.n_flat)
+    applied = []
+    for t, g in enumerate(grads):
+        st, _ = o.step(g)
+        np.testing.assert_array_equal(st["sensitive"], expect_sens[t])
+        a = np.ones(lay.n_flat)
+        for l, (o_, n, f) in enumerate(table):
+            if f & layouts.LAYER_SCALE and not expect_sens[t][l]:
+                a[o_:o_ + n] = s_fixed if mode == "static" else scale[o_:o_ + n]
+            assert abs(st["coef_a"][l] - a[o_:o_ + n].mean()) < 1e-12
+        applied.append(a)
+        if mode == "elementwise":
+            g64 = g.astype(np.float64)
+            gbar = g64.mean(axis=0)
+            for o_, n, f in table:
+                if f & layouts.LAYER_SCALE:
+                    r = np.abs(g64[0, o_:o_ + n] / (gbar[o_:o_ + n] + eps))
+                    scale[o_:o_ + n] = np.minimum(r, math.sqrt(K))
+    params, groups = [], []
+    for o_, n, f in table:
+        p = torch.tensor(np.asarray(w0[o_:o_ + n], np.float64), requires_grad=True)
+        params.append(p)
+        groups.append({"params": [p], "weight_decay": 5e-4 if f & layouts.LAYER_DECAY else 0.0})
+    opt = torch.optim.SGD(groups, lr=0.05, momentum=0.9)
+    for g, a in zip(grads, applied):
+        gm = g.astype(np.float64).mean(axis=0) * a
+        for l, (o_, n, _) in enumerate(table):
+            params[l].grad = torch.tensor(gm[o_:o_ + n])
+        opt.step()
+    for l, (o_, n, _) in enumerate(table):
+        np.testing.assert_allclose(o.w[o_:o_ + n], params[l].detach().numpy(), rtol=1e-12,
+                                   atol=1e-14)
