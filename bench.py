@@ -27,6 +27,7 @@ ones, (K*2 + 24) bytes per parameter.
 
 Usage: python bench.py [--gpus 1] [--steps 200] [--warmup 20]
                        [--no-cpu-baseline] [--copy-probe] [--elementwise]
+                       [--delta-scope global|layer] [--mode ags|sgd|lars|static]
 """
 from __future__ import annotations
 
@@ -100,8 +101,9 @@ def traffic_file(workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
 
 
-def workload_key(workload: str, elementwise: bool) -> str:
-    return workload + ("_elementwise" if elementwise else "")
+def workload_key(workload: str, elementwise: bool, delta_scope: str = "global") -> str:
+    return (workload + ("_elementwise" if elementwise else "")
+            + ("_layer_delta" if delta_scope == "layer" else ""))
 
 
 def read_traffic(workload: str, kernel: str):
@@ -170,6 +172,8 @@ def main():
                     help="only run the 1 GiB device copy (counter calibration)")
     ap.add_argument("--elementwise", action="store_true",
                     help="AGS with one scale per parameter element")
+    ap.add_argument("--delta-scope", default="global", choices=["global", "layer"],
+                    help="variability measure that decides a layer: global Delta or Delta_l")
     args = ap.parse_args()
     if args.elementwise and args.mode != "ags":
         print("--elementwise needs --mode ags", file=sys.stderr)
@@ -197,7 +201,8 @@ def main():
     layout_name, K, gdt, desc = WORKLOADS[args.workload]
     E_G = 2 if gdt == "bf16" else 4
     HYPER["elementwise"] = bool(args.elementwise)
-    wkey = workload_key(args.workload, args.elementwise)
+    HYPER["delta_scope"] = args.delta_scope
+    wkey = workload_key(args.workload, args.elementwise, args.delta_scope)
     lib = ags.load_library()
     log(f"libags: {ags.library_path()}")
     lay = layouts.get_layout(layout_name)
@@ -324,7 +329,8 @@ def main():
     out = {
         "metric": ("AGS step+stats GB/s & % HBM peak (ResNet-50 layout, K=16); steps/s"
                    if wkey == WORKLOAD else
-                   f"AGS step+stats GB/s ({desc}{', elementwise scales' if args.elementwise else ''})"),
+                   f"AGS step+stats GB/s ({desc}{', elementwise scales' if args.elementwise else ''}"
+                   f"{', per-layer Delta' if args.delta_scope == 'layer' else ''})"),
         "value": round(value, 1),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -341,6 +347,7 @@ def main():
         "config": {"workload": wkey, "layout": layout_name, "tensors": lay.n_layers,
                    "params": N, "K": K, "grad_dtype": gdt, "param_dtype": "f32",
                    "mode": args.mode, "elementwise": bool(args.elementwise),
+                   "delta_scope": args.delta_scope,
                    "algorithmic_bytes_per_step": ab["whole_step"],
                    "parallelism": "single GPU (K replicas stand in for K data-parallel workers)"},
         "kernel_us": {n: round(v * 1e3, 2) for n, v in avg_ms.items()},

@@ -21,6 +21,8 @@
  *   G           = sum_l G_l
  *   Delta       = |G - G_prev| / G_prev                  gradient variability
  *   sensitive   = !(Delta < delta)                       (inf on the 1st step)
+ *   Delta_l     = |G_l - G_l,prev| / G_l,prev            per layer (reported;
+ *                 decides layer l with AGS_DELTA_LAYER)
  *   d           = a_l gbar + b_l w                       a_l, b_l per mode
  *   m <- mu m + d ;  w <- w - eta m                      momentum SGD
  *   gradscale_l <- min(sqrt(S_l) / (sqrt(G_l) + eps), s_max)   (refresh)
@@ -57,9 +59,9 @@
  *    not), so that a bad pointer is an error, not a GPU fault.
  *  - Work is enqueued on hip_stream (a hipStream_t; NULL is the default
  *    stream) and the call returns without waiting, except ags_read_stats,
- *    ags_get_state, ags_set_state, ags_get_elementwise_scale,
- *    ags_set_elementwise_scale and ags_get_kernel_times, which wait for the
- *    handle's last stream.
+ *    ags_get_state, ags_set_state, ags_get_layer_state, ags_set_layer_state,
+ *    ags_get_elementwise_scale, ags_set_elementwise_scale and
+ *    ags_get_kernel_times, which wait for the handle's last stream.
  *  - A handle is not thread-safe: one thread at a time.
  */
 #ifndef AGS_H
@@ -85,6 +87,12 @@ typedef enum {
 typedef enum { AGS_F32 = 0, AGS_BF16 = 1 } ags_dtype;
 
 typedef enum { AGS_MODE_SGD = 0, AGS_MODE_AGS = 1, AGS_MODE_LARS = 2, AGS_MODE_STATIC = 3 } ags_mode;
+
+/* Which variability measure decides a layer's coefficient in AGS and STATIC
+ * modes: the global Delta of Eq. (5) (Sec. III-B), or the same measure on
+ * the layer's own norm, Delta_l (a per-layer variant of Eq. (5); the first
+ * step, G_l,prev <= 0 and non-finite norms give +inf as for Delta). */
+typedef enum { AGS_DELTA_GLOBAL = 0, AGS_DELTA_LAYER = 1 } ags_delta_scope;
 
 #define AGS_LAYER_SCALE 1u /* the layer takes part in AGS / LARS scaling  */
 #define AGS_LAYER_DECAY 2u /* the layer receives weight decay             */
@@ -125,15 +133,20 @@ typedef struct {
                                 -1 = mean over replicas of ||g_k||^2        */
     double static_scale;     /* s of AGS_MODE_STATIC (> 0)                 */
     int32_t elementwise;     /* 1: AGS scale per element (AGS mode only)    */
-    int32_t reserved;        /* must be 0                                   */
+    int32_t delta_scope;     /* ags_delta_scope                            */
 } ags_config;
 
 /* Per-layer record of the last ags_stats / ags_step.  var is V_l (the 1/K
  * normalised spread), noise_ratio = V_l / G_l (0 if both are 0, +inf if
  * only G_l is 0), coef_a / coef_b the update coefficients used (or that
- * would be used, for ags_stats), gradscale the state after the call. */
+ * would be used, for ags_stats), gradscale the state after the call, delta
+ * the layer's Delta_l, sensitive the bit that decided the layer (the global
+ * one with AGS_DELTA_GLOBAL). */
 typedef struct {
     double w_sq, g_sq, var, gsmall_sq, noise_ratio, coef_a, coef_b, gradscale;
+    double delta;
+    int32_t sensitive;
+    int32_t reserved;
 } ags_layer_stats;
 
 /* Global record.  step: steps completed after the call; g_sq_prev: the
@@ -199,6 +212,12 @@ ags_status ags_get_state(ags_handle *h, double *gradscale_L, double *g_sq_prev,
                          int64_t *step);
 ags_status ags_set_state(ags_handle *h, const double *gradscale_L, double g_sq_prev,
                          int64_t step);
+
+/* Per-layer G_l,prev (the ||gbar_l||^2 of the last step), the state of
+ * Delta_l: host [n_layers].  Get waits for the handle's last stream; set
+ * checks every value is finite and >= 0 (AGS_E_ARG, nothing changed). */
+ags_status ags_get_layer_state(ags_handle *h, double *g_sq_prev_L);
+ags_status ags_set_layer_state(ags_handle *h, const double *g_sq_prev_L);
 
 /* Elementwise scales gradscale_j (Algorithm 1 read per element; handles
  * created with cfg.elementwise = 1, else AGS_E_STATE).  scale: host fp32

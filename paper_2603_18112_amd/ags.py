@@ -28,6 +28,8 @@ STATUS_NAMES = {0: "AGS_OK", 1: "AGS_E_ARG", 2: "AGS_E_LAYOUT", 3: "AGS_E_ALIGN"
 AGS_F32, AGS_BF16 = 0, 1
 AGS_MODE_SGD, AGS_MODE_AGS, AGS_MODE_LARS, AGS_MODE_STATIC = 0, 1, 2, 3
 AGS_LAYER_SCALE, AGS_LAYER_DECAY = 1, 2
+AGS_DELTA_GLOBAL, AGS_DELTA_LAYER = 0, 1
+DELTA_SCOPES = {"global": AGS_DELTA_GLOBAL, "layer": AGS_DELTA_LAYER}
 AGS_ALIGN_ELEMS = 8
 AGS_MAX_K = 1024
 AGS_N_KERNELS = 3
@@ -51,12 +53,13 @@ class ags_config(ctypes.Structure):
                 ("eps", ctypes.c_double), ("s_max", ctypes.c_double),
                 ("trust_coef", ctypes.c_double), ("refresh_every", ctypes.c_int32),
                 ("small_replica", ctypes.c_int32), ("static_scale", ctypes.c_double),
-                ("elementwise", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("elementwise", ctypes.c_int32), ("delta_scope", ctypes.c_int32)]
 
 
 class ags_layer_stats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_double) for n in
-                ("w_sq", "g_sq", "var", "gsmall_sq", "noise_ratio", "coef_a", "coef_b", "gradscale")]
+                ("w_sq", "g_sq", "var", "gsmall_sq", "noise_ratio", "coef_a", "coef_b", "gradscale",
+                 "delta")] + [("sensitive", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class ags_global_stats(ctypes.Structure):
@@ -65,10 +68,11 @@ class ags_global_stats(ctypes.Structure):
                 ("sensitive", ctypes.c_int32), ("nonfinite", ctypes.c_int32)]
 
 
-LAYER_STATS_FIELDS = tuple(n for n, _ in ags_layer_stats._fields_)
+LAYER_STATS_FIELDS = tuple(n for n, _ in ags_layer_stats._fields_ if n != "reserved")
 #: every function the header declares
 EXPORTS = ("ags_workspace_bytes", "ags_init", "ags_stats", "ags_step", "ags_read_stats",
-           "ags_set_lr", "ags_get_state", "ags_set_state", "ags_get_elementwise_scale",
+           "ags_set_lr", "ags_get_state", "ags_set_state", "ags_get_layer_state",
+           "ags_set_layer_state", "ags_get_elementwise_scale",
            "ags_set_elementwise_scale", "ags_set_profiling",
            "ags_get_kernel_times", "ags_status_string", "ags_last_error", "ags_destroy")
 
@@ -113,6 +117,8 @@ def load_library(path: str | None = None):
         "ags_set_lr": (c_int, [h, c_dbl]),
         "ags_get_state": (c_int, [h, vp, P(c_dbl), P(c_i64)]),
         "ags_set_state": (c_int, [h, vp, c_dbl, c_i64]),
+        "ags_get_layer_state": (c_int, [h, vp]),
+        "ags_set_layer_state": (c_int, [h, vp]),
         "ags_get_elementwise_scale": (c_int, [h, vp, c_i64]),
         "ags_set_elementwise_scale": (c_int, [h, vp, c_i64]),
         "ags_set_profiling": (c_int, [h, c_int]),
@@ -141,7 +147,8 @@ def _check(status: int, handle=None):
 
 def make_config(layers, n_flat, K, *, grad_dtype="f32", mode="ags", lr=0.1, momentum=0.9,
                 weight_decay=5e-4, delta=0.5, eps=1e-8, s_max=0.0, trust_coef=1e-3,
-                refresh_every=1, small_replica=0, static_scale=2.0, elementwise=False):
+                refresh_every=1, small_replica=0, static_scale=2.0, elementwise=False,
+                delta_scope="global"):
     """An ags_config (plus the layer array it points to, kept alive on it)."""
     arr = (ags_layer * max(len(layers), 1))()
     for i, (o, n, f) in enumerate(layers):
@@ -152,7 +159,7 @@ def make_config(layers, n_flat, K, *, grad_dtype="f32", mode="ags", lr=0.1, mome
                      delta=float(delta), eps=float(eps), s_max=float(s_max),
                      trust_coef=float(trust_coef), refresh_every=int(refresh_every),
                      small_replica=int(small_replica), static_scale=float(static_scale),
-                     elementwise=int(bool(elementwise)), reserved=0)
+                     elementwise=int(bool(elementwise)), delta_scope=DELTA_SCOPES[delta_scope])
     cfg._layers_keepalive = arr
     return cfg
 
@@ -215,6 +222,17 @@ def ags_set_state(handle, gradscale, g_sq_prev: float, step: int):
         gs = np.ascontiguousarray(gradscale, dtype=np.float64)
         ptr = gs.ctypes.data
     _check(load_library().ags_set_state(handle, ptr, float(g_sq_prev), int(step)), handle)
+
+
+def ags_get_layer_state(handle, n_layers: int):
+    out = np.zeros(max(int(n_layers), 1))
+    _check(load_library().ags_get_layer_state(handle, out.ctypes.data), handle)
+    return out[:int(n_layers)].copy()
+
+
+def ags_set_layer_state(handle, g_sq_prev):
+    a = np.ascontiguousarray(g_sq_prev, dtype=np.float64).reshape(-1)
+    _check(load_library().ags_set_layer_state(handle, a.ctypes.data), handle)
 
 
 def ags_get_elementwise_scale(handle, n: int):
@@ -312,6 +330,15 @@ class AGS:
 
     def set_state(self, gradscale, g_sq_prev, step):
         ags_set_state(self.handle, gradscale, g_sq_prev, step)
+
+    def get_layer_state(self):
+        return ags_get_layer_state(self.handle, self.n_layers)
+
+    def set_layer_state(self, g_sq_prev):
+        g = np.asarray(g_sq_prev, dtype=np.float64).reshape(-1)
+        if g.size != self.n_layers:
+            raise ValueError(f"expected {self.n_layers} values, got {g.size}")
+        ags_set_layer_state(self.handle, g)
 
     def get_elementwise_scale(self):
         return ags_get_elementwise_scale(self.handle, self.w.numel())

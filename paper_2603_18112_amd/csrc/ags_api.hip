@@ -33,6 +33,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct WsLayout {
     size_t gbar = 0, tiles = 0, partials = 0, ldev = 0, coef = 0, corr = 0, counters = 0;
     size_t ew_buf = 0, ew_partials = 0;  // element scales: two [n_flat] fp32 buffers
+    size_t g_prev_l = 0;                  // [L] fp64 per-layer G_prev
     size_t chunks = 0, chunk_sums = 0, chunk_count = 0;
     size_t counters_bytes = 0;  // finished-layer counter, correction flag
     size_t lstats = 0, gstats = 0, gradscale = 0, state = 0, end = 0;
@@ -81,6 +82,8 @@ WsLayout ws_layout(const ags_config& c, int64_t n_tiles, int64_t n_chunks) {
     w.counters = p;
     w.counters_bytes = 2 * sizeof(unsigned);
     p = align_up(p + w.counters_bytes);
+    w.g_prev_l = p;
+    p = align_up(p + L * sizeof(double));
     w.lstats = p;
     p += L * sizeof(ags_layer_stats);
     w.gstats = p;
@@ -133,7 +136,10 @@ ags_status check_config(const ags_config* c, std::string& why) {
         why = "elementwise scales need AGS_MODE_AGS";
         return AGS_E_ARG;
     }
-    if (c->reserved != 0) { why = "reserved must be 0"; return AGS_E_ARG; }
+    if (c->delta_scope != AGS_DELTA_GLOBAL && c->delta_scope != AGS_DELTA_LAYER) {
+        why = "bad delta_scope";
+        return AGS_E_ARG;
+    }
     if (c->refresh_every < 0) { why = "refresh_every must be >= 0"; return AGS_E_ARG; }
     if (c->small_replica < -1 || c->small_replica >= c->K) {
         why = "small_replica must be -1 or in 0..K-1";
@@ -283,6 +289,7 @@ struct ags_handle {
     ags_layer_stats* lstats() const { return reinterpret_cast<ags_layer_stats*>(ws + wl.lstats); }
     ags_global_stats* gstats() const { return reinterpret_cast<ags_global_stats*>(ws + wl.gstats); }
     double* gradscale() const { return reinterpret_cast<double*>(ws + wl.gradscale); }
+    double* g_prev_l() const { return reinterpret_cast<double*>(ws + wl.g_prev_l); }
     DevState* state() const { return reinterpret_cast<DevState*>(ws + wl.state); }
 
     ags_status fail(ags_status s, const std::string& why) {
@@ -390,6 +397,8 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.weight_decay = c.weight_decay;
     sa.gradscale = h->gradscale();
     sa.state = h->state();
+    sa.g_prev_l = h->g_prev_l();
+    sa.delta_scope = c.delta_scope;
     sa.coef = h->coef();
     sa.corr = h->corr();
     sa.corr_flag = h->corr_flag();
@@ -623,6 +632,8 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
     if (e == hipSuccess) e = hipMemsetAsync(h->ws + h->wl.counters, 0, h->wl.counters_bytes, s);
     if (e == hipSuccess)
         e = hipMemsetAsync(h->ws + h->wl.chunk_count, 0, (size_t)cfg->n_layers * sizeof(unsigned), s);
+    if (e == hipSuccess)
+        e = hipMemsetAsync(h->ws + h->wl.g_prev_l, 0, (size_t)cfg->n_layers * sizeof(double), s);
     if (e == hipSuccess && cfg->elementwise)  // element scales start at 1.0f
         e = hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(h->ew_buf(0)), 0x3f800000,
                               2 * (size_t)cfg->n_flat, s);
@@ -721,6 +732,32 @@ ags_status ags_set_state(ags_handle* h, const double* gradscale_L, double g_sq_p
     if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "writing state");
     h->step_host = step;
+    return AGS_OK;
+}
+
+ags_status ags_get_layer_state(ags_handle* h, double* g_sq_prev_L) {
+    if (!h) return AGS_E_ARG;
+    if (!g_sq_prev_L) return h->fail(AGS_E_ARG, "g_sq_prev_L is NULL");
+    const size_t bytes = (size_t)h->cfg.n_layers * sizeof(double);
+    hipError_t e = hipMemcpyAsync(g_sq_prev_L, h->g_prev_l(), bytes, hipMemcpyDeviceToHost,
+                                  h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "reading the layer state");
+    return AGS_OK;
+}
+
+ags_status ags_set_layer_state(ags_handle* h, const double* g_sq_prev_L) {
+    if (!h) return AGS_E_ARG;
+    if (!g_sq_prev_L) return h->fail(AGS_E_ARG, "g_sq_prev_L is NULL");
+    for (int32_t l = 0; l < h->cfg.n_layers; ++l)
+        if (!std::isfinite(g_sq_prev_L[l]) || g_sq_prev_L[l] < 0)
+            return h->fail(AGS_E_ARG, "g_sq_prev_L values must be finite and >= 0");
+    const size_t bytes = (size_t)h->cfg.n_layers * sizeof(double);
+    hipError_t e = hipStreamSynchronize(h->last_stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(h->g_prev_l(), g_sq_prev_L, bytes, hipMemcpyHostToDevice, h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "writing the layer state");
     return AGS_OK;
 }
 

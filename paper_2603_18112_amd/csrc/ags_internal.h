@@ -110,6 +110,8 @@ struct StepArgs {
     double delta, eps, s_max, trust_coef, weight_decay, static_scale;
     double* gradscale;       // [n_layers]; with element scales, their layer means
     DevState* state;
+    double* g_prev_l;        // [n_layers] G_l of the last committed step
+    int delta_scope;         // ags_delta_scope
     float2* coef;            // [n_layers] (a_l, b_l) as applied, fp32
     float2* corr;            // [n_layers] correction c = x + y * scale_j (fp32)
     int* corr_flag;          // 1 when some layer needs the correction pass

@@ -524,7 +524,9 @@ __device__ __forceinline__ void write_layer(const StepArgs& a, int l, const Sum4
 // The global decision and every layer's coefficients (one block, after all
 // layers are final).  Delta = |G - G_prev| / G_prev, infinite on a first
 // step, when G_prev <= 0 or when a value is not finite; sensitive =
-// !(Delta < delta).  AGS: a_l = gradscale_l on scaled layers of a
+// !(Delta < delta); Delta_l likewise from each layer's G_l, and with the
+// per-layer scope sensitive_l = !(Delta_l < delta) replaces the global bit
+// for that layer.  AGS: a_l = gradscale_l on scaled layers of a
 // non-sensitive step, else 1; STATIC: a_l = s likewise (U(s), Eq. (8));
 // LARS: a_l = tau ||w|| / (||g|| + lambda ||w||);
 // b_l = lambda_l (AGS, SGD) or a_l lambda_l (LARS).  When the refresh is due,
@@ -575,7 +577,7 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         sh_t = t;
     }
     __syncthreads();
-    const int sens = sh_sens, pred = sh_pred;
+    const int sens_g = sh_sens, pred_g = sh_pred;
     const long long t = sh_t;
     const bool refresh = a.commit && a.mode == AGS_MODE_AGS && a.refresh_every > 0 &&
                          (t % a.refresh_every) == 0;
@@ -587,6 +589,18 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         const bool scaled = (f & AGS_LAYER_SCALE) != 0;
         const double lam = (f & AGS_LAYER_DECAY) ? a.weight_decay : 0.0;
         const double gs_old = a.gradscale[l];
+        // The layer's own variability Delta_l (always reported); with the
+        // per-layer scope it decides the layer, and the step kernel's
+        // prediction was made from the layer's own G_l,prev.
+        const double Gpl = a.g_prev_l[l];
+        const bool pred_l = surely_sensitive(Gpl, t - 1);
+        const double dl = (pred_l || !isfinite(o.g_sq)) ? INFINITY : fabs((o.g_sq - Gpl) / Gpl);
+        const int sens = a.delta_scope ? !(dl < a.delta) : sens_g;
+        const int pred = a.delta_scope ? pred_l : pred_g;
+        o.delta = dl;
+        o.sensitive = sens;
+        o.reserved = 0;
+        if (a.commit) a.g_prev_l[l] = o.g_sq;
         double ca = 1.0, cb = lam;
         if (a.mode == AGS_MODE_AGS) {
             ca = (scaled && !sens) ? gs_old : 1.0;
@@ -770,7 +784,8 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     bool use_gs = false, scaled = false;
     if (UPD) {
         const uint32_t f = a.layers[l].flags;
-        const bool pred = surely_sensitive(a.state->g_prev, a.state->step);
+        const bool pred = a.delta_scope ? surely_sensitive(a.g_prev_l[l], a.state->step)
+                                        : surely_sensitive(a.state->g_prev, a.state->step);
         scaled = (f & AGS_LAYER_SCALE) != 0;
         if (scaled && !pred) {
             if (EW > 0) use_gs = true;

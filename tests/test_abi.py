@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol(lib):
 def test_struct_sizes_match_the_header():
     # Sizes follow from the field lists in include/ags.h on x86-64.
     assert ctypes.sizeof(ags.ags_layer) == 24
-    assert ctypes.sizeof(ags.ags_layer_stats) == 64
+    assert ctypes.sizeof(ags.ags_layer_stats) == 9 * 8 + 4 + 4
     assert ctypes.sizeof(ags.ags_global_stats) == 40
     assert ctypes.sizeof(ags.ags_config) == 4 + 4 + 8 + 8 + 4 + 4 + 4 + 4 + 7 * 8 + 4 + 4 + 8 + 4 + 4
 
@@ -139,8 +139,9 @@ def test_bad_enum_values(lib):
     assert e.value.status == ags.AGS_E_ARG
 
 
-def test_bad_elementwise_and_reserved_fields(lib):
-    for field, value in (("elementwise", 2), ("elementwise", -1), ("reserved", 1)):
+def test_bad_elementwise_and_delta_scope_fields(lib):
+    for field, value in (("elementwise", 2), ("elementwise", -1), ("delta_scope", 2),
+                         ("delta_scope", -1)):
         cfg = ags.make_config(_table(), 136, 4)
         setattr(cfg, field, value)
         with pytest.raises(ags.AGSError) as e:
@@ -181,6 +182,8 @@ def test_null_handle_calls_are_errors(lib):
     assert lib.ags_set_lr(None, 0.1) == ags.AGS_E_ARG
     assert lib.ags_set_profiling(None, 1) == ags.AGS_E_ARG
     assert lib.ags_get_elementwise_scale(None, None, 0) == ags.AGS_E_ARG
+    assert lib.ags_get_layer_state(None, None) == ags.AGS_E_ARG
+    assert lib.ags_set_layer_state(None, None) == ags.AGS_E_ARG
     assert lib.ags_set_elementwise_scale(None, None, 0) == ags.AGS_E_ARG
     lib.ags_destroy(None)
 
