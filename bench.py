@@ -158,6 +158,92 @@ def cpu_baseline(layout, w0, grads_np, budget_s=12.0, max_steps=8):
     return sec, len(times)
 
 
+PLAN_KS = (1, 2, 4, 8, 16, 32, 64)
+
+
+def run_plan(args, torch, np):
+    """The planner on this library's own step times: ResNet-50 layout, bf16
+    replicas, AGS, K = 1..64.  On one GPU the K replicas stand in for K
+    workers and the device reads every worker's gradient, the centralized
+    form of Eq. (2c): t(K) = c0 + c_sync K.  Full search fits every K,
+    partial search the extremes (K = 1 and 64) only; both predict every K.
+    The knee of the time per replica gradient, t(K) / K, over K is where
+    more replicas per step stop amortising the step's fixed costs."""
+    from paper_2603_18112_amd import ags, layouts, plan, synth
+    lay = layouts.get_layout("resnet50")
+    N = lay.n_params
+    stride = layouts.replica_stride(lay)
+    kmax = max(PLAN_KS)
+    t0 = time.time()
+    g_np = synth.replica_grads(lay, kmax, 0, 0, dtype="bf16", stride=stride)
+    g_all = torch.from_numpy(g_np.view(np.int16)).cuda()
+    del g_np
+    log(f"plan: {kmax} bf16 replicas generated in {time.time() - t0:.1f}s")
+    w0 = synth.init_weights(lay, 0)
+    steps = max(20, min(args.steps, 200))
+    hyper = dict(HYPER)
+    measured = {}
+    for k in PLAN_KS:
+        w = torch.from_numpy(w0.copy()).cuda()
+        m = torch.zeros_like(w)
+        g = g_all[:k]
+        h = ags.AGS(lay.table(), w, m, k, grad_dtype="bf16", mode="ags", **hyper)
+        stream = torch.cuda.current_stream()
+        for _ in range(args.warmup):
+            h.step(g, stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            h.step(g, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        measured[k] = e0.elapsed_time(e1) / steps * 1e-3
+        h.close()
+        del w, m
+        log(f"plan: K={k}: {measured[k] * 1e6:.1f} us/step")
+    samples = [(k, 0.0, measured[k]) for k in PLAN_KS]
+    terms = plan.AGS_PLAN_INTERCEPT | plan.AGS_PLAN_SYNC
+    tf = time.perf_counter()
+    full = plan.ags_plan_fit(samples, "ps", terms)
+    fit_us = (time.perf_counter() - tf) * 1e6
+    part = plan.ags_plan_fit([s for s in samples if s[0] in (PLAN_KS[0], PLAN_KS[-1])], "ps", terms)
+
+    def report(model):
+        rows, worst = [], 0.0
+        for k in PLAN_KS:
+            pred = plan.ags_plan_step_time(model, k, 0.0)
+            err = pred / measured[k] - 1.0
+            worst = max(worst, abs(err))
+            rows.append({"K": k, "measured_us": round(measured[k] * 1e6, 2),
+                         "predicted_us": round(pred * 1e6, 2), "rel_err": round(err, 4)})
+        return {"c0_us": round(model.c0 * 1e6, 3), "c_sync_us_per_replica": round(model.c_sync * 1e6, 3),
+                "rms_residual_us": round(model.rms_residual * 1e6, 3),
+                "max_abs_rel_err": round(worst, 4), "per_K": rows}
+
+    ks = np.array(PLAN_KS, dtype=np.float64)
+    per_rep = np.array([measured[k] / k for k in PLAN_KS])
+    knee = plan.ags_plan_knee(ks, per_rep, "convex_dec", 1.0)
+    bytes_per_step = {k: N * (k * 2 + 16) for k in PLAN_KS}
+    out = {
+        "metric": "planner step-time model on measured AGS steps (ResNet-50 layout, bf16, K sweep)",
+        "unit": "relative error",
+        "value": round(report(part)["max_abs_rel_err"], 4),
+        "higher_is_better": False,
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup, "data": "synthetic",
+        "config": {"workload": "resnet50_bf16_ksweep", "K": list(PLAN_KS), "mode": "ags",
+                   "model": "t(K) = c0 + c_sync * K (Eq. (2), centralized sync term)"},
+        "full_search": report(full),
+        "partial_search": report(part),
+        "knee": {"K": None if knee is None else PLAN_KS[knee],
+                 "curve": "seconds per replica gradient t(K)/K over K (Kneedle, convex decreasing)",
+                 "per_replica_us": [round(x * 1e6, 2) for x in per_rep]},
+        "algorithmic_GBps": {str(k): round(bytes_per_step[k] / measured[k] / 1e9, 1) for k in PLAN_KS},
+        "fit_call_us": round(fit_us, 2),
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -174,6 +260,9 @@ def main():
                     help="AGS with one scale per parameter element")
     ap.add_argument("--delta-scope", default="global", choices=["global", "layer"],
                     help="variability measure that decides a layer: global Delta or Delta_l")
+    ap.add_argument("--plan", action="store_true",
+                    help="time the ResNet-50 bf16 step for K = 1..64 and fit the planner's "
+                         "step-time model to it (full and partial search), then its knee")
     args = ap.parse_args()
     if args.elementwise and args.mode != "ags":
         print("--elementwise needs --mode ags", file=sys.stderr)
@@ -195,6 +284,10 @@ def main():
         bw = copy_probe(torch)
         log(f"copy probe: {bw:.1f} GB/s")
         print(json.dumps({"copy_probe_GBps": round(bw, 1), "bytes_per_copy": 2 * (1 << 30)}))
+        return
+
+    if args.plan:
+        run_plan(args, torch, np)
         return
 
     global K, E_G

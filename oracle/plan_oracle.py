@@ -81,8 +81,9 @@ def time_cost(model, nodes, global_batch, epochs, dataset_size, price_per_node_h
 
 
 def max_local_batch(capacity, m_static, m_per_sample):
-    """Largest b with M_static + m_per_sample * b <= capacity (Eq. (3))."""
-    return math.floor((capacity - m_static) / m_per_sample)
+    """Largest b with M_static + m_per_sample * b <= capacity (Eq. (3)); 0
+    when not even the static memory fits."""
+    return max(0, math.floor((capacity - m_static) / m_per_sample))
 
 
 def knee(x, y, shape="convex_dec", sensitivity=1.0):

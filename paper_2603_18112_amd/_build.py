@@ -11,8 +11,10 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libags.so")
-SOURCES = [os.path.join(CSRC, "ags_api.hip"), os.path.join(CSRC, "ags_kernels.hip")]
-HEADERS = [os.path.join(CSRC, "ags_internal.h"), os.path.join(INCLUDE, "ags.h")]
+SOURCES = [os.path.join(CSRC, "ags_api.hip"), os.path.join(CSRC, "ags_kernels.hip"),
+           os.path.join(CSRC, "ags_plan.cpp")]
+HEADERS = [os.path.join(CSRC, "ags_internal.h"), os.path.join(INCLUDE, "ags.h"),
+           os.path.join(INCLUDE, "ags_plan.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -248,6 +248,10 @@ size_t workspace_cap() {
 
 }  // namespace
 
+namespace ags {
+void set_thread_error(const char* why) { g_thread_error = why ? why : ""; }
+}  // namespace ags
+
 struct ags_handle {
     ags_config cfg{};
     std::vector<ags_layer> layers;

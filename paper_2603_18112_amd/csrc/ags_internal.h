@@ -149,6 +149,9 @@ struct UpdateArgs {
     float momentum;
 };
 
+// Text for ags_last_error(NULL) on this thread (ags_api.hip).
+void set_thread_error(const char* why);
+
 // Launchers (ags_kernels.hip).  They only enqueue; the return value is the
 // launch status.  update != 0 makes the step kernel apply the update.
 hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s);

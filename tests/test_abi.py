@@ -10,7 +10,7 @@ import subprocess
 
 import pytest
 
-from paper_2603_18112_amd import _build, ags, layouts
+from paper_2603_18112_amd import _build, ags, layouts, plan
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -22,14 +22,19 @@ def lib():
     return ags.load_library()
 
 
-def header_functions():
-    text = open(os.path.join(ROOT, "include", "ags.h")).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(ags_[a-z_]+)\s*\(", text)))
+def header_functions(name=None):
+    names = [name] if name else sorted(os.listdir(os.path.join(ROOT, "include")))
+    out = set()
+    for h in names:
+        text = open(os.path.join(ROOT, "include", h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        out |= set(re.findall(r"\b(ags_[a-z_]+)\s*\(", text))
+    return sorted(out)
 
 
 def test_header_declares_the_binding_names():
-    assert header_functions() == sorted(ags.EXPORTS)
+    assert header_functions("ags.h") == sorted(ags.EXPORTS)
+    assert header_functions("ags_plan.h") == sorted(plan.EXPORTS)
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -45,6 +50,9 @@ def test_struct_sizes_match_the_header():
     # Sizes follow from the field lists in include/ags.h on x86-64.
     assert ctypes.sizeof(ags.ags_layer) == 24
     assert ctypes.sizeof(ags.ags_layer_stats) == 9 * 8 + 4 + 4
+    assert ctypes.sizeof(plan.ags_plan_sample) == 24
+    assert ctypes.sizeof(plan.ags_plan_model) == 4 + 4 + 4 * 8 + 4 + 4
+    assert ctypes.sizeof(plan.ags_plan_candidate) == 16
     assert ctypes.sizeof(ags.ags_global_stats) == 40
     assert ctypes.sizeof(ags.ags_config) == 4 + 4 + 8 + 8 + 4 + 4 + 4 + 4 + 7 * 8 + 4 + 4 + 8 + 4 + 4
 
