@@ -537,7 +537,33 @@ __device__ __forceinline__ void write_layer(const StepArgs& a, int l, const Sum4
 // (so a_l above is the mean coefficient applied), the step kernel has
 // refreshed the elements, and a mispredicted scaled layer is corrected per
 // element by c_j = 1 - gradscale_j (x = 1, y = -1).
-__device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* shi) {
+// Inputs of the global part that no block of this launch writes before the
+// last block reads them, loaded by every block at its start so that the
+// last one has them at hand: the state (thread 0) and, for layer
+// threadIdx.x, its flags, gradscale and G_l,prev.
+struct Prefetch {
+    double g_prev, gs, gpl;
+    long long step;
+    uint32_t flags;
+};
+
+__device__ __forceinline__ Prefetch prefetch_global(const StepArgs& a) {
+    Prefetch p{0.0, 0.0, 0.0, 0, 0u};
+    if (threadIdx.x == 0) {
+        p.g_prev = a.state->g_prev;
+        p.step = a.state->step;
+    }
+    const int l = threadIdx.x;
+    if (l < a.n_layers) {
+        p.flags = a.layers[l].flags;
+        p.gs = a.gradscale[l];
+        p.gpl = a.g_prev_l[l];
+    }
+    return p;
+}
+
+__device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* shi,
+                                const Prefetch& pf) {
     __shared__ int sh_sens, sh_pred;
     __shared__ long long sh_t;
     Sum4 v = {0.0, 0.0, 0.0, 0.0, 0.0};
@@ -550,8 +576,8 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
     const double G = v.g;
     int nf = v.w != 0.0;
     if (threadIdx.x == 0) {
-        const double Gp = __hip_atomic_load(&a.state->g_prev, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const long long step = __hip_atomic_load(&a.state->step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const double Gp = pf.g_prev;
+        const long long step = pf.step;
         const long long t = step + 1;
         double delta;
         if (surely_sensitive(Gp, step) || !isfinite(G))
@@ -585,14 +611,15 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
     int need = 0;
     for (int l = threadIdx.x; l < a.n_layers; l += kBlock) {
         ags_layer_stats& o = a.lstats[l];
-        const uint32_t f = a.layers[l].flags;
+        const bool first = l == (int)threadIdx.x;
+        const uint32_t f = first ? pf.flags : a.layers[l].flags;
         const bool scaled = (f & AGS_LAYER_SCALE) != 0;
         const double lam = (f & AGS_LAYER_DECAY) ? a.weight_decay : 0.0;
-        const double gs_old = a.gradscale[l];
+        const double gs_old = first ? pf.gs : a.gradscale[l];
         // The layer's own variability Delta_l (always reported); with the
         // per-layer scope it decides the layer, and the step kernel's
         // prediction was made from the layer's own G_l,prev.
-        const double Gpl = a.g_prev_l[l];
+        const double Gpl = first ? pf.gpl : a.g_prev_l[l];
         const bool pred_l = surely_sensitive(Gpl, t - 1);
         const double dl = (pred_l || !isfinite(o.g_sq)) ? INFINITY : fabs((o.g_sq - Gpl) / Gpl);
         const int sens = a.delta_scope ? !(dl < a.delta) : sens_g;
@@ -836,6 +863,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
     __shared__ Sum4 sh4[kBlock / 64];
     __shared__ int shi[kBlock / 64];
     __shared__ int sh_last;
+    const Prefetch pf = prefetch_global(a);
     const FinChunk c = a.chunks[blockIdx.x];
     const int l = c.layer;
     const Sum4 v = sum_tiles(a, c.tile_begin, c.tile_end, sh4);
@@ -875,7 +903,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
     __syncthreads();
     if (!sh_last) return;
     __threadfence();
-    finalize_global(a, a.updated != 0, sh4, shi);
+    finalize_global(a, a.updated != 0, sh4, shi, pf);
     if (threadIdx.x == 0) *a.done_count = 0u;  // ready for the next launch
 }
 
