@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <array>
 #include <cmath>
+#include <cstddef>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -268,10 +269,6 @@ struct ags_handle {
     char* pinned = nullptr;
     hipStream_t last_stream = nullptr;
     bool has_stats = false;
-    // Host mirror of the device step count (only ags_step advances it and
-    // ags_set_state sets it) and the element-scale buffer in force.
-    int64_t step_host = 0;
-    int ew_cur = 0;
     std::string err;
     bool profiling = false;
     std::vector<std::array<hipEvent_t, AGS_N_KERNELS + 1>> ev_pending, ev_free;
@@ -370,10 +367,9 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     const bool fused = commit && c.mode != AGS_MODE_LARS;
     // Element scales: the step reads the buffer in force and, when the
     // refresh is due, writes the other one, which is in force afterwards;
-    // the old one stays intact for the correction pass.
+    // the old one stays intact for the correction pass.  The kernels take
+    // both from the device state.
     const bool ew = c.elementwise != 0;
-    const bool ew_refresh = ew && commit && c.refresh_every > 0 &&
-                            (h->step_host + 1) % c.refresh_every == 0;
 
     ags::StepArgs sa{};
     sa.grads = d_grads;
@@ -415,9 +411,8 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.lstats = h->lstats();
     sa.gstats = h->gstats();
     sa.ew = ew ? 1 : 0;
-    sa.ew_refresh = ew_refresh ? 1 : 0;
-    sa.gs_old = h->ew_buf(h->ew_cur);
-    sa.gs_new = ew_refresh ? h->ew_buf(1 - h->ew_cur) : nullptr;
+    sa.ew_buf = h->ew_buf(0);
+    sa.n_flat = c.n_flat;
     sa.ew_partials = h->ew_partials();
     hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s);
     if (e != hipSuccess) return h->hip_fail(e, "step kernel launch");
@@ -439,7 +434,10 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         ua.m = h->d_m;
         ua.coef = h->coef();
         ua.corr = h->corr();
-        ua.gs_old = h->ew_buf(h->ew_cur);
+        ua.ew_buf = h->ew_buf(0);
+        ua.n_flat = c.n_flat;
+        ua.state = h->state();
+        ua.refresh_every = c.refresh_every;
         ua.corr_flag = h->corr_flag();
         ua.lr = (float)h->lr;
         ua.momentum = (float)c.momentum;
@@ -451,8 +449,6 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         (void)hipEventRecord(ev[3], s);
         h->ev_pending.push_back(ev);
     }
-    if (commit) ++h->step_host;
-    if (ew_refresh) h->ew_cur ^= 1;
     h->last_stream = s;
     h->has_stats = true;
     return AGS_OK;
@@ -620,7 +616,7 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
     // Initial device state: tables, gradscale = 1, G_prev = 0, step = 0.
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     std::vector<double> ones(cfg->n_layers, 1.0);
-    DevState ds{0.0, 0};
+    DevState ds{0.0, 0, 0, 0};
     const struct {
         size_t off;
         const void* src;
@@ -721,21 +717,18 @@ ags_status ags_set_state(ags_handle* h, const double* gradscale_L, double g_sq_p
     // shared with them.
     hipError_t e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "waiting for the last stream");
-    DevState ds{g_sq_prev, step};
+    // g_prev and step only: the element-scale buffer index stays.
+    DevState ds{g_sq_prev, step, 0, 0};
     const size_t soff = h->wl.state - h->wl.gradscale;
-    std::memcpy(h->pinned + soff, &ds, sizeof ds);
-    if (ew) {
-        // The layer means belong to the element scales; only the state moves.
-        e = hipMemcpyAsync(h->ws + h->wl.state, h->pinned + soff, sizeof ds,
-                           hipMemcpyHostToDevice, h->last_stream);
-    } else {
-        std::memcpy(h->pinned, gradscale_L, L * sizeof(double));
-        e = hipMemcpyAsync(h->ws + h->wl.gradscale, h->pinned, h->wl.state_bytes,
-                           hipMemcpyHostToDevice, h->last_stream);
-    }
+    const size_t head = offsetof(DevState, ew_cur);
+    std::memcpy(h->pinned + soff, &ds, head);
+    if (!ew) std::memcpy(h->pinned, gradscale_L, L * sizeof(double));
+    e = ew ? hipMemcpyAsync(h->ws + h->wl.state, h->pinned + soff, head, hipMemcpyHostToDevice,
+                            h->last_stream)
+           : hipMemcpyAsync(h->ws + h->wl.gradscale, h->pinned, soff + head,
+                            hipMemcpyHostToDevice, h->last_stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "writing state");
-    h->step_host = step;
     return AGS_OK;
 }
 
@@ -765,12 +758,30 @@ ags_status ags_set_layer_state(ags_handle* h, const double* g_sq_prev_L) {
     return AGS_OK;
 }
 
+namespace {
+
+// The element-scale buffer in force (read from the device state).
+ags_status ew_current(ags_handle* h, int* cur) {
+    int32_t v = 0;
+    hipError_t e = hipMemcpyAsync(&v, h->ws + h->wl.state + offsetof(DevState, ew_cur), sizeof v,
+                                  hipMemcpyDeviceToHost, h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "reading the element-scale buffer index");
+    *cur = v ? 1 : 0;
+    return AGS_OK;
+}
+
+}  // namespace
+
 ags_status ags_get_elementwise_scale(ags_handle* h, float* scale, int64_t n) {
     if (!h) return AGS_E_ARG;
     if (!h->cfg.elementwise) return h->fail(AGS_E_STATE, "the handle has no element scales");
     if (!scale) return h->fail(AGS_E_ARG, "scale is NULL");
     if (n != h->cfg.n_flat) return h->fail(AGS_E_ARG, "n must equal n_flat");
-    hipError_t e = hipMemcpyAsync(scale, h->ew_buf(h->ew_cur), (size_t)n * sizeof(float),
+    int cur = 0;
+    ags_status st = ew_current(h, &cur);
+    if (st != AGS_OK) return st;
+    hipError_t e = hipMemcpyAsync(scale, h->ew_buf(cur), (size_t)n * sizeof(float),
                                   hipMemcpyDeviceToHost, h->last_stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "reading element scales");
@@ -793,10 +804,17 @@ ags_status ags_set_elementwise_scale(ags_handle* h, const float* scale, int64_t 
         for (int64_t j = 0; j < ly.numel; ++j) sum += (double)scale[ly.offset + j];
         mean[l] = sum / (double)ly.numel;
     }
-    hipError_t e = hipMemcpyAsync(h->ew_buf(h->ew_cur), scale, (size_t)n * sizeof(float),
-                                  hipMemcpyHostToDevice, h->last_stream);
+    // The scales go to buffer 0, which is then the one in force.
+    const int32_t zero = 0;
+    hipError_t e = hipStreamSynchronize(h->last_stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(h->ew_buf(0), scale, (size_t)n * sizeof(float), hipMemcpyHostToDevice,
+                           h->last_stream);
     if (e == hipSuccess)
         e = hipMemcpyAsync(h->ws + h->wl.gradscale, mean.data(), L * sizeof(double),
+                           hipMemcpyHostToDevice, h->last_stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(h->ws + h->wl.state + offsetof(DevState, ew_cur), &zero, sizeof zero,
                            hipMemcpyHostToDevice, h->last_stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "writing element scales");

@@ -76,8 +76,10 @@ struct ChunkSum {
 
 // Device-resident AGS state, updated by the last block of a committed step.
 struct DevState {
-    double g_prev;  // ||G||^2 of the last committed step (0 before the first)
-    int64_t step;   // steps completed
+    double g_prev;   // ||G||^2 of the last committed step (0 before the first)
+    int64_t step;    // steps completed
+    int32_t ew_cur;  // element scales: which of the two buffers is in force
+    int32_t pad_;
 };
 
 // Per-tile fp32 partial sums: W (sum w^2), G (sum gbar^2), D (sum over
@@ -123,11 +125,12 @@ struct StepArgs {
     unsigned* layer_chunk_count;  // [n_layers] chunks finished (reset by the last)
     ags_layer_stats* lstats;
     ags_global_stats* gstats;
-    // Element scales (elementwise AGS; all null / 0 otherwise).
+    // Element scales (elementwise AGS; all null / 0 otherwise).  The buffer
+    // in force and whether a step refreshes are read from the device state
+    // (state->ew_cur, state->step), so a captured step replays correctly.
     int ew;                  // the scale is per element
-    int ew_refresh;          // this step refreshes the element scales
-    const float* gs_old;     // [n_flat] scales in force before the step
-    float* gs_new;           // [n_flat] refreshed scales (refresh steps)
+    float* ew_buf;           // [2][n_flat] the two scale buffers
+    int64_t n_flat;
     float* ew_partials;      // [n_tiles] per-tile sums of the refreshed scales
 };
 
@@ -143,7 +146,10 @@ struct UpdateArgs {
     float* m;
     const float2* coef;   // LARS update: (a_l, b_l)
     const float2* corr;   // correction pass: c = x + y * gs_old_j per layer
-    const float* gs_old;  // element scales in force before the step (or null)
+    const float* ew_buf;  // [2][n_flat] element scales (or null)
+    int64_t n_flat;
+    const DevState* state;  // after the step: the buffer in force and the step count
+    int refresh_every;
     const int* corr_flag;
     float lr;
     float momentum;

@@ -463,12 +463,12 @@ __device__ __forceinline__ bool surely_sensitive(double g_prev, long long step) 
 
 // Sum of the tile partials [tb, te) in fp64, in a fixed order; every
 // thread of the block gets the result.
-__device__ Sum4 sum_tiles(const StepArgs& a, int tb, int te, Sum4* sh) {
+__device__ Sum4 sum_tiles(const StepArgs& a, int tb, int te, Sum4* sh, bool ew_refresh) {
     // Four independent accumulators per thread (tiles i, i + 256, i + 512,
     // i + 768, then the next 1024), combined in a fixed order, so that four
     // loads are in flight per thread.
     constexpr int U = 4;
-    const bool ex = a.ew_refresh != 0;
+    const bool ex = ew_refresh;
     Sum4 acc[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) acc[u] = {0.0, 0.0, 0.0, 0.0, 0.0};
@@ -511,14 +511,15 @@ __device__ Sum4 sum_tiles(const StepArgs& a, int tb, int te, Sum4* sh) {
     return block_sum4(v, sh);
 }
 
-__device__ __forceinline__ void write_layer(const StepArgs& a, int l, const Sum4& v) {
+__device__ __forceinline__ void write_layer(const StepArgs& a, int l, const Sum4& v,
+                                            bool ew_refresh) {
     ags_layer_stats& o = a.lstats[l];
     o.w_sq = v.w;
     o.g_sq = v.g;
     o.var = v.d / (double)a.K;
     o.gsmall_sq = v.s;
     // Mean of the refreshed element scales, taken over by finalize_global.
-    if (a.ew_refresh) o.gradscale = v.x / (double)a.layers[l].numel;
+    if (ew_refresh) o.gradscale = v.x / (double)a.layers[l].numel;
 }
 
 // The global decision and every layer's coefficients (one block, after all
@@ -545,14 +546,17 @@ struct Prefetch {
     double g_prev, gs, gpl;
     long long step;
     uint32_t flags;
+    int ew_cur;
+    bool ew_refresh;  // a committed elementwise step whose refresh is due
 };
 
 __device__ __forceinline__ Prefetch prefetch_global(const StepArgs& a) {
-    Prefetch p{0.0, 0.0, 0.0, 0, 0u};
-    if (threadIdx.x == 0) {
-        p.g_prev = a.state->g_prev;
-        p.step = a.state->step;
-    }
+    Prefetch p{0.0, 0.0, 0.0, 0, 0u, 0, false};
+    p.g_prev = a.state->g_prev;
+    p.step = a.state->step;
+    p.ew_cur = a.state->ew_cur;
+    p.ew_refresh = a.ew && a.commit && a.refresh_every > 0 &&
+                   ((p.step + 1) % a.refresh_every) == 0;
     const int l = threadIdx.x;
     if (l < a.n_layers) {
         p.flags = a.layers[l].flags;
@@ -564,6 +568,7 @@ __device__ __forceinline__ Prefetch prefetch_global(const StepArgs& a) {
 
 __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* shi,
                                 const Prefetch& pf) {
+    const bool ew_refresh = pf.ew_refresh;
     __shared__ int sh_sens, sh_pred;
     __shared__ long long sh_t;
     Sum4 v = {0.0, 0.0, 0.0, 0.0, 0.0};
@@ -597,6 +602,7 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         if (a.commit) {
             a.state->g_prev = G;
             a.state->step = t;
+            if (ew_refresh) a.state->ew_cur = 1 - pf.ew_cur;  // the refreshed buffer
         }
         sh_sens = sens;
         sh_pred = surely_sensitive(Gp, step);
@@ -661,7 +667,7 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         }
         double gsc = gs_old;
         if (a.ew) {
-            if (a.ew_refresh) {
+            if (ew_refresh) {
                 gsc = o.gradscale;
                 a.gradscale[l] = gsc;
             }
@@ -706,37 +712,38 @@ __device__ __forceinline__ float element_scale(float gsmall, double q, double in
 #endif
 }
 
-// One group of a tile.  EW: 0 per-layer coefficients; 1 element scales
-// applied (use_gs: the layer is scaled and the step is predicted not
-// sensitive); 2 applied and refreshed into a.gs_new, whose sum over the
-// group's elements goes to sx.
-template <typename GT, int KT, int RMODE, bool UPD, int EW, bool FULL>
+// One group of a tile.  EW: element scales from gs_old applied (use_gs:
+// the layer is scaled and the step is predicted not sensitive) and, when
+// refresh, the refreshed scales written to gs_new with their sum over the
+// group's elements in sx.  Without EW, per-layer coefficients.
+template <typename GT, int KT, int RMODE, bool UPD, bool EW, bool FULL>
 __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restrict__ g,
                                            int64_t idx, int n0, int n1, int K, float ca,
-                                           float cb, bool use_gs, bool scaled, float smax,
-                                           float& sw, float& sg, float& sd, float& ss,
-                                           float& sx) {
+                                           float cb, bool use_gs, bool scaled, bool refresh,
+                                           const float* __restrict__ gs_old,
+                                           float* __restrict__ gs_new, float smax, float& sw,
+                                           float& sg, float& sd, float& ss, float& sx) {
     constexpr bool late_wm = KT >= AGS_LATE_WM_K;
     constexpr int HS = Map<GT>::HS;
-    constexpr bool NT = EW > 0 && (sizeof(GT) == 2 ? AGS_EW_NT_BF16 : AGS_EW_NT_F32);
+    constexpr bool NT = EW && (sizeof(GT) == 2 ? AGS_EW_NT_BF16 : AGS_EW_NT_F32);
     float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
     double q[kVec];
     if (!late_wm) {
         load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
         if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
     }
-    constexpr int kb = EW > 0 ? RawGroup<GT>::kBatchEw : RawGroup<GT>::kBatch;
-    moments<GT, KT, RMODE, FULL, EW == 2, kb>(g, a.stride, idx, n0, n1, K, a.small_replica,
-                                              a.invK, gb, dv, gr, q);
+    constexpr int kb = EW ? RawGroup<GT>::kBatchEw : RawGroup<GT>::kBatch;
+    moments<GT, KT, RMODE, FULL, EW, kb>(g, a.stride, idx, n0, n1, K, a.small_replica, a.invK,
+                                         gb, dv, gr, q);
     if (late_wm) {
         load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
         if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
     }
     float gsv[kVec];
-    if (EW > 0) {
+    if (EW) {
         // Old scales: applied on scaled layers, carried over on the others.
-        if (use_gs || (EW == 2 && !scaled)) {
-            load_f32_as<NT, FULL, HS>(a.gs_old + idx, n0, n1, gsv);
+        if (use_gs || (refresh && !scaled)) {
+            load_f32_as<NT, FULL, HS>(gs_old + idx, n0, n1, gsv);
         } else {
 #pragma unroll
             for (int e = 0; e < kVec; ++e) gsv[e] = 1.0f;
@@ -756,7 +763,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
         // d = a gbar + b w ; m <- mu m + d ; w <- w - eta m
 #pragma unroll
         for (int e = 0; e < kVec; ++e) {
-            const float ae = (EW > 0 && use_gs) ? gsv[e] : ca;
+            const float ae = (EW && use_gs) ? gsv[e] : ca;
             const float d = fmaf(ae, gb[e], cb * wv[e]);
             mv[e] = fmaf(a.momentum, mv[e], d);
             wv[e] = fmaf(-a.lr, mv[e], wv[e]);
@@ -764,7 +771,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
         store_f32_as<NT, FULL, HS>(a.w + idx, n0, n1, wv);
         store_f32_as<NT, FULL, HS>(a.m + idx, n0, n1, mv);
     }
-    if (EW == 2) {
+    if (EW && refresh) {
         float sn[kVec];
         if (scaled) {
             const double invK = 1.0 / (double)K;
@@ -777,7 +784,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
 #pragma unroll
             for (int e = 0; e < kVec; ++e) sn[e] = gsv[e];
         }
-        store_f32_as<NT, FULL, HS>(a.gs_new + idx, n0, n1, sn);
+        store_f32_as<NT, FULL, HS>(gs_new + idx, n0, n1, sn);
 #pragma unroll
         for (int e = 0; e < kVec; ++e) {
             const bool valid = FULL || (e < kHalf ? e < n0 : e - kHalf < n1);
@@ -796,7 +803,7 @@ __device__ __forceinline__ int tile_of_block(int b, int n, int xcd_map) {
     return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
 }
 
-template <typename GT, int KT, int RMODE, bool UPD, int EW>
+template <typename GT, int KT, int RMODE, bool UPD, bool EW>
 __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     __shared__ float red[5][kBlock / 64];
     const int ti = tile_of_block(blockIdx.x, gridDim.x, a.xcd_map);
@@ -808,14 +815,24 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     // Coefficients predicted before the step: on a step whose Delta is
     // infinite by definition the unscaled ones, otherwise the scaled ones.
     float ca = 1.0f, cb = 0.0f;
-    bool use_gs = false, scaled = false;
+    bool use_gs = false, scaled = false, refresh = false;
+    const float* gs_old = nullptr;
+    float* gs_new = nullptr;
     if (UPD) {
         const uint32_t f = a.layers[l].flags;
-        const bool pred = a.delta_scope ? surely_sensitive(a.g_prev_l[l], a.state->step)
-                                        : surely_sensitive(a.state->g_prev, a.state->step);
+        const long long step = a.state->step;
+        const bool pred = a.delta_scope ? surely_sensitive(a.g_prev_l[l], step)
+                                        : surely_sensitive(a.state->g_prev, step);
         scaled = (f & AGS_LAYER_SCALE) != 0;
+        if (EW) {
+            // The buffer in force and the refresh, from the device state.
+            const int cur = a.state->ew_cur;
+            gs_old = a.ew_buf + (size_t)cur * (size_t)a.n_flat;
+            gs_new = a.ew_buf + (size_t)(1 - cur) * (size_t)a.n_flat;
+            refresh = a.refresh_every > 0 && ((step + 1) % a.refresh_every) == 0;
+        }
         if (scaled && !pred) {
-            if (EW > 0) use_gs = true;
+            if (EW) use_gs = true;
             else if (a.mode == AGS_MODE_AGS) ca = (float)a.gradscale[l];
             else if (a.mode == AGS_MODE_STATIC) ca = (float)a.static_scale;
         }
@@ -826,7 +843,8 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f, sx = 0.0f;
     for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
         step_group<GT, KT, RMODE, UPD, EW, decltype(full)::value>(
-            a, g, idx, n0, n1, K, ca, cb, use_gs, scaled, smax, sw, sg, sd, ss, sx);
+            a, g, idx, n0, n1, K, ca, cb, use_gs, scaled, refresh, gs_old, gs_new, smax, sw, sg, sd,
+            ss, sx);
     });
 
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -834,7 +852,7 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     sg = wave_sum(sg);
     sd = wave_sum(sd);
     ss = wave_sum(ss);
-    if (EW == 2) sx = wave_sum(sx);
+    if (EW && refresh) sx = wave_sum(sx);
     if (lane == 0) {
         red[0][wid] = sw;
         red[1][wid] = sg;
@@ -850,7 +868,7 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
         p.d = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
         p.s = (red[3][0] + red[3][1]) + (red[3][2] + red[3][3]);
         a.partials[ti] = p;
-        if (EW == 2) a.ew_partials[ti] = (red[4][0] + red[4][1]) + (red[4][2] + red[4][3]);
+        if (EW && refresh) a.ew_partials[ti] = (red[4][0] + red[4][1]) + (red[4][2] + red[4][3]);
     }
 }
 
@@ -866,11 +884,11 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
     const Prefetch pf = prefetch_global(a);
     const FinChunk c = a.chunks[blockIdx.x];
     const int l = c.layer;
-    const Sum4 v = sum_tiles(a, c.tile_begin, c.tile_end, sh4);
+    const Sum4 v = sum_tiles(a, c.tile_begin, c.tile_end, sh4, pf.ew_refresh);
     const LayerDev ld = a.layers[l];
     const int nch = ld.chunk_end - ld.chunk_begin;
     if (nch == 1) {
-        if (threadIdx.x == 0) write_layer(a, l, v);
+        if (threadIdx.x == 0) write_layer(a, l, v, pf.ew_refresh);
     } else {
         if (threadIdx.x == 0) {
             a.chunk_sums[blockIdx.x] = ChunkSum{v.w, v.g, v.d, v.s, v.x};
@@ -891,7 +909,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
                 t.s += cs.s;
                 t.x += cs.x;
             }
-            write_layer(a, l, t);
+            write_layer(a, l, t, pf.ew_refresh);
             a.layer_chunk_count[l] = 0u;  // ready for the next launch
         }
     }
@@ -914,14 +932,15 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
 // scales (PE) c_j = x + y * gs_old_j.
 template <typename GT, int KT, bool PE, bool FULL>
 __device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __restrict__ g,
-                                              int64_t idx, int n0, int n1, int K, float2 c) {
+                                              int64_t idx, int n0, int n1, int K, float2 c,
+                                              const float* __restrict__ gs_old) {
     constexpr int HS = Map<GT>::HS;
     float gb[kVec], dv[kVec], gr[kVec], wv[kVec], mv[kVec], cv[kVec];
     double q[kVec];
     load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
     load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
     if (PE) {
-        load_f32<FULL, HS>(a.gs_old + idx, n0, n1, cv);
+        load_f32<FULL, HS>(gs_old + idx, n0, n1, cv);
 #pragma unroll
         for (int e = 0; e < kVec; ++e) cv[e] = fmaf(c.y, cv[e], c.x);
     } else {
@@ -946,6 +965,15 @@ __global__ __launch_bounds__(kBlock) void correct_kernel(UpdateArgs a) {
     if (*a.corr_flag == 0) return;
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
+    // Element scales in force before the step: the other buffer if the
+    // step (already counted) refreshed them.
+    const float* gs_old = nullptr;
+    if (a.ew_buf) {
+        const long long t = a.state->step;
+        const bool refreshed = a.refresh_every > 0 && (t % a.refresh_every) == 0;
+        const int cur = a.state->ew_cur;
+        gs_old = a.ew_buf + (size_t)(refreshed ? 1 - cur : cur) * (size_t)a.n_flat;
+    }
 #pragma unroll 1
     for (int ti = blockIdx.x; ti < a.n_tiles; ti += gridDim.x) {
         const Tile t = a.tiles[ti];
@@ -953,11 +981,11 @@ __global__ __launch_bounds__(kBlock) void correct_kernel(UpdateArgs a) {
         if (c.x == 0.0f && c.y == 0.0f) continue;
         if (c.y == 0.0f) {
             for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
-                correct_group<GT, KT, false, decltype(full)::value>(a, g, idx, n0, n1, K, c);
+                correct_group<GT, KT, false, decltype(full)::value>(a, g, idx, n0, n1, K, c, gs_old);
             });
         } else {
             for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
-                correct_group<GT, KT, true, decltype(full)::value>(a, g, idx, n0, n1, K, c);
+                correct_group<GT, KT, true, decltype(full)::value>(a, g, idx, n0, n1, K, c, gs_old);
             });
         }
     }
@@ -1008,13 +1036,11 @@ template <typename GT, int KT, int RMODE>
 void step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
     const dim3 grid(n_tiles), block(kBlock);
     if (!update)
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, false, 0>), grid, block, 0, s, a);
-    else if (a.ew_refresh)
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 2>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, false, false>), grid, block, 0, s, a);
     else if (a.ew)
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 1>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, true>), grid, block, 0, s, a);
     else
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 0>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, false>), grid, block, 0, s, a);
 }
 
 template <typename GT, int KT>

@@ -337,20 +337,26 @@ def test_bad_device_pointers_are_errors_not_faults():
             hip.hipFree(p)
 
 
-@pytest.mark.parametrize("lay_name,K,dtype", [("tiny_cnn", 4, "f32"), ("resnet18_cifar", 8, "f32")])
-def test_hip_graph_capture_replays_match_eager(lay_name, K, dtype):
+@pytest.mark.parametrize("lay_name,K,dtype,hyper", [
+    ("tiny_cnn", 4, "f32", {}), ("resnet18_cifar", 8, "f32", {}),
+    ("tiny_cnn", 4, "bf16", {"elementwise": True}),
+    ("resnet18_cifar", 8, "f32", {"elementwise": True, "refresh_every": 2}),
+    ("tiny_cnn", 4, "f32", {"delta_scope": "layer", "mode": "static"})])
+def test_hip_graph_capture_replays_match_eager(lay_name, K, dtype, hyper):
     """One ags_step captured in a HIP graph and replayed with fresh gradients
     copied into the captured buffer between replays (with eager work and a
     synchronisation in between) gives, replay after replay, the same bits as
-    eager steps.  The step enqueues kernels only (no memset or copy)."""
+    eager steps.  The step enqueues kernels only (no memset or copy), and
+    every decision that changes from step to step (the sensitive bit, the
+    refresh, the element-scale buffer in force) is taken on the device."""
     import torch
     lay = layouts.get_layout(lay_name)
     w0 = torch.from_numpy(synth.init_weights(lay, 5)).cuda()
     grads = [to_device(synth.replica_grads(lay, K, t, 5, dtype=dtype)) for t in range(6)]
     we, me = w0.clone(), torch.zeros_like(w0)
-    eager = ags.AGS(lay.table(), we, me, K, grad_dtype=dtype)
+    eager = ags.AGS(lay.table(), we, me, K, grad_dtype=dtype, **hyper)
     wg, mg = w0.clone(), torch.zeros_like(w0)
-    graphed = ags.AGS(lay.table(), wg, mg, K, grad_dtype=dtype)
+    graphed = ags.AGS(lay.table(), wg, mg, K, grad_dtype=dtype, **hyper)
     gbuf = torch.empty_like(grads[0])
     s = torch.cuda.Stream()
     torch.cuda.synchronize()
@@ -371,6 +377,8 @@ def test_hip_graph_capture_replays_match_eager(lay_name, K, dtype):
         for f in ags.LAYER_STATS_FIELDS:
             assert np.array_equal(se.layer[f], sg.layer[f]), (t, f)
         assert se.glob == sg.glob
+        if hyper.get("elementwise"):
+            assert np.array_equal(eager.get_elementwise_scale(), graphed.get_elementwise_scale())
     eager.close()
     graphed.close()
 
