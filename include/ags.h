@@ -169,7 +169,10 @@ typedef struct ags_handle ags_handle;
  *    which exits at once otherwise; LARS: the update; SGD: none). */
 #define AGS_N_KERNELS 3
 
-/* Bytes of device workspace ags_init would allocate for cfg (host only). */
+/* Bytes of device workspace ags_init would allocate for cfg (host only).
+ * Both reject (AGS_E_LAYOUT) layer tables that need 2^24 or more tiles of
+ * 2048 elements (about 3.4e10 parameters): a launch holds fewer than 2^32
+ * work-items. */
 ags_status ags_workspace_bytes(const ags_config *cfg, size_t *out_bytes);
 
 /* Create a handle bound to d_w, d_m (fp32 [n_flat], caller-owned, must
@@ -199,7 +202,8 @@ ags_status ags_step(ags_handle *h, const void *d_grads, int64_t replica_stride,
 ags_status ags_read_stats(ags_handle *h, ags_layer_stats *out_layers,
                           ags_global_stats *out_global);
 
-/* Learning rate for the steps launched after this call (host schedules). */
+/* Learning rate for the steps launched after this call (host schedules).
+ * A step captured in a HIP graph keeps the rate it was captured with. */
 ags_status ags_set_lr(ags_handle *h, double lr);
 
 /* Checkpoint / resume of the AGS state (w and m are the caller's).

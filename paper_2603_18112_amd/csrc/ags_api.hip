@@ -200,6 +200,18 @@ int64_t count_chunks(const ags_config& c) {
     return n;
 }
 
+// check_config, then the launch limits: a step kernel launch has one
+// 256-thread block per tile, and a launch holds fewer than 2^32 work-items.
+ags_status check_config_and_size(const ags_config* c, std::string& why) {
+    const ags_status s = check_config(c, why);
+    if (s != AGS_OK) return s;
+    if (count_tiles(*c) * ags::kBlock > (int64_t)0xffffffffLL) {
+        why = "the layers need too many tiles for one launch (tiles x 256 must be < 2^32)";
+        return AGS_E_LAYOUT;
+    }
+    return AGS_OK;
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Is [p, p + bytes) inside one device allocation of the current device?
@@ -477,7 +489,7 @@ const char* ags_last_error(const ags_handle* h) {
 
 ags_status ags_workspace_bytes(const ags_config* cfg, size_t* out_bytes) {
     std::string why;
-    ags_status s = check_config(cfg, why);
+    ags_status s = check_config_and_size(cfg, why);
     if (s != AGS_OK) {
         g_thread_error = why;
         return s;
@@ -498,7 +510,7 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         return AGS_E_ARG;
     }
     *out = nullptr;
-    ags_status st = check_config(cfg, why);
+    ags_status st = check_config_and_size(cfg, why);
     if (st != AGS_OK) {
         g_thread_error = why;
         return st;
@@ -512,10 +524,6 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         return AGS_E_ALIGN;
     }
     const int64_t n_tiles = count_tiles(*cfg);
-    if (n_tiles > 0x7fffffff) {
-        g_thread_error = "too many tiles";
-        return AGS_E_ARG;
-    }
 
     // Host-side tables.
     std::vector<Tile> tiles;

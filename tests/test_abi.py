@@ -134,6 +134,17 @@ def test_config_validation(lib, kw, status):
     assert ags.ags_last_error(None)
 
 
+def test_launch_size_limit(lib):
+    # 4e10 elements in one layer: 19.5M tiles of 2048, 5.0e9 work-items in
+    # the step kernel launch, more than one launch holds.
+    n = 40_000_000_000
+    st, msg = _ws(layers=[(0, n, 3)], n_flat=n)
+    assert st == ags.AGS_E_LAYOUT and "2^32" in msg
+    # 1.6e10 elements fit (7.8M tiles, 2.0e9 work-items)
+    st, _ = _ws(layers=[(0, 16_000_000_000, 3)], n_flat=16_000_000_000)
+    assert st == ags.AGS_OK
+
+
 def test_bad_enum_values(lib):
     cfg = ags.make_config(_table(), 136, 4)
     cfg.mode = 7
