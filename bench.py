@@ -435,7 +435,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": gdt,
+        "dtype": "f32",  # arithmetic: fp32 (statistics in fp64); gradients stored as grad_dtype
         "data": "synthetic",
         "config": {"workload": wkey, "layout": layout_name, "tensors": lay.n_layers,
                    "params": N, "K": K, "grad_dtype": gdt, "param_dtype": "f32",
