@@ -102,6 +102,17 @@ WsLayout ws_layout(const ags_config& c, int64_t n_tiles, int64_t n_chunks) {
 
 bool finite(double x) { return std::isfinite(x); }
 
+// The 32-bit value of an enum-typed field as the caller stored it: loading
+// an enum object that holds a value outside the enumeration is undefined
+// behaviour in C++, so fields are validated from their bytes.
+template <typename E>
+int32_t raw_enum(const E& e) {
+    static_assert(sizeof(E) == sizeof(int32_t), "enum fields are 32-bit");
+    int32_t v;
+    std::memcpy(&v, &e, sizeof v);
+    return v;
+}
+
 // Host-only validation of a configuration.  Fills why on failure.
 ags_status check_config(const ags_config* c, std::string& why) {
     if (!c) { why = "cfg is NULL"; return AGS_E_ARG; }
@@ -109,9 +120,10 @@ ags_status check_config(const ags_config* c, std::string& why) {
     if (!c->layers) { why = "layers is NULL"; return AGS_E_ARG; }
     if (c->n_flat < 1) { why = "n_flat must be >= 1"; return AGS_E_LAYOUT; }
     if (c->K < 1 || c->K > AGS_MAX_K) { why = "K out of range 1..AGS_MAX_K"; return AGS_E_ARG; }
-    if (c->grad_dtype != AGS_F32 && c->grad_dtype != AGS_BF16) { why = "bad grad_dtype"; return AGS_E_ARG; }
-    if (c->mode != AGS_MODE_SGD && c->mode != AGS_MODE_AGS && c->mode != AGS_MODE_LARS &&
-        c->mode != AGS_MODE_STATIC) {
+    const int32_t dt = raw_enum(c->grad_dtype), mode = raw_enum(c->mode);
+    if (dt != AGS_F32 && dt != AGS_BF16) { why = "bad grad_dtype"; return AGS_E_ARG; }
+    if (mode != AGS_MODE_SGD && mode != AGS_MODE_AGS && mode != AGS_MODE_LARS &&
+        mode != AGS_MODE_STATIC) {
         why = "bad mode";
         return AGS_E_ARG;
     }

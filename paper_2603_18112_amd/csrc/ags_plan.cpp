@@ -4,6 +4,7 @@
 // Kneedle knee of the time-batch curve).  Plain fp64 host code.
 #include <cmath>
 #include <cstdio>
+#include <cstring>
 #include <vector>
 
 #include "ags_plan.h"
@@ -24,7 +25,17 @@ double sync_term(int32_t nodes, ags_sync_model sync) {
     return 0.0;
 }
 
-bool valid_sync(int s) { return s == AGS_SYNC_NONE || s == AGS_SYNC_RING || s == AGS_SYNC_PS; }
+// Enum arguments and fields are validated from their 32-bit value: loading
+// an enum object outside its enumeration is undefined behaviour in C++.
+template <typename E>
+int32_t raw_enum(const E& e) {
+    static_assert(sizeof(E) == sizeof(int32_t), "enum values are 32-bit");
+    int32_t v;
+    std::memcpy(&v, &e, sizeof v);
+    return v;
+}
+
+bool valid_sync(int32_t s) { return s == AGS_SYNC_NONE || s == AGS_SYNC_RING || s == AGS_SYNC_PS; }
 
 double model_step(const ags_plan_model& m, int32_t nodes, double b) {
     return m.c0 + m.c_compute * b + m.c_sync * sync_term(nodes, m.sync);
@@ -32,7 +43,7 @@ double model_step(const ags_plan_model& m, int32_t nodes, double b) {
 
 ags_status check_model(const ags_plan_model* m) {
     if (!m) return fail(AGS_E_ARG, "model is NULL");
-    if (!valid_sync(m->sync)) return fail(AGS_E_ARG, "bad sync model");
+    if (!valid_sync(raw_enum(m->sync))) return fail(AGS_E_ARG, "bad sync model");
     if (!fin(m->c0) || !fin(m->c_compute) || !fin(m->c_sync))
         return fail(AGS_E_ARG, "model coefficients must be finite");
     return AGS_OK;
@@ -89,7 +100,7 @@ extern "C" {
 ags_status ags_plan_fit(const ags_plan_sample* samples, int32_t n, ags_sync_model sync,
                         uint32_t terms, ags_plan_model* out) {
     if (!samples || !out) return fail(AGS_E_ARG, "samples and out must not be NULL");
-    if (!valid_sync(sync)) return fail(AGS_E_ARG, "bad sync model");
+    if (!valid_sync(raw_enum(sync))) return fail(AGS_E_ARG, "bad sync model");
     if (terms == 0 || (terms & ~(AGS_PLAN_INTERCEPT | AGS_PLAN_COMPUTE | AGS_PLAN_SYNC)) != 0)
         return fail(AGS_E_ARG, "terms must be a non-empty set of AGS_PLAN_* bits");
     int p = 0;
@@ -181,7 +192,8 @@ ags_status ags_plan_knee(const double* x, const double* y, int32_t n, ags_knee_s
                          double sensitivity, int32_t* index) {
     if (!index) return fail(AGS_E_ARG, "index is NULL");
     if (n < 0 || (n > 0 && (!x || !y))) return fail(AGS_E_ARG, "bad arrays");
-    if (shape < AGS_KNEE_CONCAVE_INC || shape > AGS_KNEE_CONVEX_DEC) return fail(AGS_E_ARG, "bad shape");
+    const int32_t shp = raw_enum(shape);
+    if (shp < AGS_KNEE_CONCAVE_INC || shp > AGS_KNEE_CONVEX_DEC) return fail(AGS_E_ARG, "bad shape");
     if (!fin(sensitivity) || sensitivity < 0) return fail(AGS_E_ARG, "sensitivity must be finite, >= 0");
     for (int32_t i = 0; i < n; ++i) {
         if (!fin(x[i]) || !fin(y[i])) return fail(AGS_E_ARG, "x and y must be finite");
@@ -234,7 +246,8 @@ ags_status ags_plan_select(const ags_plan_model* m, const ags_plan_candidate* ca
     ags_status s = check_model(m);
     if (s != AGS_OK) return s;
     if (!best || n < 0 || (n > 0 && !cand)) return fail(AGS_E_ARG, "bad arguments");
-    if (objective < AGS_PLAN_MIN_TIME || objective > AGS_PLAN_KNEE) return fail(AGS_E_ARG, "bad objective");
+    const int32_t obj = raw_enum(objective);
+    if (obj < AGS_PLAN_MIN_TIME || obj > AGS_PLAN_KNEE) return fail(AGS_E_ARG, "bad objective");
     if (std::isnan(max_local_batch)) return fail(AGS_E_ARG, "max_local_batch is NaN");
     for (int32_t i = 0; i < n; ++i) {
         if (cand[i].nodes < 1 || cand[i].reserved != 0 || !fin(cand[i].global_batch) ||

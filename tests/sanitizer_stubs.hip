@@ -1,0 +1,21 @@
+// Launcher stubs for the sanitizer build of libags's host code (test
+// infrastructure): the host-only build has no kernels, and the host-side
+// tests it runs never reach a launch.
+#include "ags_internal.h"
+
+namespace ags {
+
+hipError_t launch_step(const StepArgs&, ags_dtype, int, bool, hipStream_t) {
+    return hipErrorInvalidDeviceFunction;
+}
+hipError_t launch_finalize(const StepArgs&, int, hipStream_t) {
+    return hipErrorInvalidDeviceFunction;
+}
+hipError_t launch_update(const UpdateArgs&, ags_dtype, hipStream_t) {
+    return hipErrorInvalidDeviceFunction;
+}
+hipError_t launch_correct(const UpdateArgs&, ags_dtype, hipStream_t) {
+    return hipErrorInvalidDeviceFunction;
+}
+
+}  // namespace ags
