@@ -124,6 +124,21 @@ def read_traffic(workload: str, kernel: str):
         return None
 
 
+def hbm_probe():
+    """Streaming-bandwidth ceilings of this GPU from the package's hbm_probe
+    program (read-only, copy, 5 reads : 1 write), run as a child process
+    before this process touches the GPU; None if it is not built."""
+    from paper_2603_18112_amd import _build
+    import subprocess
+    if not os.path.exists(_build.PROBE):
+        return None
+    r = subprocess.run([_build.PROBE], capture_output=True, text=True, timeout=120)
+    if r.returncode != 0:
+        log(f"hbm_probe failed: {r.stderr.strip()}")
+        return None
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
 def copy_probe(torch, nbytes=1 << 30, reps=20):
     """Device-to-device copy bandwidth (read + write bytes / time)."""
     n = nbytes // 4
@@ -272,6 +287,11 @@ def main():
               f"single-GPU AGS step (got --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
 
+    probe = None if (args.copy_probe or args.plan) else hbm_probe()
+    if probe:
+        log(f"hbm probe: read {probe['read_GBps']} GB/s, copy {probe['copy_GBps']} GB/s, "
+            f"5r:1w {probe['mix_5r1w_GBps']} GB/s")
+
     import numpy as np
     import torch
     from paper_2603_18112_amd import ags, layouts, synth
@@ -403,6 +423,8 @@ def main():
     achieved = ab[dom] / (avg_ms[dom] * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "frac_of_measured_read_ceiling": (round(achieved / probe["read_GBps"], 4)
+                                                  if probe else None),
                 "traffic": read_traffic(wkey, dom),
                 "algorithmic_bytes_per_launch": ab[dom],
                 "avg_launch_us": round(avg_ms[dom] * 1e3, 2)}
@@ -453,6 +475,7 @@ def main():
                                        "coefficients, then corrected (AGS); SGD never corrects"},
         "graph_replay_ms_per_step": None if graph_ms is None else round(graph_ms, 5),
         "device_copy_GBps": round(copy_bw, 1),
+        "hbm_probe": probe,
         "roofline": roofline,
         "cpu_baseline": cpu,
         "last_step": {"delta": s.glob["delta"], "sensitive": s.glob["sensitive"],

@@ -29,8 +29,19 @@ FLAGS = [
 ]
 
 
+#: the HBM bandwidth probe the benchmark runs for context (a program, not
+#: part of the library)
+PROBE_SRC = os.path.join(CSRC, "hbm_probe.hip")
+PROBE = os.path.join(LIBDIR, "hbm_probe")
+
+
 def command(out: str = LIB):
     return [HIPCC, *FLAGS, "-I", INCLUDE, "-I", CSRC, *SOURCES, "-o", out]
+
+
+def probe_command(out: str = PROBE):
+    flags = [f for f in FLAGS if f not in ("-fPIC", "-shared")]
+    return [HIPCC, *flags, PROBE_SRC, "-o", out]
 
 
 def build(verbose: bool = False) -> str:
@@ -45,6 +56,12 @@ def build(verbose: bool = False) -> str:
         sys.stderr.write(r.stdout + r.stderr)
         raise RuntimeError("hipcc failed to build libags.so")
     os.replace(tmp, LIB)
+    tmp = PROBE + f".tmp{os.getpid()}"
+    r = subprocess.run(probe_command(tmp), capture_output=True, text=True)
+    if r.returncode != 0:
+        sys.stderr.write(r.stdout + r.stderr)
+        raise RuntimeError("hipcc failed to build hbm_probe")
+    os.replace(tmp, PROBE)
     return LIB
 
 
