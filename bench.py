@@ -17,7 +17,11 @@ Prints one JSON line (last line of stdout):
                  average duration (HIP events on the launch stream), against
                  the 8 TB/s HBM peak; traffic = HBM bytes per launch from
                  rocprofv3 FETCH_SIZE/WRITE_SIZE (committed summary), or null
-                 when the kernels changed since it was taken
+                 when the kernels changed since it was taken; also as a
+                 fraction of two ceilings measured on this GPU by the
+                 package's hbm_probe (random data): a read-only stream, and
+                 the step's own byte pattern with trivial arithmetic
+  hbm_probe      those measured ceilings (and a copy), GB/s
   cpu_baseline   the float64 oracle on the host on whole steps of the same
                  workload (a reported baseline, not a target)
 
@@ -124,15 +128,18 @@ def read_traffic(workload: str, kernel: str):
         return None
 
 
-def hbm_probe():
+def hbm_probe(K: int, grad_dtype: str, n_elements: int):
     """Streaming-bandwidth ceilings of this GPU from the package's hbm_probe
-    program (read-only, copy, 5 reads : 1 write), run as a child process
-    before this process touches the GPU; None if it is not built."""
+    program (random data: read-only, copy, and the step's own byte pattern
+    for K replica rows of grad_dtype over n_elements with trivial
+    arithmetic), run as a child process before this process touches the
+    GPU; None if it is not built."""
     from paper_2603_18112_amd import _build
     import subprocess
     if not os.path.exists(_build.PROBE):
         return None
-    r = subprocess.run([_build.PROBE], capture_output=True, text=True, timeout=120)
+    r = subprocess.run([_build.PROBE, str(K), grad_dtype, str(n_elements)], capture_output=True,
+                       text=True, timeout=180)
     if r.returncode != 0:
         log(f"hbm_probe failed: {r.stderr.strip()}")
         return None
@@ -158,7 +165,7 @@ def copy_probe(torch, nbytes=1 << 30, reps=20):
     return 2 * n * 4 / (ms * 1e-3) / 1e9
 
 
-def cpu_baseline(layout, w0, grads_np, budget_s=12.0, max_steps=8):
+def cpu_baseline(layout, w0, grads_np, budget_s=20.0, max_steps=30):
     """The float64 oracle as it stands, single-threaded, on whole steps."""
     from oracle import OracleAGS
     o = OracleAGS(layout.table(), layout.n_flat, K, w0, grad_dtype="bf16" if E_G == 2 else "f32",
@@ -287,14 +294,17 @@ def main():
               f"single-GPU AGS step (got --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
 
-    probe = None if (args.copy_probe or args.plan) else hbm_probe()
-    if probe:
-        log(f"hbm probe: read {probe['read_GBps']} GB/s, copy {probe['copy_GBps']} GB/s, "
-            f"5r:1w {probe['mix_5r1w_GBps']} GB/s")
-
     import numpy as np
     import torch
     from paper_2603_18112_amd import ags, layouts, synth
+
+    probe = None
+    if not (args.copy_probe or args.plan):
+        p_lay, p_k, p_dt, _ = WORKLOADS[args.workload]
+        probe = hbm_probe(p_k, p_dt, layouts.get_layout(p_lay).n_params)
+    if probe:
+        log(f"hbm probe (random data): read {probe['read_GBps']} GB/s, copy {probe['copy_GBps']} GB/s, "
+            f"the step's byte pattern {probe['step_pattern_GBps']} GB/s")
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -424,6 +434,8 @@ def main():
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                 "frac_of_measured_read_ceiling": (round(achieved / probe["read_GBps"], 4)
+                                                  if probe else None),
+                "frac_of_measured_step_pattern": (round(achieved / probe["step_pattern_GBps"], 4)
                                                   if probe else None),
                 "traffic": read_traffic(wkey, dom),
                 "algorithmic_bytes_per_launch": ab[dom],

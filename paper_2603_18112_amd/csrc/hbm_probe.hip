@@ -1,16 +1,50 @@
-// hbm_probe: streaming bandwidth of this GPU's HBM for the benchmark's
-// context (not part of the AGS library).  Three patterns over 4 GiB of
-// device memory, each timed with HIP events over 10 launches:
-//   read   16-byte non-temporal loads only (the ceiling of a read stream),
-//   copy   one non-temporal read stream, one write stream,
-//   mix    four non-temporal read streams and one read-modify-write stream,
-//          5 reads : 1 write by bytes, the byte mix of the AGS step.
-// Prints one JSON line; exits non-zero on any HIP error.
+// hbm_probe: streaming-bandwidth ceilings of this GPU's HBM, for the
+// benchmark's context (not part of the AGS library).  Every buffer is first
+// filled with random bits (random data streams measurably slower than
+// zeros), then each pattern is timed with HIP events:
+//   read  16-byte non-temporal loads only over 4 GiB (best of four grids),
+//   copy  one non-temporal read stream and one write stream, 2 GiB each way,
+//   step  the AGS step's own byte pattern with trivial arithmetic: K replica
+//         rows (bf16 or fp32, non-temporal 16-byte loads) and the fp32 w and
+//         m rows read and written, one 256-thread block per 2048-element
+//         tile, the lane mapping of the step kernel.  Its rate is the
+//         ceiling of that access pattern on this GPU: what a kernel moving
+//         exactly those bytes, with no statistics, sustains.
+// Usage: hbm_probe [K grad_dtype(bf16|f32) n_elements]; without arguments
+// the step pattern is the ResNet-50 layout's (K = 16, bf16, 25,557,032).
+// Prints one JSON line; exits non-zero on any HIP error or bad argument.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
+#include <cstdlib>
+#include <cstring>
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kTile = 2048;  // elements per block, as the step kernel's tiles
+
+__global__ __launch_bounds__(256) void fill_random(unsigned* p, size_t n_words, unsigned seed,
+                                                   int kind) {
+    for (size_t i = blockIdx.x * 256 + threadIdx.x; i < n_words; i += (size_t)gridDim.x * 256) {
+        unsigned h = (unsigned)i * 2654435761u ^ seed;
+        h ^= h >> 15;
+        h *= 2246822519u;
+        h ^= h >> 13;
+        h *= 3266489917u;
+        h ^= h >> 16;
+        unsigned v;
+        if (kind == 0) {
+            // two bf16 values: random sign and mantissa, exponent 2^-16 .. 2^-1
+            const unsigned a = (h & 0x807fu) | ((0x6fu + ((h >> 8) & 15u)) << 7);
+            const unsigned b = ((h >> 16) & 0x807fu) | ((0x6fu + ((h >> 24) & 15u)) << 7);
+            v = a | (b << 16);
+        } else {
+            // one fp32 value: random sign and mantissa, exponent 2^-16 .. 2^-1
+            v = (h & 0x807fffffu) | ((0x6fu + ((h >> 23) & 15u)) << 23);
+        }
+        p[i] = v;
+    }
+}
 
 __global__ __launch_bounds__(256) void probe_read(const u32x4* __restrict__ p, size_t n,
                                                   unsigned* out) {
@@ -19,7 +53,7 @@ __global__ __launch_bounds__(256) void probe_read(const u32x4* __restrict__ p, s
         const u32x4 v = __builtin_nontemporal_load(p + i);
         acc ^= v.x ^ v.y ^ v.z ^ v.w;
     }
-    // the buffer holds zeros, so this store never happens; it keeps the loads
+    // never true for the fill's values (a random match is harmless); keeps the loads
     if (acc == 0x9e3779b9u) out[0] = acc;
 }
 
@@ -29,15 +63,78 @@ __global__ __launch_bounds__(256) void probe_copy(const u32x4* __restrict__ p,
         q[i] = __builtin_nontemporal_load(p + i);
 }
 
-__global__ __launch_bounds__(256) void probe_mix(const u32x4* __restrict__ p,
-                                                 u32x4* __restrict__ q, size_t n) {
-    for (size_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
-        const u32x4 a = __builtin_nontemporal_load(p + i);
-        const u32x4 b = __builtin_nontemporal_load(p + n + i);
-        const u32x4 c = __builtin_nontemporal_load(p + 2 * n + i);
-        const u32x4 d = __builtin_nontemporal_load(p + 3 * n + i);
-        q[i] = q[i] ^ a ^ b ^ c ^ d;
+__device__ __forceinline__ void add_bf16x8(const u32x4& v, float (&s)[8]) {
+    const unsigned u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        s[2 * i] += __uint_as_float(u[i] << 16);
+        s[2 * i + 1] += __uint_as_float(u[i] & 0xffff0000u);
     }
+}
+
+// One block per tile of kTile elements; lane l of wave v owns, for bf16
+// rows, elements [512v + 8l, +8) (one 16-byte load per row), for fp32 rows
+// [512v + 4l, +4) and [512v + 256 + 4l, +4) (two 16-byte loads per row).
+// Rows are loaded in batches of B before any is used.  w and m: the same
+// elements, fp32, read and written.  n is a multiple of kTile.
+template <bool BF16>
+__global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads, size_t stride,
+                                                  int K, float* __restrict__ w,
+                                                  float* __restrict__ m) {
+    constexpr int B = 8;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const size_t base = (size_t)blockIdx.x * kTile + (size_t)wave * 512;
+    const size_t i0 = base + (BF16 ? 8 * lane : 4 * lane);
+    const size_t i1 = BF16 ? i0 + 4 : i0 + 256;
+    float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    float4 w0 = *reinterpret_cast<const float4*>(w + i0), w1 = *reinterpret_cast<const float4*>(w + i1);
+    float4 m0 = *reinterpret_cast<const float4*>(m + i0), m1 = *reinterpret_cast<const float4*>(m + i1);
+    for (int k0 = 0; k0 < K; k0 += B) {
+        if (BF16) {
+            const unsigned short* g = static_cast<const unsigned short*>(grads);
+            u32x4 v[B];
+#pragma unroll
+            for (int j = 0; j < B; ++j) {
+                const bool in = k0 + j < K;
+                const unsigned short* r = g + (size_t)(in ? k0 + j : 0) * stride;
+                v[j] = in ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(r + i0))
+                          : u32x4{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+            for (int j = 0; j < B; ++j) add_bf16x8(v[j], s);
+        } else {
+            const float* g = static_cast<const float*>(grads);
+            u32x4 a[B / 2], b[B / 2];
+            for (int kk = 0; kk < B; kk += B / 2) {
+#pragma unroll
+                for (int j = 0; j < B / 2; ++j) {
+                    const bool in = k0 + kk + j < K;
+                    const float* r = g + (size_t)(in ? k0 + kk + j : 0) * stride;
+                    a[j] = in ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(r + i0)) : u32x4{0u, 0u, 0u, 0u};
+                    b[j] = in ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(r + i1)) : u32x4{0u, 0u, 0u, 0u};
+                }
+#pragma unroll
+                for (int j = 0; j < B / 2; ++j) {
+                    s[0] += __uint_as_float(a[j].x); s[1] += __uint_as_float(a[j].y);
+                    s[2] += __uint_as_float(a[j].z); s[3] += __uint_as_float(a[j].w);
+                    s[4] += __uint_as_float(b[j].x); s[5] += __uint_as_float(b[j].y);
+                    s[6] += __uint_as_float(b[j].z); s[7] += __uint_as_float(b[j].w);
+                }
+            }
+        }
+    }
+    m0.x = fmaf(0.9f, m0.x, s[0]); m0.y = fmaf(0.9f, m0.y, s[1]);
+    m0.z = fmaf(0.9f, m0.z, s[2]); m0.w = fmaf(0.9f, m0.w, s[3]);
+    m1.x = fmaf(0.9f, m1.x, s[4]); m1.y = fmaf(0.9f, m1.y, s[5]);
+    m1.z = fmaf(0.9f, m1.z, s[6]); m1.w = fmaf(0.9f, m1.w, s[7]);
+    w0.x = fmaf(-1e-3f, m0.x, w0.x); w0.y = fmaf(-1e-3f, m0.y, w0.y);
+    w0.z = fmaf(-1e-3f, m0.z, w0.z); w0.w = fmaf(-1e-3f, m0.w, w0.w);
+    w1.x = fmaf(-1e-3f, m1.x, w1.x); w1.y = fmaf(-1e-3f, m1.y, w1.y);
+    w1.z = fmaf(-1e-3f, m1.z, w1.z); w1.w = fmaf(-1e-3f, m1.w, w1.w);
+    *reinterpret_cast<float4*>(w + i0) = w0;
+    *reinterpret_cast<float4*>(w + i1) = w1;
+    *reinterpret_cast<float4*>(m + i0) = m0;
+    *reinterpret_cast<float4*>(m + i1) = m1;
 }
 
 #define CHECK(x)                                                                  \
@@ -49,7 +146,48 @@ __global__ __launch_bounds__(256) void probe_mix(const u32x4* __restrict__ p,
         }                                                                         \
     } while (0)
 
-int main() {
+template <typename F>
+int time_launches(F&& launch, int reps, hipEvent_t e0, hipEvent_t e1, double* us_per) {
+    launch();
+    CHECK(hipGetLastError());
+    CHECK(hipEventRecord(e0));
+    for (int r = 0; r < reps; ++r) launch();
+    CHECK(hipEventRecord(e1));
+    CHECK(hipEventSynchronize(e1));
+    float ms = 0;
+    CHECK(hipEventElapsedTime(&ms, e0, e1));
+    *us_per = ms * 1e3 / reps;
+    return 0;
+}
+
+int fill(void* p, size_t bytes, unsigned seed, int kind) {
+    hipLaunchKernelGGL(fill_random, dim3(8192), dim3(256), 0, 0, static_cast<unsigned*>(p), bytes / 4,
+                       seed, kind);
+    CHECK(hipGetLastError());
+    return 0;
+}
+
+int main(int argc, char** argv) {
+    int K = 16;
+    bool bf16 = true;
+    long long n_req = 25557032;
+    if (argc == 4) {
+        K = atoi(argv[1]);
+        bf16 = strcmp(argv[2], "bf16") == 0;
+        n_req = atoll(argv[3]);
+        if (K < 1 || K > 1024 || n_req < 1 || (!bf16 && strcmp(argv[2], "f32") != 0)) {
+            fprintf(stderr, "hbm_probe: usage: hbm_probe [K bf16|f32 n_elements]\n");
+            return 2;
+        }
+    } else if (argc != 1) {
+        fprintf(stderr, "hbm_probe: usage: hbm_probe [K bf16|f32 n_elements]\n");
+        return 2;
+    }
+    hipEvent_t e0, e1;
+    CHECK(hipEventCreate(&e0));
+    CHECK(hipEventCreate(&e1));
+
+    // read and copy over 4 GiB
     const size_t bytes = (size_t)4 << 30;
     const size_t n = bytes / sizeof(u32x4);
     u32x4 *p = nullptr, *q = nullptr;
@@ -57,44 +195,66 @@ int main() {
     CHECK(hipMalloc(&p, bytes));
     CHECK(hipMalloc(&q, bytes));
     CHECK(hipMalloc(&out, sizeof(unsigned)));
-    CHECK(hipMemset(p, 0, bytes));
-    CHECK(hipMemset(q, 0, bytes));
-    hipEvent_t e0, e1;
-    CHECK(hipEventCreate(&e0));
-    CHECK(hipEventCreate(&e1));
-    const int reps = 10;
-    double best[3] = {0, 0, 0};
-    int best_grid[3] = {0, 0, 0};
+    if (fill(p, bytes, 1u, 1) || fill(q, bytes, 2u, 1)) return 1;
+    CHECK(hipDeviceSynchronize());
+    double best[2] = {0, 0};
+    int best_grid[2] = {0, 0};
     for (int grid : {2048, 4096, 8192, 16384}) {
-        for (int pat = 0; pat < 3; ++pat) {
-            // read: 4 GiB; copy: 2 GiB in, 2 GiB out; mix: 4 x 1 GiB in, 1 GiB in and out
-            const size_t np = pat == 0 ? n : (pat == 1 ? n / 2 : n / 4);
-            const double moved = pat == 0 ? (double)bytes : (pat == 1 ? 2.0 * np * 16 : 6.0 * np * 16);
-            auto launch = [&]() {
-                if (pat == 0) hipLaunchKernelGGL(probe_read, dim3(grid), dim3(256), 0, 0, p, np, out);
-                else if (pat == 1) hipLaunchKernelGGL(probe_copy, dim3(grid), dim3(256), 0, 0, p, q, np);
-                else hipLaunchKernelGGL(probe_mix, dim3(grid), dim3(256), 0, 0, p, q, np);
-            };
-            launch();
-            CHECK(hipGetLastError());
-            CHECK(hipEventRecord(e0));
-            for (int r = 0; r < reps; ++r) launch();
-            CHECK(hipEventRecord(e1));
-            CHECK(hipEventSynchronize(e1));
-            float ms = 0;
-            CHECK(hipEventElapsedTime(&ms, e0, e1));
-            const double gbps = reps * moved / (ms * 1e-3) / 1e9;
+        for (int pat = 0; pat < 2; ++pat) {
+            const size_t np = pat == 0 ? n : n / 2;
+            const double moved = pat == 0 ? (double)bytes : 2.0 * np * 16;
+            double us = 0;
+            const int rc = time_launches(
+                [&]() {
+                    if (pat == 0) hipLaunchKernelGGL(probe_read, dim3(grid), dim3(256), 0, 0, p, np, out);
+                    else hipLaunchKernelGGL(probe_copy, dim3(grid), dim3(256), 0, 0, p, q, np);
+                },
+                10, e0, e1, &us);
+            if (rc) return rc;
+            const double gbps = moved / (us * 1e-6) / 1e9;
             if (gbps > best[pat]) {
                 best[pat] = gbps;
                 best_grid[pat] = grid;
             }
         }
     }
-    printf("{\"read_GBps\": %.1f, \"read_grid\": %d, \"copy_GBps\": %.1f, \"copy_grid\": %d, "
-           "\"mix_5r1w_GBps\": %.1f, \"mix_grid\": %d, \"bytes\": %zu}\n",
-           best[0], best_grid[0], best[1], best_grid[1], best[2], best_grid[2], bytes);
     CHECK(hipFree(p));
     CHECK(hipFree(q));
+
+    // the step's pattern
+    const size_t es = bf16 ? 2 : 4;
+    const size_t ne = ((size_t)n_req + kTile - 1) / kTile * kTile;
+    const size_t stride = ne + kTile;  // rows staggered like the benchmark's replica stride
+    void* g = nullptr;
+    float *w = nullptr, *m = nullptr;
+    CHECK(hipMalloc(&g, (size_t)K * stride * es));
+    CHECK(hipMalloc(&w, ne * sizeof(float)));
+    CHECK(hipMalloc(&m, ne * sizeof(float)));
+    if (fill(g, (size_t)K * stride * es, 3u, bf16 ? 0 : 1) || fill(w, ne * 4, 4u, 1) ||
+        fill(m, ne * 4, 5u, 1))
+        return 1;
+    CHECK(hipDeviceSynchronize());
+    const int grid = (int)(ne / kTile);
+    double step_us = 0;
+    const int rc = time_launches(
+        [&]() {
+            if (bf16)
+                hipLaunchKernelGGL(probe_step<true>, dim3(grid), dim3(256), 0, 0, g, stride, K, w, m);
+            else
+                hipLaunchKernelGGL(probe_step<false>, dim3(grid), dim3(256), 0, 0, g, stride, K, w, m);
+        },
+        50, e0, e1, &step_us);
+    if (rc) return rc;
+    const double step_bytes = (double)ne * (double)(K * es + 16);
+    printf("{\"read_GBps\": %.1f, \"read_grid\": %d, \"copy_GBps\": %.1f, \"copy_grid\": %d, "
+           "\"step_pattern_GBps\": %.1f, \"step_pattern_us\": %.2f, \"step_pattern\": "
+           "{\"K\": %d, \"grad_dtype\": \"%s\", \"elements\": %zu, \"bytes_per_element\": %zu}, "
+           "\"bytes\": %zu, \"data\": \"random\"}\n",
+           best[0], best_grid[0], best[1], best_grid[1], step_bytes / (step_us * 1e-6) / 1e9, step_us,
+           K, bf16 ? "bf16" : "f32", ne, (size_t)K * es + 16, bytes);
+    CHECK(hipFree(g));
+    CHECK(hipFree(w));
+    CHECK(hipFree(m));
     CHECK(hipFree(out));
     return 0;
 }

@@ -40,6 +40,17 @@ def test_ragged_layout(K, dtype, r):
               label=f"ew ragged K={K} {dtype} r={r}")
 
 
+@pytest.mark.parametrize("n_layers", [1024, 1100])
+def test_many_layers(n_layers):
+    # Layer means of the refreshed scales over many short layers (the
+    # finalize's global part handles several layers per thread).
+    rng = np.random.default_rng(n_layers)
+    sizes = [int(x) for x in rng.integers(1, 3000, size=n_layers)]
+    cyc = [SD, layouts.LAYER_SCALE, 0, layouts.LAYER_DECAY]
+    lay = layouts.custom_layout(sizes, [cyc[i % 4] for i in range(n_layers)], pad=8)
+    run_steps(lay, 3, 3, elementwise=True, label=f"ew {n_layers} layers")
+
+
 def test_resnet18_cifar_k8_three_steps():
     lay = layouts.get_layout("resnet18_cifar")
     run_steps(lay, 8, 3, elementwise=True, label="ew r18")

@@ -116,6 +116,28 @@ def test_ragged_layout(K, dtype, r):
     run_steps(lay, K, 4, dtype=dtype, small_replica=r, label=f"ragged K={K} {dtype} r={r}")
 
 
+def _mixed_sizes(n, seed, hi=5000):
+    rng = np.random.default_rng(seed)
+    return [int(x) for x in rng.integers(1, hi, size=n)]
+
+
+@pytest.mark.parametrize("n_layers", [1024, 1300])
+def test_many_layers(n_layers):
+    # Many short layers of mixed sizes and flags: the finalize's per-layer
+    # blocks and its global part over more than one thread per layer.
+    sizes = _mixed_sizes(n_layers, n_layers)
+    cyc = [SD, layouts.LAYER_SCALE, 0, layouts.LAYER_DECAY]
+    flags = [cyc[i % 4] for i in range(n_layers)]
+    lay = layouts.custom_layout(sizes, flags, pad=8)
+    run_steps(lay, 3, 3, label=f"{n_layers} layers")
+
+
+def test_one_large_layer_among_many_small_ones():
+    sizes = [8] * 500 + [1500 * 2048] + [8] * 500
+    lay = layouts.custom_layout(sizes, pad=8)
+    run_steps(lay, 2, 3, dtype="bf16", label="large among small")
+
+
 def test_stride_larger_than_n_flat():
     lay = layouts.custom_layout([100, 9000, 13], pad=8)
     run_steps(lay, 4, 2, stride=lay.n_flat + 4096 + 8, label="stride")
