@@ -30,7 +30,7 @@ With --elementwise the scale of Algorithm 1 is kept per parameter element
 ones, (K*2 + 24) bytes per parameter.
 
 Usage: python bench.py [--gpus 1] [--steps 200] [--warmup 20]
-                       [--no-cpu-baseline] [--copy-probe] [--elementwise]
+                       [--no-cpu-baseline] [--no-probe] [--copy-probe] [--elementwise]
                        [--delta-scope global|layer] [--mode ags|sgd|lars|static]
 """
 from __future__ import annotations
@@ -276,6 +276,9 @@ def main():
     ap.add_argument("--mode", default="ags", choices=["ags", "sgd", "lars", "static"])
     ap.add_argument("--graph", action="store_true",
                     help="also time the step captured once in a HIP graph and replayed")
+    ap.add_argument("--no-probe", action="store_true",
+                    help="skip the hbm_probe child process (for runs under a profiler, whose "
+                         "preloaded library has already initialised the GPU in this process)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run the 1 GiB device copy (counter calibration)")
     ap.add_argument("--elementwise", action="store_true",
@@ -299,7 +302,7 @@ def main():
     from paper_2603_18112_amd import ags, layouts, synth
 
     probe = None
-    if not (args.copy_probe or args.plan):
+    if not (args.copy_probe or args.plan or args.no_probe):
         p_lay, p_k, p_dt, _ = WORKLOADS[args.workload]
         probe = hbm_probe(p_k, p_dt, layouts.get_layout(p_lay).n_params)
     if probe:

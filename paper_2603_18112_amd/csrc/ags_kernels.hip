@@ -341,7 +341,28 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
         }
     } else {
         // Runtime K, and the ragged end of a layer (rare; unrolling it
-        // would raise the register count of the whole kernel).
+        // would raise the register count of the whole kernel).  The fp32
+        // sums of every four replicas are added to fp64 totals: each d_k
+        // carries replica 0's own deviation, so one fp32 running sum would
+        // drift by k times it and gather a rounding error growing like K
+        // (about 1e-5 of the mean at K = 1024); with fp64 totals the error
+        // stays that of four terms.  Mean and spread are then formed in fp64
+        // and rounded once.
+        double t1[kVec], t2[kVec];
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) {
+            t1[e] = 0.0;
+            t2[e] = 0.0;
+        }
+        auto flush = [&]() {
+#pragma unroll
+            for (int e = 0; e < kVec; ++e) {
+                t1[e] += (double)s1[e];
+                t2[e] += (double)s2[e];
+                s1[e] = 0.0f;
+                s2[e] = 0.0f;
+            }
+        };
         int k = 1;
 #pragma unroll 1
         for (; k + 3 < K; k += 4) {
@@ -358,6 +379,7 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc(k + j, x[j]);
+            flush();
         }
 #pragma unroll 1
         for (; k < K; ++k) {
@@ -371,6 +393,14 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
             }
             acc(k, x);
         }
+        flush();
+        const double dK = (double)K;
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) {
+            gbar[e] = (float)((double)g0[e] + t1[e] / dK);
+            dev[e] = (float)fmax(t2[e] - t1[e] * (t1[e] / dK), 0.0);
+        }
+        return;
     }
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {

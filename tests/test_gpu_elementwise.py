@@ -40,6 +40,14 @@ def test_ragged_layout(K, dtype, r):
               label=f"ew ragged K={K} {dtype} r={r}")
 
 
+@pytest.mark.parametrize("K,dtype", [(100, "f32"), (1024, "bf16")])
+def test_large_k_runtime_replica_loop(K, dtype):
+    # The runtime-K replica loop with the fp64 replica sums of the refresh,
+    # up to the largest K the C-ABI accepts.
+    lay = layouts.custom_layout(RAGGED, pad=8)
+    run_steps(lay, K, 2, dtype=dtype, elementwise=True, label=f"ew large K={K} {dtype}")
+
+
 @pytest.mark.parametrize("n_layers", [1024, 1100])
 def test_many_layers(n_layers):
     # Layer means of the refreshed scales over many short layers (the

@@ -116,6 +116,15 @@ def test_ragged_layout(K, dtype, r):
     run_steps(lay, K, 4, dtype=dtype, small_replica=r, label=f"ragged K={K} {dtype} r={r}")
 
 
+@pytest.mark.parametrize("K,dtype", [(65, "bf16"), (100, "f32"), (1024, "bf16")])
+def test_large_k_runtime_replica_loop(K, dtype):
+    # K outside the compiled set {1, 2, 4, 8, 16, 32, 64} takes the
+    # runtime-K replica loop; 1024 is the largest K the C-ABI accepts.
+    assert ags.AGS_MAX_K == 1024
+    lay = layouts.custom_layout(RAGGED, pad=8)
+    run_steps(lay, K, 2, dtype=dtype, label=f"large K={K} {dtype}")
+
+
 def _mixed_sizes(n, seed, hi=5000):
     rng = np.random.default_rng(seed)
     return [int(x) for x in rng.integers(1, hi, size=n)]
