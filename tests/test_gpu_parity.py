@@ -238,6 +238,26 @@ def test_zero_and_nonfinite_gradients():
     p.close()
 
 
+def test_nonfinite_weight_is_flagged():
+    # W_l is not finite while every gradient norm is: the step is flagged
+    # although Delta is finite (the oracle's rule; nothing is compared
+    # element by element, w holds an infinity).
+    lay = layouts.custom_layout([300, 17], pad=8)
+    w0 = np.ones(lay.n_flat, np.float32)
+    w0[310] = np.inf
+    p = Pair(lay, 3, w0=w0)
+    g = np.ones((3, lay.n_flat), np.float32)
+    for t in range(2):
+        p.gpu.step(to_device(g))
+        _, og = p.ora.step(g)
+        s = p.gpu.read_stats()
+        assert s.glob["nonfinite"] == 1 == og["nonfinite"]
+        assert s.glob["sensitive"] == og["sensitive"] == (1 if t == 0 else 0)
+        # inf on the first step; inf - eta * inf = nan afterwards
+        assert not math.isfinite(s.layer["w_sq"][1]) and math.isfinite(s.layer["w_sq"][0])
+    p.close()
+
+
 # ----------------------------------------------------- state and contract --
 
 

@@ -459,6 +459,80 @@ def test_nonfinite_gradient_is_flagged_and_sensitive():
     assert gl["nonfinite"] == 1 and gl["sensitive"] == 1
 
 
+def test_nonfinite_weight_is_flagged():
+    # A non-finite weight makes W_l non-finite while the gradient norms stay
+    # finite: the step is flagged even though Delta is finite.
+    lay, table = _layers([8, 8])
+    g = np.ones((2, lay.n_flat), np.float32)
+    w = np.ones(lay.n_flat)
+    w[10] = np.inf
+    o = OracleAGS(table, lay.n_flat, 2, w)
+    _, gl = o.step(g)
+    assert gl["nonfinite"] == 1
+    _, gl = o.step(g)
+    assert gl["nonfinite"] == 1 and math.isfinite(gl["delta"]) and gl["delta"] == 0.0
+
+
+def test_refresh_period_and_lag():
+    """UpdateGradScale every third step (R5): the scale after step t is
+    sqrt(S)/(sqrt(G)+eps) of step t's own statistics (numpy) when t is a
+    multiple of 3, else the previous scale; the coefficient applied at step t
+    is the scale in force before it."""
+    rng = np.random.default_rng(77)
+    K, eps = 4, 1e-8
+    lay, table = _layers([50, 30])
+    w0 = rng.standard_normal(lay.n_flat)
+    # shared mean plus replica noise: the ratio stays below the clip
+    base = (rng.standard_normal(lay.n_flat) + 0.5 * rng.standard_normal((K, lay.n_flat)))
+    base = base.astype(np.float32)
+    o = OracleAGS(table, lay.n_flat, K, w0, eps=eps, refresh_every=3, delta=1e9)
+    expect = np.ones(2)
+    for t in range(1, 8):
+        g = (base * np.float32(1.0 + 0.01 * t)).astype(np.float32)
+        st, gl = o.step(g)
+        applied = np.ones(2) if t == 1 else expect.copy()   # step 1 is sensitive by definition
+        np.testing.assert_allclose(st["coef_a"], applied, rtol=1e-15)
+        if t % 3 == 0:
+            g64 = g.astype(np.float64)
+            for l, (oo, n, _) in enumerate(table):
+                S = float(np.sum(g64[0, oo:oo + n] ** 2))
+                G = float(np.sum(g64[:, oo:oo + n].mean(axis=0) ** 2))
+                expect[l] = min(math.sqrt(S) / (math.sqrt(G) + eps), math.sqrt(K))
+        np.testing.assert_allclose(st["gradscale"], expect, rtol=1e-13)
+    assert np.all(expect != 1.0) and np.all(expect < math.sqrt(K))
+
+
+def test_elementwise_unscaled_layer_ignores_its_element_scales():
+    """Element scales set on a layer without the scale flag are never
+    applied: that layer follows torch.optim.SGD on the plain mean, while the
+    scaled layer takes its scales on non-sensitive steps."""
+    rng = np.random.default_rng(5)
+    K = 3
+    flags = [layouts.LAYER_DECAY, SD]
+    lay, table = _layers([16, 16], flags)
+    w0 = rng.standard_normal(lay.n_flat)
+    g = rng.standard_normal((K, lay.n_flat)).astype(np.float32)
+    o = OracleAGS(table, lay.n_flat, K, w0, lr=0.05, refresh_every=0, elementwise=True,
+                  delta=1e9)
+    o.gradscale[:] = 3.0          # every element, including the unscaled layer
+    (o0, n0, _), (o1, n1, _) = table
+    p0 = torch.tensor(w0[o0:o0 + n0].copy(), requires_grad=True)
+    p1 = torch.tensor(w0[o1:o1 + n1].copy(), requires_grad=True)
+    opt = torch.optim.SGD([{"params": [p0], "weight_decay": 5e-4},
+                           {"params": [p1], "weight_decay": 5e-4}], lr=0.05, momentum=0.9)
+    gm = g.astype(np.float64).mean(axis=0)
+    for t in range(3):
+        st, gl = o.step(g)
+        assert gl["sensitive"] == (1 if t == 0 else 0)
+        assert st["coef_a"][0] == 1.0
+        assert st["coef_a"][1] == (1.0 if t == 0 else 3.0)
+        p0.grad = torch.tensor(gm[o0:o0 + n0])
+        p1.grad = torch.tensor(gm[o1:o1 + n1] * (1.0 if t == 0 else 3.0))
+        opt.step()
+    np.testing.assert_allclose(o.w[o0:o0 + n0], p0.detach().numpy(), rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(o.w[o1:o1 + n1], p1.detach().numpy(), rtol=1e-13, atol=1e-15)
+
+
 # --------------------------------------------------------------------------
 # state: stats() does not mutate, checkpoint / resume is exact
 
