@@ -105,9 +105,14 @@ def traffic_file(workload: str) -> str:
     return os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
 
 
-def workload_key(workload: str, elementwise: bool, delta_scope: str = "global") -> str:
+def workload_key(workload: str, elementwise: bool, delta_scope: str = "global",
+                 mode: str = "ags") -> str:
+    """Name of the committed counter summary for a run.  SGD and static
+    steps run the AGS step kernel (only the coefficients differ), so they
+    share its summary; LARS runs other kernels and has its own."""
     return (workload + ("_elementwise" if elementwise else "")
-            + ("_layer_delta" if delta_scope == "layer" else ""))
+            + ("_layer_delta" if delta_scope == "layer" else "")
+            + ("_lars" if mode == "lars" else ""))
 
 
 def read_traffic(workload: str, kernel: str):
@@ -328,7 +333,7 @@ def main():
     E_G = 2 if gdt == "bf16" else 4
     HYPER["elementwise"] = bool(args.elementwise)
     HYPER["delta_scope"] = args.delta_scope
-    wkey = workload_key(args.workload, args.elementwise, args.delta_scope)
+    wkey = workload_key(args.workload, args.elementwise, args.delta_scope, args.mode)
     lib = ags.load_library()
     log(f"libags: {ags.library_path()}")
     lay = layouts.get_layout(layout_name)
@@ -456,11 +461,13 @@ def main():
                "sample": f"median of {n} whole steps of {wkey}, float64, 1 thread"}
         log(f"cpu baseline: {sec:.2f} s/step")
 
+    headline = wkey == WORKLOAD and args.mode == "ags"
+    mode_note = "" if args.mode == "ags" else f", {args.mode.upper()} mode"
     out = {
         "metric": ("AGS step+stats GB/s & % HBM peak (ResNet-50 layout, K=16); steps/s"
-                   if wkey == WORKLOAD else
+                   if headline else
                    f"AGS step+stats GB/s ({desc}{', elementwise scales' if args.elementwise else ''}"
-                   f"{', per-layer Delta' if args.delta_scope == 'layer' else ''})"),
+                   f"{', per-layer Delta' if args.delta_scope == 'layer' else ''}{mode_note})"),
         "value": round(value, 1),
         "unit": "GB/s",
         "n_gpus": 1,

@@ -279,8 +279,12 @@ template <> struct RawGroup<float> {
 // practice, for fp32 ones), from which an element scale's denominator
 // gbar + eps is formed without the cancellation of the fp32 sums.
 
+// SPLIT: keep each later batch in its packed form until the batch before
+// it is summed (a scheduling barrier after the batch's loads).  Without it
+// the statistics-only step kernel widened all K = 16 bf16 replicas as they
+// arrived and took 202 VGPRs (two waves per SIMD); the sums are the same.
 template <typename GT, int KT, int RMODE, bool FULL, bool EX = false,
-          int BATCH = RawGroup<GT>::kBatch>
+          int BATCH = RawGroup<GT>::kBatch, bool SPLIT = false>
 __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride, int64_t idx,
                                         int n0, int n1, int K, int r, float invK,
                                         float (&gbar)[kVec], float (&dev)[kVec],
@@ -332,6 +336,7 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
             RawGroup<GT> x[KB];
 #pragma unroll
             for (int j = 0; j < KB; ++j) x[j].load(g + (int64_t)(kb + j) * stride + idx);
+            if constexpr (SPLIT) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int j = 0; j < KB; ++j) {
                 float v[kVec];
@@ -761,10 +766,14 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
     if (!late_wm) {
         load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
         if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
+        // Keep the w (and m) loads in front of the replica loads: without
+        // the barrier the statistics-only variant issued them only after
+        // consuming every replica, a second round trip per block.
+        if (!UPD) __builtin_amdgcn_sched_barrier(0);
     }
     constexpr int kb = EW ? RawGroup<GT>::kBatchEw : RawGroup<GT>::kBatch;
-    moments<GT, KT, RMODE, FULL, EW, kb>(g, a.stride, idx, n0, n1, K, a.small_replica, a.invK,
-                                         gb, dv, gr, q);
+    moments<GT, KT, RMODE, FULL, EW, kb, !UPD>(g, a.stride, idx, n0, n1, K, a.small_replica,
+                                               a.invK, gb, dv, gr, q);
     if (late_wm) {
         load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
         if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
