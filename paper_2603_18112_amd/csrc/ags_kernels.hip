@@ -911,6 +911,13 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     }
 }
 
+// Device-scope fences of the finalize's counting protocol: a block makes its
+// records visible before it counts itself done (release), and the block
+// that counts last sees every record before reading them (acquire).  A full
+// __threadfence() would also invalidate the XCD's L2 in every block.
+__device__ __forceinline__ void release_fence() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
+__device__ __forceinline__ void acquire_fence() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+
 // One block per chunk of at most kFinTilesPerChunk tiles of one layer.  A
 // layer of several chunks is finished by the block that counts its last
 // chunk (one device-scope atomic after a release fence), which adds the
@@ -931,13 +938,13 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
     } else {
         if (threadIdx.x == 0) {
             a.chunk_sums[blockIdx.x] = ChunkSum{v.w, v.g, v.d, v.s, v.x};
-            __threadfence();
+            release_fence();
             const unsigned prev = atomicAdd(&a.layer_chunk_count[l], 1u);
             sh_last = (prev + 1 == (unsigned)nch);
         }
         __syncthreads();
         if (!sh_last) return;
-        __threadfence();
+        acquire_fence();
         if (threadIdx.x == 0) {
             Sum4 t = {0.0, 0.0, 0.0, 0.0, 0.0};
             for (int q = ld.chunk_begin; q < ld.chunk_end; ++q) {
@@ -953,13 +960,13 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
         }
     }
     if (threadIdx.x == 0) {
-        __threadfence();
+        release_fence();
         const unsigned prev = atomicAdd(a.done_count, 1u);
         sh_last = (prev + 1 == (unsigned)a.n_layers);
     }
     __syncthreads();
     if (!sh_last) return;
-    __threadfence();
+    acquire_fence();
     finalize_global(a, a.updated != 0, sh4, shi, pf);
     if (threadIdx.x == 0) *a.done_count = 0u;  // ready for the next launch
 }
