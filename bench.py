@@ -312,7 +312,8 @@ def main():
         probe = hbm_probe(p_k, p_dt, layouts.get_layout(p_lay).n_params)
     if probe:
         log(f"hbm probe (random data): read {probe['read_GBps']} GB/s, copy {probe['copy_GBps']} GB/s, "
-            f"the step's byte pattern {probe['step_pattern_GBps']} GB/s")
+            f"the step's byte pattern {probe['step_pattern_GBps']} GB/s "
+            f"(cold {probe.get('step_pattern_cold_GBps')} GB/s)")
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -463,6 +464,7 @@ def main():
 
     headline = wkey == WORKLOAD and args.mode == "ags"
     mode_note = "" if args.mode == "ags" else f", {args.mode.upper()} mode"
+    cold_value = ab["whole_step"] / (cold_step * 1e-3) / 1e9
     out = {
         "metric": ("AGS step+stats GB/s & % HBM peak (ResNet-50 layout, K=16); steps/s"
                    if headline else
@@ -489,8 +491,13 @@ def main():
                    "parallelism": "single GPU (K replicas stand in for K data-parallel workers)"},
         "kernel_us": {n: round(v * 1e3, 2) for n, v in avg_ms.items()},
         "cold_cache": {"ms_per_step": round(cold_step, 5),
-                       "value": round(ab["whole_step"] / (cold_step * 1e-3) / 1e9, 1),
-                       "note": "median of single steps after a 1 GiB read evicts the caches"},
+                       "value": round(cold_value, 1),
+                       "frac_of_measured_cold_step_pattern": (
+                           round(cold_value / probe["step_pattern_cold_GBps"], 4)
+                           if probe and "step_pattern_cold_GBps" in probe else None),
+                       "note": "median of single whole steps after a 1 GiB read evicts the "
+                               "caches; the fraction is against hbm_probe's step pattern "
+                               "timed the same way"},
         "replica_stride": stride,
         "mispredicted_steps": {"ms_per_step": round(mis_ms, 5), "last_sensitive": mis_sens,
                                "note": "every step sensitive: applied with the predicted "

@@ -34,9 +34,11 @@ constexpr int64_t kMaxTilesPerLayer = AGS_MAX_TILES_PER_LAYER;
 // the last of them combines.
 constexpr int kFinTilesPerChunk = 4096;
 // From this many tiles on, the step kernel gives each XCD a contiguous range
-// of tiles (measured on MI355X: +1.6% for ResNet-50, 12,560 tiles, and
-// VGG-16, 67,569 tiles; -4.5% for ResNet-18, 5,493 tiles).
-constexpr int64_t kXcdMapMinTiles = 8192;
+// of tiles instead of the hardware's round-robin order.  Measured on MI355X
+// (same box, alternating builds): VGG-16, 67,569 tiles, 2.4% faster warm and
+// 2.3% cold with it; ResNet-50, 12,560 tiles, 2.4% slower warm and 4% slower
+// cold (K = 64: 2% and 1.2%); ResNet-18, 5,493 tiles, 4.5% slower.
+constexpr int64_t kXcdMapMinTiles = 32768;
 
 // Elements per tile of a layer of numel elements.
 inline int64_t tile_elems_for(int64_t numel) {
