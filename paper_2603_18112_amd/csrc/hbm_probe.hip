@@ -11,7 +11,8 @@
 //         ceiling of that access pattern on this GPU: what a kernel moving
 //         exactly those bytes, with no statistics, sustains.  It is timed
 //         warm (50 launches back to back) and cold (each launch alone after
-//         a 1 GiB read that evicts the L2s and the Infinity Cache).
+//         a 1 GiB read with ordinary loads, which evicts the L2s and the
+//         Infinity Cache).
 // Usage: hbm_probe [K grad_dtype(bf16|f32) n_elements]; without arguments
 // the step pattern is the ResNet-50 layout's (K = 16, bf16, 25,557,032).
 // Prints one JSON line; exits non-zero on any HIP error or bad argument.
@@ -56,6 +57,19 @@ __global__ __launch_bounds__(256) void probe_read(const u32x4* __restrict__ p, s
         acc ^= v.x ^ v.y ^ v.z ^ v.w;
     }
     // never true for the fill's values (a random match is harmless); keeps the loads
+    if (acc == 0x9e3779b9u) out[0] = acc;
+}
+
+// Eviction read: ordinary (temporal) loads, so that the lines are allocated
+// in the L2s and the Infinity Cache and displace what was there (streaming
+// loads would leave the caches as they were).
+__global__ __launch_bounds__(256) void evict_read(const u32x4* __restrict__ p, size_t n,
+                                                  unsigned* out) {
+    unsigned acc = 0;
+    for (size_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
+        const u32x4 v = p[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
     if (acc == 0x9e3779b9u) out[0] = acc;
 }
 
@@ -257,7 +271,7 @@ int main(int argc, char** argv) {
     constexpr int kCold = 21;
     float cold_ms[kCold];
     for (int r = 0; r < kCold; ++r) {
-        hipLaunchKernelGGL(probe_read, dim3(2048), dim3(256), 0, 0, evict, evict_bytes / 16, out);
+        hipLaunchKernelGGL(evict_read, dim3(2048), dim3(256), 0, 0, evict, evict_bytes / 16, out);
         CHECK(hipEventRecord(e0));
         if (bf16)
             hipLaunchKernelGGL(probe_step<true>, dim3(grid), dim3(256), 0, 0, g, stride, K, w, m);
