@@ -147,6 +147,67 @@ def test_one_large_layer_among_many_small_ones():
     run_steps(lay, 2, 3, dtype="bf16", label="large among small")
 
 
+def test_flat_buffer_beyond_2_31_elements():
+    """Element offsets past 2^31: a small layer, a filler of 2^31 + 4104
+    elements with zero gradients and uniform weights, and a small layer
+    after it (22 GB on the device).  The two small layers are compared
+    with the oracle run on them alone: a zero-gradient filler adds nothing
+    to ||gbar||^2, so Delta and every decision are the same.  The filler
+    follows momentum SGD on weight decay alone, in closed form, checked on
+    strided samples; its W is n w^2 and G, V, S are 0 (gradscale 1 by the
+    zero-norm rule)."""
+    import torch
+    fill = (1 << 31) + 4104
+    sizes = [1000, fill, 5000]
+    lay = layouts.custom_layout(sizes, pad=8)
+    table = lay.table()
+    (o0, n0, _), (of, nf, _), (o2, n2, _) = table
+    assert o2 > (1 << 31)
+    K, hyper = 1, dict(lr=0.1, momentum=0.9, weight_decay=5e-4, delta=0.5, eps=1e-8)
+    rng = np.random.default_rng(31)
+    small_w = rng.standard_normal(n0 + n2).astype(np.float32)
+    w = torch.full((lay.n_flat,), 0.5, dtype=torch.float32, device="cuda")
+    w[o0:o0 + n0] = torch.from_numpy(small_w[:n0]).cuda()
+    w[o2:o2 + n2] = torch.from_numpy(small_w[n0:]).cuda()
+    m = torch.zeros_like(w)
+    h = ags.AGS(table, w, m, K, grad_dtype="bf16", **hyper)
+    sub = [(0, n0, SD), (n0, n2, SD)]
+    ora = OracleAGS(sub, n0 + n2, K, small_w, grad_dtype="bf16", **hyper)
+    g = torch.zeros((1, lay.n_flat), dtype=torch.int16, device="cuda")
+    wf, mf = 0.5, 0.0
+    lam, mu, eta = hyper["weight_decay"], hyper["momentum"], hyper["lr"]
+    for t, c in enumerate([1.0, 1.1, 3.0]):        # the third step is sensitive
+        gs = synth.to_bf16_bits((c * rng.standard_normal((1, n0 + n2))).astype(np.float32))
+        g[0, o0:o0 + n0] = torch.from_numpy(gs[0, :n0].view(np.int16)).cuda()
+        g[0, o2:o2 + n2] = torch.from_numpy(gs[0, n0:].view(np.int16)).cuda()
+        h.step(g)
+        ol, og = ora.step(gs)
+        s = h.read_stats()
+        gl = {f: np.asarray(s.layer[f])[[0, 2]] for f in s.layer}
+        check_stats(gl, s.glob, ol, og, hyper["delta"], f"beyond 2^31 step {t + 1}")
+        # filler: closed form, uniform over the layer
+        mf = mu * mf + lam * wf
+        wf = wf - eta * mf
+        assert s.layer["g_sq"][1] == 0.0 and s.layer["var"][1] == 0.0
+        assert s.layer["gsmall_sq"][1] == 0.0 and s.layer["gradscale"][1] == 1.0
+        w_prev = wf + eta * mf
+        assert abs(s.layer["w_sq"][1] / (nf * w_prev * w_prev) - 1.0) < 1e-4
+        idx = torch.arange(of, of + nf, 7919 * 4099, device="cuda", dtype=torch.int64)
+        idx = torch.cat([idx, torch.tensor([of + nf - 1], device="cuda")])
+        ws, ms = w[idx].double().cpu().numpy(), m[idx].double().cpu().numpy()
+        assert np.all(ws == ws[0]) and np.all(ms == ms[0])
+        assert abs(ws[0] - wf) <= 1e-5 * abs(wf) and abs(ms[0] - mf) <= 1e-5 * abs(mf)
+        torch.cuda.synchronize()
+        wk = torch.cat([w[o0:o0 + n0], w[o2:o2 + n2]]).cpu().numpy()
+        mk = torch.cat([m[o0:o0 + n0], m[o2:o2 + n2]]).cpu().numpy()
+        check_params(wk, ora.w, sub, f"beyond 2^31 step {t + 1} w")
+        check_params(mk, ora.m, sub, f"beyond 2^31 step {t + 1} m")
+        log(f"  beyond 2^31: step {t + 1} ok (sensitive={og['sensitive']})")
+    h.close()
+    del w, m, g
+    torch.cuda.empty_cache()
+
+
 def test_stride_larger_than_n_flat():
     lay = layouts.custom_layout([100, 9000, 13], pad=8)
     run_steps(lay, 4, 2, stride=lay.n_flat + 4096 + 8, label="stride")
