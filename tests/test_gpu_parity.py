@@ -258,6 +258,35 @@ def test_forced_spike_takes_unscaled_branch():
     p.close()
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_exact_tie_at_the_threshold_is_sensitive(dtype):
+    """Delta = delta exactly is sensitive (Algorithm 1 scales only when
+    Delta < delta).  Two layers of the same size have the same tiles, so the
+    same gradients in both give bitwise equal G_l: a step with the second
+    layer zero and then one with it equal to the first doubles G exactly on
+    both sides, and Delta = (2G - G) / G = 1 exactly (2G - G is exact).
+    With delta = 1 that step is a tie."""
+    n, K = 5000, 4
+    lay = layouts.custom_layout([n, n], pad=8)
+    (o0, _, _), (o1, _, _) = lay.table()
+    x = synth.replica_grads(lay, K, 0, 7)[:, o0:o0 + n]
+    one = np.zeros((K, lay.n_flat), np.float32)
+    one[:, o0:o0 + n] = x
+    both = one.copy()
+    both[:, o1:o1 + n] = x
+    if dtype == "bf16":
+        one, both = synth.to_bf16_bits(one), synth.to_bf16_bits(both)
+    p = Pair(lay, K, dtype=dtype, delta=1.0)
+    expect = [(math.inf, 1), (0.0, 0), (1.0, 1), (0.0, 0)]
+    for t, (g, (d, sens)) in enumerate(zip([one, one, both, both], expect)):
+        s, (ol, og) = p.step(g, check=False, what=f"tie step {t + 1}")
+        assert s.glob["delta"] == d == og["delta"], (t, s.glob["delta"], og["delta"])
+        assert s.glob["sensitive"] == sens == og["sensitive"], t
+        np.testing.assert_allclose(s.layer["coef_a"], ol["coef_a"], rtol=1e-6)
+        p.check_state(f"tie step {t + 1}")
+    p.close()
+
+
 @pytest.mark.parametrize("K,dtype,mode", [(4, "f32", "ags"), (16, "bf16", "ags"),
                                           (3, "bf16", "ags"), (8, "f32", "static")])
 def test_mispredicted_steps_are_corrected(K, dtype, mode):
