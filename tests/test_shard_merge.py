@@ -1,7 +1,7 @@
 """The sharded design checked on the CPU (no ranks, no collectives).
 
 One GPU here runs the whole step.  Across G GPUs the path would shard as
-follows (DESIGN, "How the path would shard"): rank q holds K/G of the
+follows: rank q holds K/G of the
 replica gradients; it sums its replicas per element and, per layer, their
 squared norms sum_k ||g_k,l||^2 (and ||g_r,l||^2 where it holds the small-batch
 replica r); a reduce-scatter leaves rank q the replica sum, hence gbar, on a
