@@ -133,18 +133,19 @@ def read_traffic(workload: str, kernel: str):
         return None
 
 
-def hbm_probe(K: int, grad_dtype: str, n_elements: int):
+def hbm_probe(K: int, grad_dtype: str, n_elements: int, elementwise: bool = False):
     """Streaming-bandwidth ceilings of this GPU from the package's hbm_probe
     program (random data: read-only, copy, and the step's own byte pattern
     for K replica rows of grad_dtype over n_elements with trivial
-    arithmetic), run as a child process before this process touches the
-    GPU; None if it is not built."""
+    arithmetic, with the element-scale streams when elementwise), run as a
+    child process before this process touches the GPU; None if it is not
+    built."""
     from paper_2603_18112_amd import _build
     import subprocess
     if not os.path.exists(_build.PROBE):
         return None
-    r = subprocess.run([_build.PROBE, str(K), grad_dtype, str(n_elements)], capture_output=True,
-                       text=True, timeout=180)
+    cmd = [_build.PROBE, str(K), grad_dtype, str(n_elements)] + (["ew"] if elementwise else [])
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=180)
     if r.returncode != 0:
         log(f"hbm_probe failed: {r.stderr.strip()}")
         return None
@@ -309,7 +310,7 @@ def main():
     probe = None
     if not (args.copy_probe or args.plan or args.no_probe):
         p_lay, p_k, p_dt, _ = WORKLOADS[args.workload]
-        probe = hbm_probe(p_k, p_dt, layouts.get_layout(p_lay).n_params)
+        probe = hbm_probe(p_k, p_dt, layouts.get_layout(p_lay).n_params, bool(args.elementwise))
     if probe:
         log(f"hbm probe (random data): read {probe['read_GBps']} GB/s, copy {probe['copy_GBps']} GB/s, "
             f"the step's byte pattern {probe['step_pattern_GBps']} GB/s "
