@@ -329,6 +329,12 @@ class AGS:
         return ags_get_state(self.handle, self.n_layers)
 
     def set_state(self, gradscale, g_sq_prev, step):
+        # the C function reads n_layers values; with element scales it reads
+        # none (gradscale may be None)
+        if gradscale is not None:
+            gradscale = np.asarray(gradscale, dtype=np.float64).reshape(-1)
+            if gradscale.size != self.n_layers:
+                raise ValueError(f"expected {self.n_layers} gradscale values, got {gradscale.size}")
         ags_set_state(self.handle, gradscale, g_sq_prev, step)
 
     def get_layer_state(self):
