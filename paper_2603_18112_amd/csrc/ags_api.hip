@@ -434,7 +434,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.layer_chunk_count = reinterpret_cast<unsigned*>(h->ws + h->wl.chunk_count);
     sa.lstats = h->lstats();
     sa.gstats = h->gstats();
-    sa.ew = ew ? 1 : 0;
+    sa.ew = !ew ? 0 : (16 * c.n_flat > ags::kEwStreamMinBytes ? 2 : 1);
     sa.ew_buf = h->ew_buf(0);
     sa.n_flat = c.n_flat;
     sa.ew_partials = h->ew_partials();

@@ -40,6 +40,16 @@ constexpr int kFinTilesPerChunk = 4096;
 // cold (K = 64: 2% and 1.2%); ResNet-18, 5,493 tiles, 4.5% slower.
 constexpr int64_t kXcdMapMinTiles = 32768;
 
+// Element scales: the step kernel loads the scales in force and stores the
+// refreshed ones, w and m non-temporally once w, m and the two scale
+// buffers (16 bytes per element) pass this size; below it they can stay in
+// the 256 MB Infinity Cache from one step to the next and ordinary accesses
+// keep them there.  Measured on MI355X, fp32 K = 8, whole step, ordinary
+// against streaming: ResNet-18 (11.2M elements) 113.2 / 113.5 us, 16M
+// elements 157.8 / 157.1, 20M 195.7 / 186.2, ResNet-50 (25.6M) 272.2 /
+// 229.6, VGG-16 (138M) 1400 / 1358.
+constexpr int64_t kEwStreamMinBytes = 192ll << 20;
+
 // Elements per tile of a layer of numel elements.
 inline int64_t tile_elems_for(int64_t numel) {
     const int64_t per = (int64_t)kTileElems * kMaxTilesPerLayer;
@@ -130,7 +140,7 @@ struct StepArgs {
     // Element scales (elementwise AGS; all null / 0 otherwise).  The buffer
     // in force and whether a step refreshes are read from the device state
     // (state->ew_cur, state->step), so a captured step replays correctly.
-    int ew;                  // the scale is per element
+    int ew;                  // 0: per layer; per element with 1: ordinary, 2: streaming accesses
     float* ew_buf;           // [2][n_flat] the two scale buffers
     int64_t n_flat;
     float* ew_partials;      // [n_tiles] per-tile sums of the refreshed scales

@@ -64,16 +64,6 @@ namespace {
 #define AGS_LATE_WM_K 1 << 30
 #endif
 
-// Element-scale kernels with bf16 gradients: the scale loads, the refreshed
-// scale stores and the w and m stores are non-temporal (measured on MI355X,
-// ResNet-50 layout K = 16: step kernel 262 -> 221 us); with fp32 gradients
-// ordinary accesses measured faster (ResNet-18 K = 8: 97 against 101 us).
-#ifndef AGS_EW_NT_BF16
-#define AGS_EW_NT_BF16 1
-#endif
-#ifndef AGS_EW_NT_F32
-#define AGS_EW_NT_F32 0
-#endif
 
 // bf16 gradients: a lane's two halves are adjacent (8 consecutive elements,
 // one 16-byte load per replica); fp32 gradients: 256 elements apart (every
@@ -751,7 +741,10 @@ __device__ __forceinline__ float element_scale(float gsmall, double q, double in
 // the layer is scaled and the step is predicted not sensitive) and, when
 // refresh, the refreshed scales written to gs_new with their sum over the
 // group's elements in sx.  Without EW, per-layer coefficients.
-template <typename GT, int KT, int RMODE, bool UPD, bool EW, bool FULL>
+// EW: 0 = one scale per layer; 1 = element scales, ordinary accesses; 2 =
+// element scales with non-temporal scale loads and scale, w and m stores
+// (the host's choice for working sets the Infinity Cache cannot keep).
+template <typename GT, int KT, int RMODE, bool UPD, int EW, bool FULL>
 __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restrict__ g,
                                            int64_t idx, int n0, int n1, int K, float ca,
                                            float cb, bool use_gs, bool scaled, bool refresh,
@@ -760,7 +753,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
                                            float& sg, float& sd, float& ss, float& sx) {
     constexpr bool late_wm = KT >= AGS_LATE_WM_K;
     constexpr int HS = Map<GT>::HS;
-    constexpr bool NT = EW && (sizeof(GT) == 2 ? AGS_EW_NT_BF16 : AGS_EW_NT_F32);
+    constexpr bool NT = EW == 2;
     float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
     double q[kVec];
     if (!late_wm) {
@@ -772,7 +765,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
         if (!UPD) __builtin_amdgcn_sched_barrier(0);
     }
     constexpr int kb = EW ? RawGroup<GT>::kBatchEw : RawGroup<GT>::kBatch;
-    moments<GT, KT, RMODE, FULL, EW, kb, !UPD>(g, a.stride, idx, n0, n1, K, a.small_replica,
+    moments<GT, KT, RMODE, FULL, EW != 0, kb, !UPD>(g, a.stride, idx, n0, n1, K, a.small_replica,
                                                a.invK, gb, dv, gr, q);
     if (late_wm) {
         load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
@@ -842,7 +835,7 @@ __device__ __forceinline__ int tile_of_block(int b, int n, int xcd_map) {
     return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
 }
 
-template <typename GT, int KT, int RMODE, bool UPD, bool EW>
+template <typename GT, int KT, int RMODE, bool UPD, int EW>
 __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     __shared__ float red[5][kBlock / 64];
     const int ti = tile_of_block(blockIdx.x, gridDim.x, a.xcd_map);
@@ -1082,11 +1075,13 @@ template <typename GT, int KT, int RMODE>
 void step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
     const dim3 grid(n_tiles), block(kBlock);
     if (!update)
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, false, false>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, false, 0>), grid, block, 0, s, a);
+    else if (a.ew == 2)
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 2>), grid, block, 0, s, a);
     else if (a.ew)
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, true>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 1>), grid, block, 0, s, a);
     else
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, false>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 0>), grid, block, 0, s, a);
 }
 
 template <typename GT, int KT>

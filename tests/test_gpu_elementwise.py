@@ -72,6 +72,18 @@ def test_resnet50_k16_bf16_three_steps():
     log(f"  ew r50 worst param error / tolerance scale: w {w[0]:.2e} m {w[1]:.2e}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_streaming_variant_above_the_cache_sized_working_set(dtype):
+    # 13.1M elements: w, m and the two scale buffers (16 bytes per element)
+    # pass 192 MiB, so the step kernel takes its non-temporal variant; ragged
+    # layers and one large one, every flag combination.
+    sizes = [13_000_000, 7, 2049, 20003, 63, 77_777, 1]
+    flags = [SD, layouts.LAYER_SCALE, 0, layouts.LAYER_DECAY, SD, SD, 0]
+    lay = layouts.custom_layout(sizes, flags, pad=8)
+    assert 16 * lay.n_flat > 192 << 20
+    run_steps(lay, 4, 3, dtype=dtype, elementwise=True, label=f"ew streaming {dtype}")
+
+
 def test_refresh_every_three_steps():
     # Scales refresh on steps 3 and 6 only: the buffer in force must carry
     # over between refreshes.
