@@ -84,6 +84,14 @@ def test_streaming_variant_above_the_cache_sized_working_set(dtype):
     run_steps(lay, 4, 3, dtype=dtype, elementwise=True, label=f"ew streaming {dtype}")
 
 
+def test_vgg16_k8_two_steps():
+    # The largest layout: streaming accesses, the XCD-aware tile order and
+    # fp32 replicas at full size (138M elements, 67,569 tiles).
+    lay = layouts.get_layout("vgg16")
+    run_steps(lay, 8, 2, check_each=False, elementwise=True, stride=layouts.replica_stride(lay),
+              label="ew vgg16")
+
+
 def test_refresh_every_three_steps():
     # Scales refresh on steps 3 and 6 only: the buffer in force must carry
     # over between refreshes.
