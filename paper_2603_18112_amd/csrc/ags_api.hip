@@ -217,7 +217,7 @@ int64_t count_chunks(const ags_config& c) {
 ags_status check_config_and_size(const ags_config* c, std::string& why) {
     const ags_status s = check_config(c, why);
     if (s != AGS_OK) return s;
-    if (count_tiles(*c) * ags::kBlock > (int64_t)0xffffffffLL) {
+    if (count_tiles(*c) * ags::kTileBlock > (int64_t)0xffffffffLL) {
         why = "the layers need too many tiles for one launch (tiles x 256 must be < 2^32)";
         return AGS_E_LAYOUT;
     }

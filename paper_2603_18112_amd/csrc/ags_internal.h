@@ -18,11 +18,18 @@ namespace ags {
 // for 8192 (the many short blocks balance the 256 CUs best).
 constexpr int kBlock = 256;
 constexpr int kVec = 8;
-#ifndef AGS_TILE_ELEMS
-#define AGS_TILE_ELEMS 2048
+// Threads of a block of the kernels that walk tiles (step, correction and
+// LARS update); a round of such a block covers kTileBlock * kVec elements.
+#ifndef AGS_TILE_BLOCK
+#define AGS_TILE_BLOCK 256
 #endif
-constexpr int kTileElems = AGS_TILE_ELEMS;  // a multiple of kBlock * kVec
-static_assert(kTileElems % (kBlock * kVec) == 0, "tile must hold whole block rounds");
+constexpr int kTileBlock = AGS_TILE_BLOCK;
+static_assert(kTileBlock % 64 == 0 && kTileBlock >= 64 && kTileBlock <= 1024, "whole waves");
+#ifndef AGS_TILE_ELEMS
+#define AGS_TILE_ELEMS (AGS_TILE_BLOCK * 8)
+#endif
+constexpr int kTileElems = AGS_TILE_ELEMS;  // a multiple of kTileBlock * kVec
+static_assert(kTileElems % (kTileBlock * kVec) == 0, "tile must hold whole block rounds");
 // A layer is cut into at most this many tiles (bigger layers get tiles of a
 // multiple of kTileElems).
 #ifndef AGS_MAX_TILES_PER_LAYER

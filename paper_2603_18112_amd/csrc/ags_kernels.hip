@@ -75,8 +75,8 @@ namespace {
 
 constexpr int kHalf = 4;                    // elements per half group
 constexpr int kWaveSpan = 512;              // elements per wave per round
-constexpr int kRound = kBlock * kVec;       // 2048 elements per block per round
-static_assert(kRound == (kBlock / 64) * kWaveSpan, "round layout");
+constexpr int kRound = kTileBlock * kVec;   // elements per tile-kernel block per round
+static_assert(kRound == (kTileBlock / 64) * kWaveSpan, "round layout");
 
 // Distance between a lane's two halves for gradients of type GT.
 template <typename GT> struct Map {
@@ -825,6 +825,14 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
     }
 }
 
+// Sum of the N wave totals of a block in a fixed pairwise order (for four
+// waves: (v0 + v1) + (v2 + v3)).
+template <int N>
+__device__ __forceinline__ float tree_sum(const float* v) {
+    if constexpr (N == 1) return v[0];
+    else return tree_sum<N / 2>(v) + tree_sum<N - N / 2>(v + N / 2);
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs.  With xcd_map each
 // XCD walks a contiguous range of tiles instead of every 8th tile (a
 // bijection of block indices onto tiles).
@@ -836,8 +844,8 @@ __device__ __forceinline__ int tile_of_block(int b, int n, int xcd_map) {
 }
 
 template <typename GT, int KT, int RMODE, bool UPD, int EW>
-__global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
-    __shared__ float red[5][kBlock / 64];
+__global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
+    __shared__ float red[5][kTileBlock / 64];
     const int ti = tile_of_block(blockIdx.x, gridDim.x, a.xcd_map);
     const Tile t = a.tiles[ti];
     const int l = t.layer;
@@ -895,12 +903,12 @@ __global__ __launch_bounds__(kBlock) void step_kernel(StepArgs a) {
     __syncthreads();
     if (threadIdx.x == 0) {
         Partial p;
-        p.w = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
-        p.g = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
-        p.d = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
-        p.s = (red[3][0] + red[3][1]) + (red[3][2] + red[3][3]);
+        p.w = tree_sum<kTileBlock / 64>(red[0]);
+        p.g = tree_sum<kTileBlock / 64>(red[1]);
+        p.d = tree_sum<kTileBlock / 64>(red[2]);
+        p.s = tree_sum<kTileBlock / 64>(red[3]);
         a.partials[ti] = p;
-        if (EW && refresh) a.ew_partials[ti] = (red[4][0] + red[4][1]) + (red[4][2] + red[4][3]);
+        if (EW && refresh) a.ew_partials[ti] = tree_sum<kTileBlock / 64>(red[4]);
     }
 }
 
@@ -1000,7 +1008,7 @@ __device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __r
 }
 
 template <typename GT, int KT>
-__global__ __launch_bounds__(kBlock) void correct_kernel(UpdateArgs a) {
+__global__ __launch_bounds__(kTileBlock) void correct_kernel(UpdateArgs a) {
     if (*a.corr_flag == 0) return;
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
@@ -1059,7 +1067,7 @@ __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __re
 }
 
 template <typename GT, int KT, bool RECOMP>
-__global__ __launch_bounds__(kBlock) void update_kernel(UpdateArgs a) {
+__global__ __launch_bounds__(kTileBlock) void update_kernel(UpdateArgs a) {
     const Tile t = a.tiles[blockIdx.x];
     const float2 ab = a.coef[t.layer];
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
@@ -1073,7 +1081,7 @@ __global__ __launch_bounds__(kBlock) void update_kernel(UpdateArgs a) {
 
 template <typename GT, int KT, int RMODE>
 void step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
-    const dim3 grid(n_tiles), block(kBlock);
+    const dim3 grid(n_tiles), block(kTileBlock);
     if (!update)
         hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, false, 0>), grid, block, 0, s, a);
     else if (a.ew == 2)
@@ -1095,7 +1103,7 @@ hipError_t step_k(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
 
 template <typename GT, int KT>
 hipError_t update_k(const UpdateArgs& a, hipStream_t s) {
-    const dim3 grid(a.n_tiles), block(kBlock);
+    const dim3 grid(a.n_tiles), block(kTileBlock);
     if (a.gbar)
         hipLaunchKernelGGL((update_kernel<GT, KT, false>), grid, block, 0, s, a);
     else
@@ -1106,7 +1114,7 @@ hipError_t update_k(const UpdateArgs& a, hipStream_t s) {
 template <typename GT, int KT>
 hipError_t correct_k(const UpdateArgs& a, hipStream_t s) {
     const int nb = a.n_tiles < kCorrectBlocks ? a.n_tiles : kCorrectBlocks;
-    hipLaunchKernelGGL((correct_kernel<GT, KT>), dim3(nb), dim3(kBlock), 0, s, a);
+    hipLaunchKernelGGL((correct_kernel<GT, KT>), dim3(nb), dim3(kTileBlock), 0, s, a);
     return hipGetLastError();
 }
 
