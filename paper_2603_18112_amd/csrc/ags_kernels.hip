@@ -4,10 +4,10 @@
 //                  spread and the tile's partial statistics, and (AGS / SGD
 //                  steps) the momentum-SGD update with the coefficients
 //                  predicted before the step.
-// finalize_kernel  one block per layer: the layer's statistics from its tile
-//                  partials in fp64; the last layer to finish runs the global
-//                  decision (Eq. (5), Algorithm 1), the coefficients and the
-//                  gradscale refresh.
+// finalize_kernel  one block per chunk of a layer's tiles: the layer's
+//                  statistics from its tile partials in fp64; the block that
+//                  finishes the last layer runs the global decision (Eq. (5),
+//                  Algorithm 1), the coefficients and the gradscale refresh.
 // correct_kernel   AGS steps whose sensitive bit was mispredicted: adds
 //                  (a_true - a_predicted) * gbar to m and -eta times it to w;
 //                  exits at once otherwise.
@@ -58,12 +58,6 @@ namespace {
 #ifndef AGS_BATCH_F32_EW
 #define AGS_BATCH_F32_EW 2
 #endif
-// From this many replicas on, w and m are loaded after the replica loop
-// rather than before it, so that they do not hold registers through it.
-#ifndef AGS_LATE_WM_K
-#define AGS_LATE_WM_K 1 << 30
-#endif
-
 
 // bf16 gradients: a lane's two halves are adjacent (8 consecutive elements,
 // one 16-byte load per replica); fp32 gradients: 256 elements apart (every
@@ -751,26 +745,19 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
                                            const float* __restrict__ gs_old,
                                            float* __restrict__ gs_new, float smax, float& sw,
                                            float& sg, float& sd, float& ss, float& sx) {
-    constexpr bool late_wm = KT >= AGS_LATE_WM_K;
     constexpr int HS = Map<GT>::HS;
     constexpr bool NT = EW == 2;
     float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
     double q[kVec];
-    if (!late_wm) {
-        load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
-        if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
-        // Keep the w (and m) loads in front of the replica loads: without
-        // the barrier the statistics-only variant issued them only after
-        // consuming every replica, a second round trip per block.
-        if (!UPD) __builtin_amdgcn_sched_barrier(0);
-    }
+    load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
+    if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
+    // Keep the w (and m) loads in front of the replica loads: without the
+    // barrier the statistics-only variant issued them only after consuming
+    // every replica, a second round trip per block.
+    if (!UPD) __builtin_amdgcn_sched_barrier(0);
     constexpr int kb = EW ? RawGroup<GT>::kBatchEw : RawGroup<GT>::kBatch;
     moments<GT, KT, RMODE, FULL, EW != 0, kb, !UPD>(g, a.stride, idx, n0, n1, K, a.small_replica,
                                                a.invK, gb, dv, gr, q);
-    if (late_wm) {
-        load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
-        if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
-    }
     float gsv[kVec];
     if (EW) {
         // Old scales: applied on scaled layers, carried over on the others.
