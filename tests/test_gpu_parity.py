@@ -382,6 +382,45 @@ def test_bitwise_determinism():
     assert np.array_equal(a[3][0], b[3][0]) and a[3][1:] == b[3][1:]
 
 
+def test_two_handles_on_two_streams_interleaved():
+    """Handles share no device state: two handles stepping in turn on two
+    streams, with no synchronisation between their steps, end bitwise where
+    each ends alone on the default stream."""
+    import torch
+    cases = [(layouts.get_layout("tiny_cnn"), 4, "f32", {}),
+             (layouts.custom_layout(RAGGED, pad=8), 5, "bf16", {"elementwise": True})]
+    grads = [[to_device(synth.replica_grads(lay, K, t, 7, dtype=dt)) for t in range(4)]
+             for lay, K, dt, _ in cases]
+    torch.cuda.synchronize()
+
+    def run(interleaved):
+        hs = []
+        for lay, K, dt, extra in cases:
+            w = torch.from_numpy(synth.init_weights(lay, 7)).cuda()
+            hs.append(ags.AGS(lay.table(), w, torch.zeros_like(w), K, grad_dtype=dt, **extra))
+        torch.cuda.synchronize()
+        if interleaved:
+            streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+            for t in range(4):
+                for i, h in enumerate(hs):
+                    h.step(grads[i][t], streams[i])
+        else:
+            for i, h in enumerate(hs):
+                for t in range(4):
+                    h.step(grads[i][t])
+        torch.cuda.synchronize()
+        out = [(h.w.cpu().numpy(), h.m.cpu().numpy(), h.read_stats().layer, h.get_state()) for h in hs]
+        for h in hs:
+            h.close()
+        return out
+
+    for a, b in zip(run(False), run(True)):
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+        for f in ags.LAYER_STATS_FIELDS:
+            assert np.array_equal(a[2][f], b[2][f]), f
+        assert np.array_equal(a[3][0], b[3][0]) and a[3][1:] == b[3][1:]
+
+
 def test_checkpoint_resume_bitwise():
     import torch
     lay = layouts.get_layout("resnet18_cifar")
