@@ -233,9 +233,12 @@ ags_status ags_set_layer_state(ags_handle *h, const double *g_sq_prev_L);
 ags_status ags_get_elementwise_scale(ags_handle *h, float *scale, int64_t n);
 ags_status ags_set_elementwise_scale(ags_handle *h, const float *scale, int64_t n);
 
-/* Per-kernel timing with HIP events on the launch stream: enable, then
- * read the summed milliseconds per kernel (out_ms [AGS_N_KERNELS]) and the
- * number of steps measured since the last read; reading resets. */
+/* Per-kernel timing: with profiling enabled, each kernel of a step is
+ * launched with a start and a stop HIP event of its own dispatch on the
+ * launch stream (the kernel's execution alone); read the summed
+ * milliseconds per kernel (out_ms [AGS_N_KERNELS]: step kernel, finalize,
+ * second pass, which is 0 for SGD) and the number of steps measured since
+ * the last read; reading resets. */
 ags_status ags_set_profiling(ags_handle *h, int enable);
 ags_status ags_get_kernel_times(ags_handle *h, double *out_ms, int64_t *out_calls);
 

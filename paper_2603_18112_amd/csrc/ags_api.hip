@@ -295,7 +295,8 @@ struct ags_handle {
     bool has_stats = false;
     std::string err;
     bool profiling = false;
-    std::vector<std::array<hipEvent_t, AGS_N_KERNELS + 1>> ev_pending, ev_free;
+    // Per timed step: start and stop event of each kernel's dispatch.
+    std::vector<std::array<hipEvent_t, 2 * AGS_N_KERNELS>> ev_pending, ev_free;
 
     Tile* tiles() const { return reinterpret_cast<Tile*>(ws + wl.tiles); }
     Partial* partials() const { return reinterpret_cast<Partial*>(ws + wl.partials); }
@@ -366,7 +367,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         (void)hipGetLastError();
         return h->fail(AGS_E_DEVICE, "the current HIP device is not the handle's device");
     }
-    constexpr int NE = AGS_N_KERNELS + 1;
+    constexpr int NE = 2 * AGS_N_KERNELS;
     std::array<hipEvent_t, NE> ev{};
     const bool prof = commit && h->profiling;
     if (prof) {
@@ -382,8 +383,15 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
                 }
             }
         }
-        (void)hipEventRecord(ev[0], s);
     }
+    auto kev = [&](int k) {
+        return prof ? ags::KernelEvents{ev[2 * k], ev[2 * k + 1]} : ags::KernelEvents{};
+    };
+    // A failed launch hands the step's events back to the pool.
+    auto launch_fail = [&](hipError_t err, const char* what) {
+        if (prof) h->ev_free.push_back(ev);
+        return h->hip_fail(err, what);
+    };
     const ags_config& c = h->cfg;
     const float invK = (float)(1.0 / (double)c.K);
     // AGS and SGD steps update w and m in the statistics pass with the
@@ -438,12 +446,10 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.ew_buf = h->ew_buf(0);
     sa.n_flat = c.n_flat;
     sa.ew_partials = h->ew_partials();
-    hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s);
-    if (e != hipSuccess) return h->hip_fail(e, "step kernel launch");
-    if (prof) (void)hipEventRecord(ev[1], s);
-    e = ags::launch_finalize(sa, (int)h->n_chunks, s);
-    if (e != hipSuccess) return h->hip_fail(e, "finalize kernel launch");
-    if (prof) (void)hipEventRecord(ev[2], s);
+    hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s, kev(0));
+    if (e != hipSuccess) return launch_fail(e, "step kernel launch");
+    e = ags::launch_finalize(sa, (int)h->n_chunks, s, kev(1));
+    if (e != hipSuccess) return launch_fail(e, "finalize kernel launch");
 
     if (commit && c.mode != AGS_MODE_SGD) {
         ags::UpdateArgs ua{};
@@ -465,14 +471,15 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         ua.corr_flag = h->corr_flag();
         ua.lr = (float)h->lr;
         ua.momentum = (float)c.momentum;
-        e = (c.mode == AGS_MODE_LARS) ? ags::launch_update(ua, c.grad_dtype, s)
-                                      : ags::launch_correct(ua, c.grad_dtype, s);
-        if (e != hipSuccess) return h->hip_fail(e, "second-pass kernel launch");
+        e = (c.mode == AGS_MODE_LARS) ? ags::launch_update(ua, c.grad_dtype, s, kev(2))
+                                      : ags::launch_correct(ua, c.grad_dtype, s, kev(2));
+        if (e != hipSuccess) return launch_fail(e, "second-pass kernel launch");
+    } else if (prof) {
+        // No second pass (SGD): a zero-length interval.
+        (void)hipEventRecord(ev[4], s);
+        (void)hipEventRecord(ev[5], s);
     }
-    if (prof) {
-        (void)hipEventRecord(ev[3], s);
-        h->ev_pending.push_back(ev);
-    }
+    if (prof) h->ev_pending.push_back(ev);
     h->last_stream = s;
     h->has_stats = true;
     return AGS_OK;
@@ -852,11 +859,11 @@ ags_status ags_get_kernel_times(ags_handle* h, double* out_ms, int64_t* out_call
     if (!out_ms || !out_calls) return h->fail(AGS_E_ARG, "NULL output pointer");
     double tot[AGS_N_KERNELS] = {0, 0, 0};
     for (auto& q : h->ev_pending) {
-        hipError_t e = hipEventSynchronize(q[AGS_N_KERNELS]);
+        hipError_t e = hipEventSynchronize(q[2 * AGS_N_KERNELS - 1]);
         if (e != hipSuccess) return h->hip_fail(e, "hipEventSynchronize");
         for (int k = 0; k < AGS_N_KERNELS; ++k) {
             float ms = 0;
-            e = hipEventElapsedTime(&ms, q[k], q[k + 1]);
+            e = hipEventElapsedTime(&ms, q[2 * k], q[2 * k + 1]);
             if (e != hipSuccess) return h->hip_fail(e, "hipEventElapsedTime");
             tot[k] += ms;
         }

@@ -177,11 +177,20 @@ struct UpdateArgs {
 // Text for ags_last_error(NULL) on this thread (ags_api.hip).
 void set_thread_error(const char* why);
 
+// Events a launch records at its kernel's start and end (both null: none).
+// They belong to the kernel's own dispatch, so their elapsed time is the
+// kernel's execution alone, without the marker packets and cache
+// write-backs of a separate hipEventRecord between kernels.
+struct KernelEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+
 // Launchers (ags_kernels.hip).  They only enqueue; the return value is the
 // launch status.  update != 0 makes the step kernel apply the update.
-hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s);
-hipError_t launch_finalize(const StepArgs& a, int n_chunks, hipStream_t s);
-hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s);
-hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s);
+hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s,
+                       KernelEvents ev);
+hipError_t launch_finalize(const StepArgs& a, int n_chunks, hipStream_t s, KernelEvents ev);
+hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s, KernelEvents ev);
+hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s, KernelEvents ev);
 
 }  // namespace ags

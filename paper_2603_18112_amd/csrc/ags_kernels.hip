@@ -1066,43 +1066,47 @@ __global__ __launch_bounds__(kTileBlock) void update_kernel(UpdateArgs a) {
 
 // ----------------------------------------------------------- dispatch ---
 
+// One launch of a kernel whose single argument is a, with the dispatch's
+// own start and stop events when timing is on.
+template <typename A>
+hipError_t launch(void (*k)(A), dim3 grid, dim3 block, hipStream_t s, const A& a, KernelEvents ev) {
+    if (!ev.start && !ev.stop) {
+        hipLaunchKernelGGL(k, grid, block, 0, s, a);
+        return hipGetLastError();
+    }
+    void* args[] = {const_cast<A*>(&a)};
+    return hipExtLaunchKernel(reinterpret_cast<const void*>(k), grid, block, args, 0, s, ev.start,
+                              ev.stop, 0);
+}
+
 template <typename GT, int KT, int RMODE>
-void step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
+hipError_t step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s, KernelEvents ev) {
     const dim3 grid(n_tiles), block(kTileBlock);
-    if (!update)
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, false, 0>), grid, block, 0, s, a);
-    else if (a.ew == 2)
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 2>), grid, block, 0, s, a);
-    else if (a.ew)
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 1>), grid, block, 0, s, a);
-    else
-        hipLaunchKernelGGL((step_kernel<GT, KT, RMODE, true, 0>), grid, block, 0, s, a);
+    if (!update) return launch(step_kernel<GT, KT, RMODE, false, 0>, grid, block, s, a, ev);
+    if (a.ew == 2) return launch(step_kernel<GT, KT, RMODE, true, 2>, grid, block, s, a, ev);
+    if (a.ew) return launch(step_kernel<GT, KT, RMODE, true, 1>, grid, block, s, a, ev);
+    return launch(step_kernel<GT, KT, RMODE, true, 0>, grid, block, s, a, ev);
 }
 
 template <typename GT, int KT>
-hipError_t step_k(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
+hipError_t step_k(const StepArgs& a, int n_tiles, bool update, hipStream_t s, KernelEvents ev) {
     const int rm = a.small_replica == 0 ? 0 : (a.small_replica < 0 ? 1 : 2);
-    if (rm == 0) step_r<GT, KT, 0>(a, n_tiles, update, s);
-    else if (rm == 1) step_r<GT, KT, 1>(a, n_tiles, update, s);
-    else step_r<GT, KT, 2>(a, n_tiles, update, s);
-    return hipGetLastError();
+    if (rm == 0) return step_r<GT, KT, 0>(a, n_tiles, update, s, ev);
+    if (rm == 1) return step_r<GT, KT, 1>(a, n_tiles, update, s, ev);
+    return step_r<GT, KT, 2>(a, n_tiles, update, s, ev);
 }
 
 template <typename GT, int KT>
-hipError_t update_k(const UpdateArgs& a, hipStream_t s) {
+hipError_t update_k(const UpdateArgs& a, hipStream_t s, KernelEvents ev) {
     const dim3 grid(a.n_tiles), block(kTileBlock);
-    if (a.gbar)
-        hipLaunchKernelGGL((update_kernel<GT, KT, false>), grid, block, 0, s, a);
-    else
-        hipLaunchKernelGGL((update_kernel<GT, KT, true>), grid, block, 0, s, a);
-    return hipGetLastError();
+    if (a.gbar) return launch(update_kernel<GT, KT, false>, grid, block, s, a, ev);
+    return launch(update_kernel<GT, KT, true>, grid, block, s, a, ev);
 }
 
 template <typename GT, int KT>
-hipError_t correct_k(const UpdateArgs& a, hipStream_t s) {
+hipError_t correct_k(const UpdateArgs& a, hipStream_t s, KernelEvents ev) {
     const int nb = a.n_tiles < kCorrectBlocks ? a.n_tiles : kCorrectBlocks;
-    hipLaunchKernelGGL((correct_kernel<GT, KT>), dim3(nb), dim3(kTileBlock), 0, s, a);
-    return hipGetLastError();
+    return launch(correct_kernel<GT, KT>, dim3(nb), dim3(kTileBlock), s, a, ev);
 }
 
 #define AGS_K_DISPATCH(FN, GT, K, ...)           \
@@ -1118,36 +1122,36 @@ hipError_t correct_k(const UpdateArgs& a, hipStream_t s) {
     }
 
 template <typename GT>
-hipError_t step_t(const StepArgs& a, int n_tiles, bool update, hipStream_t s) {
-    AGS_K_DISPATCH(step_k, GT, a.K, a, n_tiles, update, s)
+hipError_t step_t(const StepArgs& a, int n_tiles, bool update, hipStream_t s, KernelEvents ev) {
+    AGS_K_DISPATCH(step_k, GT, a.K, a, n_tiles, update, s, ev)
 }
 template <typename GT>
-hipError_t update_t(const UpdateArgs& a, hipStream_t s) {
-    AGS_K_DISPATCH(update_k, GT, a.K, a, s)
+hipError_t update_t(const UpdateArgs& a, hipStream_t s, KernelEvents ev) {
+    AGS_K_DISPATCH(update_k, GT, a.K, a, s, ev)
 }
 template <typename GT>
-hipError_t correct_t(const UpdateArgs& a, hipStream_t s) {
-    AGS_K_DISPATCH(correct_k, GT, a.K, a, s)
+hipError_t correct_t(const UpdateArgs& a, hipStream_t s, KernelEvents ev) {
+    AGS_K_DISPATCH(correct_k, GT, a.K, a, s, ev)
 }
 
 }  // namespace
 
-hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s) {
-    return dt == AGS_BF16 ? step_t<uint16_t>(a, n_tiles, update, s)
-                          : step_t<float>(a, n_tiles, update, s);
+hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update, hipStream_t s,
+                       KernelEvents ev) {
+    return dt == AGS_BF16 ? step_t<uint16_t>(a, n_tiles, update, s, ev)
+                          : step_t<float>(a, n_tiles, update, s, ev);
 }
 
-hipError_t launch_finalize(const StepArgs& a, int n_chunks, hipStream_t s) {
-    hipLaunchKernelGGL(finalize_kernel, dim3(n_chunks), dim3(kBlock), 0, s, a);
-    return hipGetLastError();
+hipError_t launch_finalize(const StepArgs& a, int n_chunks, hipStream_t s, KernelEvents ev) {
+    return launch(finalize_kernel, dim3(n_chunks), dim3(kBlock), s, a, ev);
 }
 
-hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s) {
-    return dt == AGS_BF16 ? update_t<uint16_t>(a, s) : update_t<float>(a, s);
+hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s, KernelEvents ev) {
+    return dt == AGS_BF16 ? update_t<uint16_t>(a, s, ev) : update_t<float>(a, s, ev);
 }
 
-hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s) {
-    return dt == AGS_BF16 ? correct_t<uint16_t>(a, s) : correct_t<float>(a, s);
+hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s, KernelEvents ev) {
+    return dt == AGS_BF16 ? correct_t<uint16_t>(a, s, ev) : correct_t<float>(a, s, ev);
 }
 
 }  // namespace ags

@@ -5,16 +5,16 @@
 
 namespace ags {
 
-hipError_t launch_step(const StepArgs&, ags_dtype, int, bool, hipStream_t) {
+hipError_t launch_step(const StepArgs&, ags_dtype, int, bool, hipStream_t, KernelEvents) {
     return hipErrorInvalidDeviceFunction;
 }
-hipError_t launch_finalize(const StepArgs&, int, hipStream_t) {
+hipError_t launch_finalize(const StepArgs&, int, hipStream_t, KernelEvents) {
     return hipErrorInvalidDeviceFunction;
 }
-hipError_t launch_update(const UpdateArgs&, ags_dtype, hipStream_t) {
+hipError_t launch_update(const UpdateArgs&, ags_dtype, hipStream_t, KernelEvents) {
     return hipErrorInvalidDeviceFunction;
 }
-hipError_t launch_correct(const UpdateArgs&, ags_dtype, hipStream_t) {
+hipError_t launch_correct(const UpdateArgs&, ags_dtype, hipStream_t, KernelEvents) {
     return hipErrorInvalidDeviceFunction;
 }
 
