@@ -474,10 +474,6 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         e = (c.mode == AGS_MODE_LARS) ? ags::launch_update(ua, c.grad_dtype, s, kev(2))
                                       : ags::launch_correct(ua, c.grad_dtype, s, kev(2));
         if (e != hipSuccess) return launch_fail(e, "second-pass kernel launch");
-    } else if (prof) {
-        // No second pass (SGD): a zero-length interval.
-        (void)hipEventRecord(ev[4], s);
-        (void)hipEventRecord(ev[5], s);
     }
     if (prof) h->ev_pending.push_back(ev);
     h->last_stream = s;
@@ -859,9 +855,11 @@ ags_status ags_get_kernel_times(ags_handle* h, double* out_ms, int64_t* out_call
     if (!out_ms || !out_calls) return h->fail(AGS_E_ARG, "NULL output pointer");
     double tot[AGS_N_KERNELS] = {0, 0, 0};
     for (auto& q : h->ev_pending) {
-        hipError_t e = hipEventSynchronize(q[2 * AGS_N_KERNELS - 1]);
+        // An SGD step launches no second pass (its time stays 0).
+        const int nk = h->cfg.mode == AGS_MODE_SGD ? AGS_N_KERNELS - 1 : AGS_N_KERNELS;
+        hipError_t e = hipEventSynchronize(q[2 * nk - 1]);
         if (e != hipSuccess) return h->hip_fail(e, "hipEventSynchronize");
-        for (int k = 0; k < AGS_N_KERNELS; ++k) {
+        for (int k = 0; k < nk; ++k) {
             float ms = 0;
             e = hipEventElapsedTime(&ms, q[2 * k], q[2 * k + 1]);
             if (e != hipSuccess) return h->hip_fail(e, "hipEventElapsedTime");

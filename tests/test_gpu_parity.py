@@ -459,6 +459,15 @@ def test_set_lr_and_profiling():
     ms, n = p.gpu.kernel_times()
     assert n == 3 and np.all(ms > 0)
     p.close()
+    # SGD launches no second pass: its interval is empty.
+    q = Pair(lay, 4, mode="sgd")
+    q.gpu.set_profiling(True)
+    for t in range(2):
+        g = synth.replica_grads(lay, 4, t, 0)
+        q.step(g, what=f"sgd profiled step {t + 1}")
+    ms, n = q.gpu.kernel_times()
+    assert n == 2 and ms[0] > 0 and ms[1] > 0 and ms[2] == 0
+    q.close()
 
 
 def _hip():
