@@ -238,7 +238,8 @@ ags_status ags_set_elementwise_scale(ags_handle *h, const float *scale, int64_t 
  * launch stream (the kernel's execution alone); read the summed
  * milliseconds per kernel (out_ms [AGS_N_KERNELS]: step kernel, finalize,
  * second pass, which is 0 for SGD) and the number of steps measured since
- * the last read; reading resets. */
+ * the last read; reading resets.  Steps enqueued during stream capture are
+ * not timed. */
 ags_status ags_set_profiling(ags_handle *h, int enable);
 ags_status ags_get_kernel_times(ags_handle *h, double *out_ms, int64_t *out_calls);
 

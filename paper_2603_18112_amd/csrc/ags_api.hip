@@ -369,7 +369,15 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     }
     constexpr int NE = 2 * AGS_N_KERNELS;
     std::array<hipEvent_t, NE> ev{};
-    const bool prof = commit && h->profiling;
+    // Steps enqueued while the stream is being captured into a graph are not
+    // timed: a graph replays them without the handle's bookkeeping.
+    bool capturing = false;
+    if (commit && h->profiling) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(s, &cs) != hipSuccess) (void)hipGetLastError();
+        capturing = cs != hipStreamCaptureStatusNone;
+    }
+    const bool prof = commit && h->profiling && !capturing;
     if (prof) {
         if (!h->ev_free.empty()) {
             ev = h->ev_free.back();

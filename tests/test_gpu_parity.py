@@ -550,9 +550,12 @@ def test_hip_graph_capture_replays_match_eager(lay_name, K, dtype, hyper):
     s = torch.cuda.Stream()
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
+    graphed.set_profiling(True)     # a captured step is not timed
     with torch.cuda.graph(graph, stream=s):
         graphed.step(gbuf)
     torch.cuda.synchronize()
+    assert graphed.kernel_times()[1] == 0
+    graphed.set_profiling(False)
     # capturing does not run the step
     assert torch.equal(wg, w0) and graphed.get_state()[2] == 0
     for t, g in enumerate(grads):
