@@ -39,11 +39,15 @@ MUTANTS = [
      "double g = grad_at(c, grads, 0, o + j);"),
     ("RMS small batch not averaged", "            S /= K;\n", "\n"),
     ("noise ratio transposed", "if (G > 0.0) rho = V / G;", "if (V > 0.0) rho = G / V;"),
+    ("noise ratio 0/0 infinite", "else rho = (V > 0.0) ? INFINITY : 0.0;", "else rho = INFINITY;"),
+    ("noise ratio V/0 zero", "else rho = (V > 0.0) ? INFINITY : 0.0;", "else rho = 0.0;"),
     # step 3: gradient variability (Eq. (5)) and the branch
     ("global norm over scaled layers only", "for (int l = 0; l < L; ++l) G += G_l[l];",
      "for (int l = 0; l < L; ++l) if (layers[l].flags & ORACLE_SCALE) G += G_l[l];"),
     ("Delta divided by the new norm", "delta = fabs((G - Gp) / Gp);", "delta = fabs((G - Gp) / G);"),
     ("Delta without the absolute value", "delta = fabs((G - Gp) / Gp);", "delta = (G - Gp) / Gp;"),
+    ("global Delta finite at step 1", "if (t == 1 || !(Gp > 0.0) || !isfinite(Gp) || !isfinite(G))",
+     "if (!(Gp > 0.0) || !isfinite(Gp) || !isfinite(G))"),
     ("tie counted as not sensitive", "const int sensitive = !(delta < c->delta);",
      "const int sensitive = !(delta <= c->delta);"),
     ("branch inverted", "const int sensitive = !(delta < c->delta);",
@@ -54,6 +58,12 @@ MUTANTS = [
     ("layer and global scope swapped", "out[OUT_SENS] = c->delta_scope ? !(dl < c->delta) : sensitive;",
      "out[OUT_SENS] = c->delta_scope ? sensitive : !(dl < c->delta);"),
     ("layer G_prev never updated", "for (int l = 0; l < L; ++l) g_prev_layers[l] = G_l[l];", ";"),
+    # step 3b: per-layer variability
+    ("layer Delta finite at step 1", "if (t == 1 || !(Gpl > 0.0) || !isfinite(Gpl) || !isfinite(G_l[l]))",
+     "if (!(Gpl > 0.0) || !isfinite(Gpl) || !isfinite(G_l[l]))"),
+    ("layer Delta of a non-finite norm not infinite",
+     "if (t == 1 || !(Gpl > 0.0) || !isfinite(Gpl) || !isfinite(G_l[l]))",
+     "if (t == 1 || !(Gpl > 0.0) || !isfinite(Gpl))"),
     # step 4: coefficients
     ("AGS scale inverted", "a = (scaled && !out[OUT_SENS]) ? gradscale[l] : 1.0;",
      "a = (scaled && !out[OUT_SENS]) ? 1.0 / gradscale[l] : 1.0;"),
@@ -63,11 +73,20 @@ MUTANTS = [
      "a = (!out[OUT_SENS]) ? gradscale[l] : 1.0;"),
     ("AGS drops weight decay", "            a = (scaled && !out[OUT_SENS]) ? gradscale[l] : 1.0;\n            b = lam;",
      "            a = (scaled && !out[OUT_SENS]) ? gradscale[l] : 1.0;\n            b = 0.0;"),
+    ("static scale on sensitive steps", "a = (scaled && !out[OUT_SENS]) ? c->static_scale : 1.0;",
+     "a = scaled ? c->static_scale : 1.0;"),
+    ("static decay scaled",
+     "            a = (scaled && !out[OUT_SENS]) ? c->static_scale : 1.0;\n            b = lam;",
+     "            a = (scaled && !out[OUT_SENS]) ? c->static_scale : 1.0;\n            b = a * lam;"),
     ("static scale inverted", "a = (scaled && !out[OUT_SENS]) ? c->static_scale : 1.0;",
      "a = (scaled && !out[OUT_SENS]) ? 1.0 / c->static_scale : 1.0;"),
     ("LARS without the decay term", "c->trust_coef * wn / (gn + lam * wn)", "c->trust_coef * wn / gn"),
     ("LARS ratio transposed", "c->trust_coef * wn / (gn + lam * wn)", "c->trust_coef * gn / (wn + lam * gn)"),
     ("LARS decay not scaled", "            b = a * lam;", "            b = lam;"),
+    ("LARS zero-norm fallback 0", "? c->trust_coef * wn / (gn + lam * wn) : 1.0;",
+     "? c->trust_coef * wn / (gn + lam * wn) : 0.0;"),
+    ("LARS scales unscaled layers", "            if (scaled) {\n                const double wn",
+     "            if (1) {\n                const double wn"),
     ("SGD without decay", "double a = 1.0, b = lam;", "double a = 1.0, b = 0.0;"),
     # step 5: wrapped momentum SGD (Eq. (7b), PyTorch semantics)
     ("momentum with dampening", "m[o + j] = c->momentum * m[o + j] + d;",

@@ -441,6 +441,32 @@ def test_zero_mean_with_noise_gives_infinite_ratio():
     assert st["g_sq"][0] == 0.0 and st["var"][0] == 4.0 and st["noise_ratio"][0] == math.inf
 
 
+def test_lars_leaves_unscaled_layers_at_one():
+    # Only layers flagged for scaling take the trust ratio; the others keep
+    # a = 1 and b = lambda_l, i.e. plain momentum SGD (against torch).
+    lam, lr, mu = 5e-4, 0.1, 0.9
+    flags = [SD, layouts.LAYER_DECAY, 0]
+    lay, table = _layers([24, 16, 8], flags)
+    rng = np.random.default_rng(21)
+    w0 = _coarse(rng.standard_normal(lay.n_flat)).astype(np.float64)
+    grads = [_coarse(rng.standard_normal((3, lay.n_flat))) for _ in range(2)]
+    o = OracleAGS(table, lay.n_flat, 3, w0, mode="lars", lr=lr, momentum=mu, weight_decay=lam,
+                  trust_coef=1e-3)
+    for g in grads:
+        st, _ = o.step(g)
+        assert st["coef_a"][0] != 1.0
+        assert list(st["coef_a"][1:]) == [1.0, 1.0] and list(st["coef_b"][1:]) == [lam, 0.0]
+    for l in (1, 2):
+        off, n, _ = table[l]
+        p = torch.nn.Parameter(torch.tensor(w0[off:off + n]))
+        opt = torch.optim.SGD([p], lr=lr, momentum=mu,
+                              weight_decay=lam if flags[l] & layouts.LAYER_DECAY else 0.0)
+        for g in grads:
+            p.grad = torch.tensor(g[:, off:off + n].astype(np.float64).mean(axis=0))
+            opt.step()
+        np.testing.assert_allclose(o.w[off:off + n], p.detach().numpy(), rtol=1e-13, atol=1e-15)
+
+
 def test_lars_zero_weight_trust_is_one():
     lay, table = _layers([16])
     g = np.ones((2, lay.n_flat), np.float32)
@@ -455,8 +481,12 @@ def test_nonfinite_gradient_is_flagged_and_sensitive():
     o.step(g)
     g2 = g.copy()
     g2[1, 3] = np.nan
-    _, gl = o.step(g2)
+    st, gl = o.step(g2)
     assert gl["nonfinite"] == 1 and gl["sensitive"] == 1
+    # Delta of a non-finite norm is +inf, never NaN: globally and for the
+    # layer holding the NaN (the other layer's norm did not change)
+    assert math.isinf(gl["delta"]) and gl["delta"] > 0
+    assert math.isinf(st["delta"][0]) and st["delta"][0] > 0 and st["delta"][1] == 0.0
 
 
 def test_nonfinite_weight_is_flagged():
@@ -950,6 +980,7 @@ def test_layer_delta_first_step_and_zero_norm_records():
     o.set_layer_state([1.0, 1.0])
     st, gl = o.step(g)
     assert np.all(np.isinf(st["delta"])) and list(st["sensitive"]) == [1, 1]
+    assert math.isinf(gl["delta"]) and gl["sensitive"] == 1
     st, gl = o.step(g)
     assert st["delta"][0] == 0.0 and math.isinf(st["delta"][1]) and st["delta"][1] > 0
     assert list(st["sensitive"]) == [0, 1]
