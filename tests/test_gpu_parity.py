@@ -218,6 +218,22 @@ def test_single_element_layers_and_lars():
     run_steps(lay, 4, 3, mode="lars", label="1-elem lars")
 
 
+@pytest.mark.parametrize("K,dtype", [(8, "f32"), (4, "bf16")])
+def test_lars_with_unscaled_layers(K, dtype):
+    # Mixed flags: unscaled layers keep a = 1 (plain momentum SGD).  K e_g of
+    # 32 bytes keeps the replica mean between the passes, 8 bytes re-reads
+    # the replicas in the update pass.
+    flags = [SD, layouts.LAYER_DECAY, 0, layouts.LAYER_SCALE] * 4
+    lay = layouts.custom_layout(RAGGED, flags[:len(RAGGED)], pad=8)
+    run_steps(lay, K, 3, dtype=dtype, mode="lars", label=f"lars mixed flags K={K} {dtype}")
+
+
+def test_resnet18_cifar_lars_two_steps():
+    # 1-D tensors (BN, biases) neither scaled nor decayed.
+    lay = layouts.get_layout("resnet18_cifar")
+    run_steps(lay, 8, 2, mode="lars", check_each=False, label="r18 lars")
+
+
 def test_identical_replicas_zero_variance_exactly():
     lay = layouts.get_layout("tiny_cnn")
     x = synth.replica_grads(lay, 1, 0, 0)
