@@ -599,7 +599,8 @@ def test_matches_golden_oracle_fixture():
     import os
     import torch
     from ags_parity import PARAM_RTOL, STAT_RTOL
-    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "tiny_cnn_ags_k4.json")))
+    with open(os.path.join(os.path.dirname(__file__), "golden", "tiny_cnn_ags_k4.json")) as f:
+        gold = json.load(f)
     lay = layouts.get_layout(gold["layout"])
     w = torch.from_numpy(synth.init_weights(lay, gold["seed"])).cuda()
     m = torch.zeros_like(w)

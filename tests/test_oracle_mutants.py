@@ -111,12 +111,32 @@ MUTANTS = [
     ("element ratio transposed", "double s = fabs(gs / (gbar_keep[l][j] + c->eps));",
      "double s = fabs(gbar_keep[l][j] / (gs + c->eps));"),
     ("element RMS without the root", "gs = sqrt(q / K);", "gs = q / K;"),
+    ("element RMS over K - 1", "gs = sqrt(q / K);", "gs = sqrt(q / (K > 1 ? K - 1 : 1));"),
+    ("element small batch always replica 0", "gs = grad_at(c, grads, c->small_replica, o + j);",
+     "gs = grad_at(c, grads, 0, o + j);"),
+    ("element eps outside the ratio", "double s = fabs(gs / (gbar_keep[l][j] + c->eps));",
+     "double s = fabs(gs / gbar_keep[l][j]) + c->eps;"),
+    ("element mean coefficient ignores the decision",
+     "sum += (scaled && !sens_l) ? gradscale[o + j] : 1.0;", "sum += scaled ? gradscale[o + j] : 1.0;"),
+    ("element scale mean not divided", "            out[OUT_GRADSCALE] = sum / (double)n;\n            continue;",
+     "            out[OUT_GRADSCALE] = sum;\n            continue;"),
     ("element 0/0 gives 0", "if (isnan(s)) s = 1.0;", "if (isnan(s)) s = 0.0;"),
     ("element scale ignores the layer flag",
      "const double a = ew ? ((scaled && !sens_l) ? gradscale[o + j] : 1.0) : a_l[l];",
      "const double a = ew ? (!sens_l ? gradscale[o + j] : 1.0) : a_l[l];"),
     ("element scales not clipped", "                    if (s > smax) s = smax;\n", "\n"),
     # bookkeeping
+    ("refresh in stats-only calls", "const int refresh = commit && c->mode == ORACLE_AGS && c->refresh_every > 0 &&",
+     "const int refresh = c->mode == ORACLE_AGS && c->refresh_every > 0 &&"),
+    ("refresh in static and LARS modes",
+     "const int refresh = commit && c->mode == ORACLE_AGS && c->refresh_every > 0 &&",
+     "const int refresh = commit && c->mode != ORACLE_SGD && c->refresh_every > 0 &&"),
+    ("G_prev reported on a first step", "out_global[GOUT_GPREV] = (t == 1) ? 0.0 : Gp;",
+     "out_global[GOUT_GPREV] = Gp;"),
+    ("state advanced by stats-only calls", "    if (commit) {\n        *g_prev = G;",
+     "    if (1) {\n        *g_prev = G;"),
+    ("s_max override ignored", "const double smax = (c->s_max > 0.0) ? c->s_max : sqrt((double)K);",
+     "const double smax = sqrt((double)K);"),
     ("non-finite statistics not flagged",
      "if (!isfinite(W) || !isfinite(G) || !isfinite(V) || !isfinite(S)) nonfinite = 1;", ";"),
 ]

@@ -659,7 +659,8 @@ def test_oracle_reproduces_golden_fixture():
     import json
     import os
     path = os.path.join(os.path.dirname(__file__), "golden", "tiny_cnn_ags_k4.json")
-    gold = json.load(open(path))
+    with open(path) as f:
+        gold = json.load(f)
     lay = layouts.get_layout(gold["layout"])
     o = OracleAGS(lay.table(), lay.n_flat, gold["K"], synth.init_weights(lay, gold["seed"]),
                   **gold["hyper"])
@@ -826,6 +827,20 @@ def test_elementwise_rms_small_batch_and_zero_rules():
         assert np.all(o.gradscale[2:] == zero_scale)
 
 
+def test_elementwise_small_batch_from_replica_r():
+    # r = 2: g_small,j is replica 2's element; the scale of element j is
+    # |g_2j / (mean_k g_kj + eps)| clipped at s_max (eps = 0, exact values).
+    g = np.array([[1.0, 2.0, 4.0, -1.0], [3.0, 2.0, 0.0, 1.0], [2.0, -4.0, 2.0, 3.0]],
+                 np.float32)
+    o = OracleAGS([(0, 4, SD)], 4, 3, np.ones(4), eps=0.0, s_max=10.0, small_replica=2,
+                  elementwise=True)
+    o.step(g)
+    gbar = g.astype(np.float64).mean(axis=0)          # [2, 0, 2, 1]
+    expect = np.minimum(np.abs(g[2] / gbar), 10.0)     # x/0 -> +inf -> s_max
+    assert list(expect) == [1.0, 10.0, 1.0, 3.0]
+    assert list(o.gradscale) == list(expect)
+
+
 # --------------------------------------------------------------------------
 # per-layer variability: Delta_l = |G_l - G_l,prev| / G_l,prev decides layer l
 
@@ -981,6 +996,7 @@ def test_layer_delta_first_step_and_zero_norm_records():
     st, gl = o.step(g)
     assert np.all(np.isinf(st["delta"])) and list(st["sensitive"]) == [1, 1]
     assert math.isinf(gl["delta"]) and gl["sensitive"] == 1
+    assert gl["g_sq_prev"] == 0.0       # a first step has no previous norm to report
     st, gl = o.step(g)
     assert st["delta"][0] == 0.0 and math.isinf(st["delta"][1]) and st["delta"][1] > 0
     assert list(st["sensitive"]) == [0, 1]
