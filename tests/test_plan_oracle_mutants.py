@@ -51,10 +51,27 @@ MUTANTS = [
     ("threshold without the sensitivity", "step = sensitivity * (xs[-1] - xs[0]) / (n - 1)",
      "step = (xs[-1] - xs[0]) / (n - 1)"),
     ("knee at the point that falls below", "            return order[lmx]", "            return order[j]"),
+    ("local maximum strict on both sides", "if j < n - 1 and d[j - 1] < d[j] >= d[j + 1]:",
+     "if j < n - 1 and d[j - 1] < d[j] > d[j + 1]:"),
+    ("threshold reached counts as a fall", "if threshold is not None and d[j] < threshold:",
+     "if threshold is not None and d[j] <= threshold:"),
+    ("memory bound not clamped at 0", "return max(0, math.floor((capacity - m_static) / m_per_sample))",
+     "return math.floor((capacity - m_static) / m_per_sample)"),
+    ("rms residual without the root", "out[\"rms_residual\"] = float(math.sqrt(np.mean(r * r)))",
+     "out[\"rms_residual\"] = float(np.mean(r * r))"),
+    ("threshold above the maximum", "threshold = d[j] - step", "threshold = d[j] + step"),
     # selection
+    ("cost tie to the last candidate", "return min(idx, key=lambda i: (Cs[i], i)), Ts, Cs",
+     "return min(idx, key=lambda i: (Cs[i], -i)), Ts, Cs"),
+    ("infeasible candidates keep their time", "        Ts.append(T if ok else math.inf)", "        Ts.append(T)"),
     ("time objective ranks by cost", "return min(idx, key=lambda i: (Ts[i], i)), Ts, Cs",
      "return min(idx, key=lambda i: (Cs[i], i)), Ts, Cs"),
     ("feasibility on the global batch", "ok = B / n <= max_local", "ok = B <= max_local"),
+    # Not listed: a knee sought on a flat curve (the NaN difference curve has
+    # no local maximum either: None both ways); the knee's index into the
+    # feasible candidates used without mapping it back (with one cluster
+    # size and increasing B the infeasible ones form a suffix, so the two
+    # indices agree).
     # Not listed: the knee taken on the cost curve instead of the time curve.
     # The knee objective works on one cluster size, where C = T N p / 3600
     # is a constant multiple of T, so Kneedle (which normalises y) finds the

@@ -124,6 +124,27 @@ def test_knee_threshold_rule_and_sensitivity():
     assert po.knee(x, np.ones_like(x), "concave_inc") is None
 
 
+# Exact curves on x = k/8 whose y spans [0, 1], so the normalisation is the
+# identity and the difference curve d = y - x holds the chosen dyadic values.
+X8 = np.arange(9) / 8.0
+D_TIE = np.array([0, 0.25, 0.125, 0.25, 0, 0, 0, 0, 0])       # d meets the threshold
+D_PLATEAU = np.array([0, 0.25, 0.25, 0, 0, 0, 0, 0, 0])       # a flat maximum
+
+
+def test_knee_threshold_is_strict_and_plateaus_count_from_their_first_point():
+    # The maximum at 1 sets the threshold 0.25 - 1/8 = 0.125; d[2] equals
+    # it, which is not a fall below it, and the next maximum (3) is the knee.
+    assert po.knee(X8, X8 + D_TIE, "concave_inc") == 3
+    # A maximum held over two points is a local maximum at its first point.
+    assert po.knee(X8, X8 + D_PLATEAU, "concave_inc") == 1
+
+
+def test_memory_bound_is_zero_when_the_static_part_does_not_fit():
+    assert po.max_local_batch(16.0, 20.0, 1.0) == 0
+    assert po.max_local_batch(20.0, 20.0, 1.0) == 0
+    assert po.max_local_batch(20.5, 20.0, 0.25) == 2
+
+
 # ------------------------------------------------------------ selection --
 
 
@@ -141,6 +162,15 @@ def test_select_min_time_min_cost_and_memory_bound():
     assert i == 4 and math.isinf(T[0]) and math.isinf(T[1])   # b = 256, 128 > 100
     i, _, _ = po.select(m, cands, 1, 25600, 1.0, "ring", "time", max_local=1)
     assert i is None
+
+
+def test_select_cost_tie_takes_the_first_candidate():
+    # Constant step time: doubling N and B halves T and keeps C = T N p / 3600
+    # exactly (powers of two), so both candidates cost the same.
+    m = {"c0": 0.5, "c_compute": 0.0, "c_sync": 0.0}
+    for cands in ([(1, 128), (2, 256)], [(2, 256), (1, 128)]):
+        i, T, C = po.select(m, cands, 2, 1e5, 3.0, "none", "cost")
+        assert C[0] == C[1] and i == 0
 
 
 def test_select_knee_on_time_versus_batch():

@@ -92,7 +92,8 @@ def test_time_cost_and_step_time_match_oracle():
 
 
 def test_max_local_batch_matches_oracle():
-    for cap, st, per in ((288.0, 40.0, 0.75), (80.0, 79.9, 0.05), (16.0, 20.0, 1.0), (1e3, 0.0, 3.0)):
+    for cap, st, per in ((288.0, 40.0, 0.75), (80.0, 79.9, 0.05), (16.0, 20.0, 1.0), (1e3, 0.0, 3.0),
+                         (20.0, 20.0, 1.0), (20.5, 20.0, 0.25)):
         assert plan.ags_plan_max_local_batch(cap, st, per) == po.max_local_batch(cap, st, per)
     with pytest.raises(ags.AGSError):
         plan.ags_plan_max_local_batch(10.0, 1.0, 0.0)
@@ -117,6 +118,9 @@ def _curves():
         y = np.exp(-xs / rng.uniform(0.5, 3)) + rng.normal(0, 0.01, len(xs))
         yield xs, y, "convex_dec"
         yield xs, -y, "concave_inc"
+    x8 = np.arange(9) / 8.0                 # exact threshold tie and plateau
+    yield x8, x8 + np.array([0, 0.25, 0.125, 0.25, 0, 0, 0, 0, 0]), "concave_inc"
+    yield x8, x8 + np.array([0, 0.25, 0.25, 0, 0, 0, 0, 0, 0]), "concave_inc"
     yield x, 2 * x, "concave_inc"
     yield x, np.ones_like(x), "convex_dec"
     yield x[:2], x[:2], "concave_inc"
@@ -161,6 +165,15 @@ def test_select_matches_oracle(objective):
             assert (math.isinf(a) and math.isinf(b)) or _close(a, b, 1e-13)
         for a, b in zip(C, oC):
             assert (math.isinf(a) and math.isinf(b)) or _close(a, b, 1e-13)
+
+
+def test_select_cost_tie_takes_the_first_candidate():
+    # Constant step time: the two candidates cost exactly the same.
+    m = plan.ags_plan_fit([(1, 32.0, 0.5), (1, 64.0, 0.5)], "none", po.TERM_INTERCEPT)
+    for cands in ([(1, 128.0), (2, 256.0)], [(2, 256.0), (1, 128.0)]):
+        i, T, C = plan.ags_plan_select(m, cands, 2, 1e5, 3.0, math.inf, "cost")
+        oi, _, oC = po.select(m.as_dict(), cands, 2, 1e5, 3.0, "none", "cost")
+        assert C[0] == C[1] and oC[0] == oC[1] and i == oi == 0
 
 
 def test_select_argument_errors():
