@@ -187,6 +187,7 @@ def cpu_baseline(layout, w0, grads_np, budget_s=20.0, max_steps=30):
 
 
 PLAN_KS = (1, 2, 4, 8, 16, 32, 64)
+PLAN_NOISES = (0.1, 0.5, 2.0)
 
 
 def run_plan(args, torch, np):
@@ -196,7 +197,14 @@ def run_plan(args, torch, np):
     form of Eq. (2c): t(K) = c0 + c_sync K.  Full search fits every K,
     partial search the extremes (K = 1 and 64) only; both predict every K.
     The knee of the time per replica gradient, t(K) / K, over K is where
-    more replicas per step stop amortising the step's fixed costs."""
+    more replicas per step stop amortising the step's fixed costs.
+
+    The sweep also checks the statistics the step computes: for noise c in
+    {0.1, 0.5, 2.0} (per-replica noise std in units of the layer's sigma)
+    and every K, the per-layer noise ratio rho_l = V_l / G_l of an ags_stats
+    call against its expectation under the generator, c^2 (K - 1) / (K + c^2)
+    (median and largest relative deviation over the layers of at least 1000
+    elements)."""
     from paper_2603_18112_amd import ags, layouts, plan, synth
     lay = layouts.get_layout("resnet50")
     N = lay.n_params
@@ -211,6 +219,16 @@ def run_plan(args, torch, np):
     steps = max(20, min(args.steps, 200))
     hyper = dict(HYPER)
     measured = {}
+    noise_sets = {}
+    for c in PLAN_NOISES:
+        if c == 0.5:
+            noise_sets[c] = g_all                      # the timing set: synth's default c
+        else:
+            g_c = synth.replica_grads(lay, kmax, 0, 0, noise=c, dtype="bf16", stride=stride)
+            noise_sets[c] = torch.from_numpy(g_c.view(np.int16)).cuda()
+            del g_c
+    big = np.array([n >= 1000 for _, n, _ in lay.table()])
+    rho_rows = []
     for k in PLAN_KS:
         w = torch.from_numpy(w0.copy()).cuda()
         m = torch.zeros_like(w)
@@ -227,6 +245,19 @@ def run_plan(args, torch, np):
         e1.record(stream)
         torch.cuda.synchronize()
         measured[k] = e0.elapsed_time(e1) / steps * 1e-3
+        for c in PLAN_NOISES:
+            h.stats(noise_sets[c][:k], stream)
+            rho = np.asarray(h.read_stats().layer["noise_ratio"])[big]
+            expect = c * c * (k - 1) / (k + c * c)
+            if expect > 0:
+                dev = np.abs(rho / expect - 1.0)
+                rho_rows.append({"K": k, "c": c, "expected": round(expect, 6),
+                                 "median_rho": round(float(np.median(rho)), 6),
+                                 "max_rel_dev": round(float(dev.max()), 4)})
+            else:
+                rho_rows.append({"K": k, "c": c, "expected": 0.0,
+                                 "median_rho": round(float(np.median(rho)), 6),
+                                 "max_abs": float(np.abs(rho).max())})
         h.close()
         del w, m
         log(f"plan: K={k}: {measured[k] * 1e6:.1f} us/step")
@@ -267,6 +298,8 @@ def run_plan(args, torch, np):
                  "curve": "seconds per replica gradient t(K)/K over K (Kneedle, convex decreasing)",
                  "per_replica_us": [round(x * 1e6, 2) for x in per_rep]},
         "algorithmic_GBps": {str(k): round(bytes_per_step[k] / measured[k] / 1e9, 1) for k in PLAN_KS},
+        "noise_ratio": {"expected": "c^2 (K - 1) / (K + c^2)", "layers": int(big.sum()),
+                        "per_K_and_c": rho_rows},
         "fit_call_us": round(fit_us, 2),
     }
     print(json.dumps(out), flush=True)
