@@ -176,7 +176,8 @@ typedef struct ags_handle ags_handle;
 ags_status ags_workspace_bytes(const ags_config *cfg, size_t *out_bytes);
 
 /* Create a handle bound to d_w, d_m (fp32 [n_flat], caller-owned, must
- * outlive the handle) on the current HIP device.  The handle allocates its
+ * outlive the handle, must not overlap: AGS_E_ARG) on the current HIP
+ * device.  The handle allocates its
  * workspace (AGS_E_NOMEM on failure or when it exceeds the byte cap given
  * by the environment variable AGS_MAX_WORKSPACE_BYTES; nothing is leaked).
  * gradscale starts at 1 (Algorithm 1), the step count at 0. */
@@ -187,7 +188,8 @@ ags_status ags_init(const ags_config *cfg, float *d_w, float *d_m, void *hip_str
  * coefficients a step would use now.  w, m and the AGS state are not
  * changed.  d_grads: [K][replica_stride] elements of grad_dtype, caller-
  * owned; replica k starts at element k * replica_stride and uses the
- * layout of w; replica_stride >= n_flat, a multiple of AGS_ALIGN_ELEMS. */
+ * layout of w; replica_stride >= n_flat, a multiple of AGS_ALIGN_ELEMS;
+ * the replica stack must not overlap w or m (AGS_E_ARG). */
 ags_status ags_stats(ags_handle *h, const void *d_grads, int64_t replica_stride,
                      void *hip_stream);
 

@@ -226,6 +226,12 @@ ags_status check_config_and_size(const ags_config* c, std::string& why) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Do the byte ranges [a, a + na) and [b, b + nb) share a byte?
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y ? y - x < na : x - y < nb;
+}
+
 // Is [p, p + bytes) inside one device allocation of the current device?
 ags_status check_device_range(const void* p, size_t bytes, const char* name, std::string& why) {
     hipPointerAttribute_t attr;
@@ -354,6 +360,9 @@ ags_status check_grads(ags_handle* h, const void* d_grads, int64_t stride) {
         return h->fail(AGS_E_ARG, "replica_stride too large");
     const size_t bytes = ((size_t)(h->cfg.K - 1) * (size_t)stride + (size_t)h->grad_extent) *
                          elem_bytes(h->cfg.grad_dtype);
+    const size_t wm_bytes = (size_t)h->cfg.n_flat * sizeof(float);
+    if (overlap(d_grads, bytes, h->d_w, wm_bytes) || overlap(d_grads, bytes, h->d_m, wm_bytes))
+        return h->fail(AGS_E_ARG, "d_grads overlaps w or m");
     std::string why;
     const ags_status s = check_device_range(d_grads, bytes, "d_grads", why);
     if (s != AGS_OK) return h->fail(s, why);
@@ -545,6 +554,10 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
     if (!aligned16(d_w) || !aligned16(d_m)) {
         g_thread_error = "d_w and d_m must be 16-byte aligned";
         return AGS_E_ALIGN;
+    }
+    if (overlap(d_w, (size_t)cfg->n_flat * sizeof(float), d_m, (size_t)cfg->n_flat * sizeof(float))) {
+        g_thread_error = "d_w and d_m overlap";
+        return AGS_E_ARG;
     }
     const int64_t n_tiles = count_tiles(*cfg);
 

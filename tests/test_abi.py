@@ -181,6 +181,14 @@ def test_init_rejects_null_and_misaligned_pointers_before_any_device_call(lib):
     assert h.value is None
 
 
+def test_init_rejects_overlapping_w_and_m_before_any_device_call(lib):
+    cfg = ags.make_config(_table(), 136, 4)        # 544 bytes each
+    for w, m in ((0x10000, 0x10000), (0x10000, 0x10000 + 528), (0x10210, 0x10000)):
+        with pytest.raises(ags.AGSError) as e:
+            ags.ags_init(cfg, w, m)
+        assert e.value.status == ags.AGS_E_ARG and "overlap" in str(e.value)
+
+
 def test_workspace_cap_gives_nomem_before_any_device_call(lib, monkeypatch):
     # The paper's runtime falls back to a smaller batch on out-of-memory; the
     # library reports AGS_E_NOMEM cleanly so a caller can do the same.
@@ -189,7 +197,7 @@ def test_workspace_cap_gives_nomem_before_any_device_call(lib, monkeypatch):
     need = ags.ags_workspace_bytes(cfg)
     monkeypatch.setenv("AGS_MAX_WORKSPACE_BYTES", str(need - 1))
     with pytest.raises(ags.AGSError) as e:
-        ags.ags_init(cfg, 0x10000, 0x20000)
+        ags.ags_init(cfg, 0x1000000000, 0x2000000000)     # disjoint (fake) w and m
     assert e.value.status == ags.AGS_E_NOMEM
     assert "AGS_MAX_WORKSPACE_BYTES" in str(e.value)
 

@@ -526,6 +526,9 @@ def test_bad_device_pointers_are_errors_not_faults():
                 ags.ags_step(h, ptr, stride)
             assert e.value.status == status
         with pytest.raises(ags.AGSError) as e:
+            ags.ags_step(h, m, n_flat)     # a replica stack on top of m
+        assert e.value.status == ags.AGS_E_ARG and "overlap" in str(e.value)
+        with pytest.raises(ags.AGSError) as e:
             ags.ags_read_stats(h, 1)       # nothing has run yet
         assert e.value.status == ags.AGS_E_STATE
         ags.ags_destroy(h)
