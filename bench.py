@@ -432,21 +432,29 @@ def main():
     cold_step = cold_ms[len(cold_ms) // 2]
     del flush
     log(f"cold-cache steps: median {cold_step * 1e3:.1f} us")
-    # Worst case of the coefficient prediction: gradient sets g and 2g in
-    # turn make every step sensitive (Delta = 3, then 0.75), so every AGS
-    # step is applied scaled and then corrected by the second pass.
+    # The coefficient prediction (sensitive iff the last step was) in a
+    # sensitive phase and in its worst case.  Gradient sets g and 2g in
+    # turn make every step sensitive (Delta = 3, then 0.75): predicted right
+    # from the second step on.  The sets g, g, 2g, 2g, ... alternate the
+    # decision (Delta = 0, 3, 0, 0.75, ...): every step is applied with the
+    # other coefficients and corrected by the second pass.
     g2 = g.view(torch.bfloat16).mul(2).view(g.dtype) if gdt == "bf16" else g * 2
-    torch.cuda.synchronize()
     nmis = min(args.steps, 100)
-    e0.record(stream)
-    for i in range(nmis):
-        h.step(g2 if i % 2 == 0 else g, stream)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    mis_ms = e0.elapsed_time(e1) / nmis
-    mis_sens = h.read_stats().glob["sensitive"]
+
+    def timed(pick):
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(nmis):
+            h.step(pick(i), stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / nmis, h.read_stats().glob["sensitive"]
+
+    sens_ms, sens_last = timed(lambda i: g2 if i % 2 == 0 else g)
+    mis_ms, mis_sens = timed(lambda i: g2 if (i // 2) % 2 == 1 else g)
     del g2
-    log(f"mispredicted steps: {mis_ms * 1e3:.1f} us/step (last step sensitive={mis_sens})")
+    log(f"sensitive phase: {sens_ms * 1e3:.1f} us/step; every step mispredicted: "
+        f"{mis_ms * 1e3:.1f} us/step")
 
     graph_ms = None
     if args.graph:
@@ -533,9 +541,13 @@ def main():
                                "caches; the fraction is against hbm_probe's step pattern "
                                "timed the same way"},
         "replica_stride": stride,
+        "sensitive_phase_steps": {"ms_per_step": round(sens_ms, 5), "last_sensitive": sens_last,
+                                  "note": "every step sensitive: predicted from the last "
+                                          "decision, so applied directly from the second on"},
         "mispredicted_steps": {"ms_per_step": round(mis_ms, 5), "last_sensitive": mis_sens,
-                               "note": "every step sensitive: applied with the predicted "
-                                       "coefficients, then corrected (AGS); SGD never corrects"},
+                               "note": "decisions alternating (not sensitive, sensitive, ...): "
+                                       "every step applied with the other coefficients, then "
+                                       "corrected (AGS); SGD never corrects"},
         "graph_replay_ms_per_step": None if graph_ms is None else round(graph_ms, 5),
         "device_copy_GBps": round(copy_bw, 1),
         "hbm_probe": probe,

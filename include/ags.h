@@ -60,6 +60,7 @@
  *  - Work is enqueued on hip_stream (a hipStream_t; NULL is the default
  *    stream) and the call returns without waiting, except ags_read_stats,
  *    ags_get_state, ags_set_state, ags_get_layer_state, ags_set_layer_state,
+ *    ags_get_last_decision, ags_set_last_decision,
  *    ags_get_elementwise_scale, ags_set_elementwise_scale and
  *    ags_get_kernel_times, which wait for the handle's last stream.
  *  - A handle is not thread-safe: one thread at a time.
@@ -213,7 +214,8 @@ ags_status ags_set_lr(ags_handle *h, double lr);
  * writes the layer means of the element scales to gradscale_L, and
  * ags_set_state sets G_prev and the step count only (gradscale_L may be
  * NULL and is not read): the element scales are restored with
- * ags_set_elementwise_scale. */
+ * ags_set_elementwise_scale.  ags_set_state clears the last step's
+ * sensitive bit (see ags_set_last_decision). */
 ags_status ags_get_state(ags_handle *h, double *gradscale_L, double *g_sq_prev,
                          int64_t *step);
 ags_status ags_set_state(ags_handle *h, const double *gradscale_L, double g_sq_prev,
@@ -221,9 +223,24 @@ ags_status ags_set_state(ags_handle *h, const double *gradscale_L, double g_sq_p
 
 /* Per-layer G_l,prev (the ||gbar_l||^2 of the last step), the state of
  * Delta_l: host [n_layers].  Get waits for the handle's last stream; set
- * checks every value is finite and >= 0 (AGS_E_ARG, nothing changed). */
+ * checks every value is finite and >= 0 (AGS_E_ARG, nothing changed) and
+ * clears the layers' last sensitive bits. */
 ags_status ags_get_layer_state(ags_handle *h, double *g_sq_prev_L);
 ags_status ags_set_layer_state(ags_handle *h, const double *g_sq_prev_L);
+
+/* The sensitive bits of the last committed step: the global one, and per
+ * layer the bit that decided the layer (host [n_layers], or NULL to skip);
+ * a step sensitive by definition (Delta infinite: the first) leaves 0.
+ * An AGS or static step applies its update with the coefficients of the
+ * decision predicted from them (sensitive when the last step was, or when
+ * Delta is infinite by definition) and corrects the layers whose actual
+ * decision differs, so the bits only choose the rounding path: a resumed
+ * run that restores them with the rest of the state repeats the original
+ * run bit for bit; without them (cleared by ags_set_state and
+ * ags_set_layer_state) it agrees to fp32 rounding.  Set checks every value
+ * is 0 or 1 (AGS_E_ARG, nothing changed). */
+ags_status ags_get_last_decision(ags_handle *h, int32_t *sensitive, int32_t *sensitive_L);
+ags_status ags_set_last_decision(ags_handle *h, int32_t sensitive, const int32_t *sensitive_L);
 
 /* Elementwise scales gradscale_j (Algorithm 1 read per element; handles
  * created with cfg.elementwise = 1, else AGS_E_STATE).  scale: host fp32

@@ -72,7 +72,8 @@ LAYER_STATS_FIELDS = tuple(n for n, _ in ags_layer_stats._fields_ if n != "reser
 #: every function the header declares
 EXPORTS = ("ags_workspace_bytes", "ags_init", "ags_stats", "ags_step", "ags_read_stats",
            "ags_set_lr", "ags_get_state", "ags_set_state", "ags_get_layer_state",
-           "ags_set_layer_state", "ags_get_elementwise_scale",
+           "ags_set_layer_state", "ags_get_last_decision", "ags_set_last_decision",
+           "ags_get_elementwise_scale",
            "ags_set_elementwise_scale", "ags_set_profiling",
            "ags_get_kernel_times", "ags_status_string", "ags_last_error", "ags_destroy")
 
@@ -119,6 +120,8 @@ def load_library(path: str | None = None):
         "ags_set_state": (c_int, [h, vp, c_dbl, c_i64]),
         "ags_get_layer_state": (c_int, [h, vp]),
         "ags_set_layer_state": (c_int, [h, vp]),
+        "ags_get_last_decision": (c_int, [h, vp, vp]),
+        "ags_set_last_decision": (c_int, [h, ctypes.c_int32, vp]),
         "ags_get_elementwise_scale": (c_int, [h, vp, c_i64]),
         "ags_set_elementwise_scale": (c_int, [h, vp, c_i64]),
         "ags_set_profiling": (c_int, [h, c_int]),
@@ -235,6 +238,22 @@ def ags_set_layer_state(handle, g_sq_prev):
     _check(load_library().ags_set_layer_state(handle, a.ctypes.data), handle)
 
 
+def ags_get_last_decision(handle, n_layers: int):
+    """(global sensitive bit, per-layer bits) of the last committed step."""
+    g = np.zeros(1, np.int32)
+    per = np.zeros(max(int(n_layers), 1), np.int32)
+    _check(load_library().ags_get_last_decision(handle, g.ctypes.data, per.ctypes.data), handle)
+    return int(g[0]), per[:int(n_layers)].copy()
+
+
+def ags_set_last_decision(handle, sensitive: int, sensitive_l=None):
+    if sensitive_l is None:
+        _check(load_library().ags_set_last_decision(handle, int(sensitive), None), handle)
+        return
+    a = np.ascontiguousarray(sensitive_l, dtype=np.int32).reshape(-1)
+    _check(load_library().ags_set_last_decision(handle, int(sensitive), a.ctypes.data), handle)
+
+
 def ags_get_elementwise_scale(handle, n: int):
     out = np.empty(max(int(n), 1), np.float32)
     _check(load_library().ags_get_elementwise_scale(handle, out.ctypes.data, int(n)), handle)
@@ -345,6 +364,16 @@ class AGS:
         if g.size != self.n_layers:
             raise ValueError(f"expected {self.n_layers} values, got {g.size}")
         ags_set_layer_state(self.handle, g)
+
+    def get_last_decision(self):
+        return ags_get_last_decision(self.handle, self.n_layers)
+
+    def set_last_decision(self, sensitive, sensitive_l=None):
+        if sensitive_l is not None:
+            sensitive_l = np.asarray(sensitive_l, dtype=np.int32).reshape(-1)
+            if sensitive_l.size != self.n_layers:
+                raise ValueError(f"expected {self.n_layers} values, got {sensitive_l.size}")
+        ags_set_last_decision(self.handle, sensitive, sensitive_l)
 
     def get_elementwise_scale(self):
         return ags_get_elementwise_scale(self.handle, self.w.numel())

@@ -35,6 +35,7 @@ struct WsLayout {
     size_t gbar = 0, tiles = 0, partials = 0, ldev = 0, coef = 0, corr = 0, counters = 0;
     size_t ew_buf = 0, ew_partials = 0;  // element scales: two [n_flat] fp32 buffers
     size_t g_prev_l = 0;                  // [L] fp64 per-layer G_prev
+    size_t last_sens_l = 0;               // [L] int32 per-layer last sensitive bit
     size_t chunks = 0, chunk_sums = 0, chunk_count = 0;
     size_t counters_bytes = 0;  // finished-layer counter, correction flag
     size_t lstats = 0, gstats = 0, gradscale = 0, state = 0, end = 0;
@@ -85,6 +86,8 @@ WsLayout ws_layout(const ags_config& c, int64_t n_tiles, int64_t n_chunks) {
     p = align_up(p + w.counters_bytes);
     w.g_prev_l = p;
     p = align_up(p + L * sizeof(double));
+    w.last_sens_l = p;
+    p = align_up(p + L * sizeof(int32_t));
     w.lstats = p;
     p += L * sizeof(ags_layer_stats);
     w.gstats = p;
@@ -322,6 +325,7 @@ struct ags_handle {
     ags_global_stats* gstats() const { return reinterpret_cast<ags_global_stats*>(ws + wl.gstats); }
     double* gradscale() const { return reinterpret_cast<double*>(ws + wl.gradscale); }
     double* g_prev_l() const { return reinterpret_cast<double*>(ws + wl.g_prev_l); }
+    int32_t* last_sens_l() const { return reinterpret_cast<int32_t*>(ws + wl.last_sens_l); }
     DevState* state() const { return reinterpret_cast<DevState*>(ws + wl.state); }
 
     ags_status fail(ags_status s, const std::string& why) {
@@ -447,6 +451,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.gradscale = h->gradscale();
     sa.state = h->state();
     sa.g_prev_l = h->g_prev_l();
+    sa.last_sens_l = h->last_sens_l();
     sa.delta_scope = c.delta_scope;
     sa.coef = h->coef();
     sa.corr = h->corr();
@@ -678,6 +683,8 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         e = hipMemsetAsync(h->ws + h->wl.chunk_count, 0, (size_t)cfg->n_layers * sizeof(unsigned), s);
     if (e == hipSuccess)
         e = hipMemsetAsync(h->ws + h->wl.g_prev_l, 0, (size_t)cfg->n_layers * sizeof(double), s);
+    if (e == hipSuccess)
+        e = hipMemsetAsync(h->ws + h->wl.last_sens_l, 0, (size_t)cfg->n_layers * sizeof(int32_t), s);
     if (e == hipSuccess && cfg->elementwise)  // element scales start at 1.0f
         e = hipMemsetD32Async(reinterpret_cast<hipDeviceptr_t>(h->ew_buf(0)), 0x3f800000,
                               2 * (size_t)cfg->n_flat, s);
@@ -797,8 +804,50 @@ ags_status ags_set_layer_state(ags_handle* h, const double* g_sq_prev_L) {
     hipError_t e = hipStreamSynchronize(h->last_stream);
     if (e == hipSuccess)
         e = hipMemcpyAsync(h->g_prev_l(), g_sq_prev_L, bytes, hipMemcpyHostToDevice, h->last_stream);
+    // the layers' last decisions are cleared (ags_set_last_decision restores them)
+    if (e == hipSuccess)
+        e = hipMemsetAsync(h->last_sens_l(), 0, (size_t)h->cfg.n_layers * sizeof(int32_t),
+                           h->last_stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "writing the layer state");
+    return AGS_OK;
+}
+
+ags_status ags_get_last_decision(ags_handle* h, int32_t* sensitive, int32_t* sensitive_L) {
+    if (!h) return AGS_E_ARG;
+    if (!sensitive) return h->fail(AGS_E_ARG, "sensitive is NULL");
+    int32_t g = 0;
+    hipError_t e = hipMemcpyAsync(&g, h->ws + h->wl.state + offsetof(DevState, last_sens), sizeof g,
+                                  hipMemcpyDeviceToHost, h->last_stream);
+    if (e == hipSuccess && sensitive_L)
+        e = hipMemcpyAsync(sensitive_L, h->last_sens_l(), (size_t)h->cfg.n_layers * sizeof(int32_t),
+                           hipMemcpyDeviceToHost, h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "reading the last decision");
+    *sensitive = g;
+    return AGS_OK;
+}
+
+ags_status ags_set_last_decision(ags_handle* h, int32_t sensitive, const int32_t* sensitive_L) {
+    if (!h) return AGS_E_ARG;
+    if (sensitive != 0 && sensitive != 1) return h->fail(AGS_E_ARG, "sensitive must be 0 or 1");
+    const size_t L = (size_t)h->cfg.n_layers;
+    if (sensitive_L)
+        for (size_t l = 0; l < L; ++l)
+            if (sensitive_L[l] != 0 && sensitive_L[l] != 1)
+                return h->fail(AGS_E_ARG, "sensitive_L values must be 0 or 1");
+    hipError_t e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "waiting for the last stream");
+    // through the pinned staging buffer (no step is queued now)
+    int32_t* st = reinterpret_cast<int32_t*>(h->pinned);
+    st[0] = sensitive;
+    e = hipMemcpyAsync(h->ws + h->wl.state + offsetof(DevState, last_sens), st, sizeof(int32_t),
+                       hipMemcpyHostToDevice, h->last_stream);
+    if (e == hipSuccess && sensitive_L)
+        e = hipMemcpyAsync(h->last_sens_l(), sensitive_L, L * sizeof(int32_t), hipMemcpyHostToDevice,
+                           h->last_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "writing the last decision");
     return AGS_OK;
 }
 

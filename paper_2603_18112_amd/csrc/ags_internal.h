@@ -95,10 +95,10 @@ struct ChunkSum {
 
 // Device-resident AGS state, updated by the last block of a committed step.
 struct DevState {
-    double g_prev;   // ||G||^2 of the last committed step (0 before the first)
-    int64_t step;    // steps completed
-    int32_t ew_cur;  // element scales: which of the two buffers is in force
-    int32_t pad_;
+    double g_prev;      // ||G||^2 of the last committed step (0 before the first)
+    int64_t step;       // steps completed
+    int32_t last_sens;  // the sensitive bit of the last committed step
+    int32_t ew_cur;     // element scales: which of the two buffers is in force
 };
 
 // Per-tile fp32 partial sums: W (sum w^2), G (sum gbar^2), D (sum over
@@ -132,6 +132,7 @@ struct StepArgs {
     double* gradscale;       // [n_layers]; with element scales, their layer means
     DevState* state;
     double* g_prev_l;        // [n_layers] G_l of the last committed step
+    int32_t* last_sens_l;    // [n_layers] the bit that decided each layer then
     int delta_scope;         // ags_delta_scope
     float2* coef;            // [n_layers] (a_l, b_l) as applied, fp32
     float2* corr;            // [n_layers] correction c = x + y * scale_j (fp32)

@@ -556,7 +556,10 @@ __device__ __forceinline__ void write_layer(const StepArgs& a, int l, const Sum4
 // With element scales gradscale_l is the layer mean of the element scales
 // (so a_l above is the mean coefficient applied), the step kernel has
 // refreshed the elements, and a mispredicted scaled layer is corrected per
-// element by c_j = 1 - gradscale_j (x = 1, y = -1).
+// element by c_j = 1 - gradscale_j (x = 1, y = -1) when it was applied
+// scaled, by c_j = gradscale_j - 1 when it was applied unscaled.  The bits
+// that decided the step are kept in the state: the next step predicts
+// from them.
 // Inputs of the global part that no block of this launch writes before the
 // last block reads them, loaded by every block at its start so that the
 // last one has them at hand: the state (thread 0) and, for layer
@@ -566,14 +569,16 @@ struct Prefetch {
     long long step;
     uint32_t flags;
     int ew_cur;
+    int last_sens, last_sens_l;  // the last committed step's bits
     bool ew_refresh;  // a committed elementwise step whose refresh is due
 };
 
 __device__ __forceinline__ Prefetch prefetch_global(const StepArgs& a) {
-    Prefetch p{0.0, 0.0, 0.0, 0, 0u, 0, false};
+    Prefetch p{0.0, 0.0, 0.0, 0, 0u, 0, 0, 0, false};
     p.g_prev = a.state->g_prev;
     p.step = a.state->step;
     p.ew_cur = a.state->ew_cur;
+    p.last_sens = a.state->last_sens;
     p.ew_refresh = a.ew && a.commit && a.refresh_every > 0 &&
                    ((p.step + 1) % a.refresh_every) == 0;
     const int l = threadIdx.x;
@@ -581,6 +586,7 @@ __device__ __forceinline__ Prefetch prefetch_global(const StepArgs& a) {
         p.flags = a.layers[l].flags;
         p.gs = a.gradscale[l];
         p.gpl = a.g_prev_l[l];
+        p.last_sens_l = a.last_sens_l[l];
     }
     return p;
 }
@@ -588,7 +594,7 @@ __device__ __forceinline__ Prefetch prefetch_global(const StepArgs& a) {
 __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* shi,
                                 const Prefetch& pf) {
     const bool ew_refresh = pf.ew_refresh;
-    __shared__ int sh_sens, sh_pred;
+    __shared__ int sh_sens, sh_pred, sh_inf;
     __shared__ long long sh_t;
     Sum4 v = {0.0, 0.0, 0.0, 0.0, 0.0};
     for (int l = threadIdx.x; l < a.n_layers; l += kBlock) {
@@ -621,10 +627,14 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         if (a.commit) {
             a.state->g_prev = G;
             a.state->step = t;
+            // A step sensitive by definition (Delta infinite: the first
+            // one) says nothing about the next: it predicts not sensitive.
+            a.state->last_sens = sens && !surely_sensitive(Gp, step);
             if (ew_refresh) a.state->ew_cur = 1 - pf.ew_cur;  // the refreshed buffer
         }
         sh_sens = sens;
-        sh_pred = surely_sensitive(Gp, step);
+        sh_inf = surely_sensitive(Gp, step);
+        sh_pred = sh_inf || pf.last_sens != 0;
         sh_t = t;
     }
     __syncthreads();
@@ -643,16 +653,20 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         const double gs_old = first ? pf.gs : a.gradscale[l];
         // The layer's own variability Delta_l (always reported); with the
         // per-layer scope it decides the layer, and the step kernel's
-        // prediction was made from the layer's own G_l,prev.
+        // prediction was made from the layer's own G_l,prev and last bit.
         const double Gpl = first ? pf.gpl : a.g_prev_l[l];
-        const bool pred_l = surely_sensitive(Gpl, t - 1);
-        const double dl = (pred_l || !isfinite(o.g_sq)) ? INFINITY : fabs((o.g_sq - Gpl) / Gpl);
+        const bool inf_l = surely_sensitive(Gpl, t - 1);
+        const double dl = (inf_l || !isfinite(o.g_sq)) ? INFINITY : fabs((o.g_sq - Gpl) / Gpl);
         const int sens = a.delta_scope ? !(dl < a.delta) : sens_g;
-        const int pred = a.delta_scope ? pred_l : pred_g;
+        const bool last_l = (first ? pf.last_sens_l : a.last_sens_l[l]) != 0;
+        const int pred = a.delta_scope ? (inf_l || last_l) : pred_g;
         o.delta = dl;
         o.sensitive = sens;
         o.reserved = 0;
-        if (a.commit) a.g_prev_l[l] = o.g_sq;
+        if (a.commit) {
+            a.g_prev_l[l] = o.g_sq;
+            a.last_sens_l[l] = sens && !(a.delta_scope ? inf_l : (bool)sh_inf);
+        }
         double ca = 1.0, cb = lam;
         if (a.mode == AGS_MODE_AGS) {
             ca = (scaled && !sens) ? gs_old : 1.0;
@@ -672,7 +686,10 @@ __device__ void finalize_global(const StepArgs& a, bool updated, Sum4* sh, int* 
         if (updated) {
             float2 c = make_float2(0.0f, 0.0f);
             if (a.ew) {
+                // c_j = x + y gradscale_j: applied scaled, true unscaled, or
+                // the other way round
                 if (scaled && !pred && sens) c = make_float2(1.0f, -1.0f);
+                else if (scaled && pred && !sens) c = make_float2(-1.0f, 1.0f);
             } else {
                 double ap = 1.0;
                 if (scaled && !pred) {
@@ -839,8 +856,9 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
 
-    // Coefficients predicted before the step: on a step whose Delta is
-    // infinite by definition the unscaled ones, otherwise the scaled ones.
+    // Coefficients predicted before the step: the unscaled ones when the
+    // step is surely sensitive (Delta infinite by definition) or the last
+    // committed step was sensitive, otherwise the scaled ones.
     float ca = 1.0f, cb = 0.0f;
     bool use_gs = false, scaled = false, refresh = false;
     const float* gs_old = nullptr;
@@ -848,8 +866,9 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
     if (UPD) {
         const uint32_t f = a.layers[l].flags;
         const long long step = a.state->step;
-        const bool pred = a.delta_scope ? surely_sensitive(a.g_prev_l[l], step)
-                                        : surely_sensitive(a.state->g_prev, step);
+        const bool pred = a.delta_scope
+                              ? surely_sensitive(a.g_prev_l[l], step) || a.last_sens_l[l] != 0
+                              : surely_sensitive(a.state->g_prev, step) || a.state->last_sens != 0;
         scaled = (f & AGS_LAYER_SCALE) != 0;
         if (EW) {
             // The buffer in force and the refresh, from the device state.

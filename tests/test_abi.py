@@ -211,6 +211,8 @@ def test_null_handle_calls_are_errors(lib):
     assert lib.ags_get_elementwise_scale(None, None, 0) == ags.AGS_E_ARG
     assert lib.ags_get_layer_state(None, None) == ags.AGS_E_ARG
     assert lib.ags_set_layer_state(None, None) == ags.AGS_E_ARG
+    assert lib.ags_get_last_decision(None, None, None) == ags.AGS_E_ARG
+    assert lib.ags_set_last_decision(None, 0, None) == ags.AGS_E_ARG
     assert lib.ags_set_elementwise_scale(None, None, 0) == ags.AGS_E_ARG
     lib.ags_destroy(None)
 

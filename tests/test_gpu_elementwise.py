@@ -208,7 +208,10 @@ def test_stats_call_does_not_mutate():
 def test_checkpoint_resume_bitwise():
     import torch
     lay = layouts.get_layout("resnet18_cifar")
-    grads = [to_device(synth.replica_grads(lay, 8, t, 2)) for t in range(8)]
+    # step 3 is sensitive (gradients doubled from it on): the resumed run
+    # restores the last decision too
+    grads = [to_device(synth.replica_grads(lay, 8, t, 2) * np.float32(2.0 if t >= 2 else 1.0))
+             for t in range(8)]
     hyper = dict(elementwise=True, refresh_every=1)
     a = Pair(lay, 8, seed=2, **hyper)
     for g in grads:
@@ -216,12 +219,14 @@ def test_checkpoint_resume_bitwise():
     b = Pair(lay, 8, seed=2, **hyper)
     for g in grads[:3]:
         b.gpu.step(g)
-    state = b.gpu.get_state()
+    state, last = b.gpu.get_state(), b.gpu.get_last_decision()
+    assert last[0] == 1
     scales = b.gpu.get_elementwise_scale()
     w2, m2 = b.w.clone(), b.m.clone()
     b.close()
     c = ags.AGS(lay.table(), w2, m2, 8, **b.hyper)
     c.set_state(None, state[1], state[2])
+    c.set_last_decision(*last)
     c.set_elementwise_scale(scales)
     for g in grads[3:]:
         c.step(g)

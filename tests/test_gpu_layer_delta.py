@@ -110,7 +110,10 @@ def test_layer_state_set_from_the_oracle_then_steps():
 def test_checkpoint_resume_bitwise():
     import torch
     lay = layouts.get_layout("resnet18_cifar")
-    grads = [to_device(synth.replica_grads(lay, 8, t, 2)) for t in range(8)]
+    # step 3 doubles every gradient (every layer sensitive): the resumed run
+    # restores the layers' last decisions too
+    grads = [to_device(synth.replica_grads(lay, 8, t, 2) * np.float32(2.0 if t >= 2 else 1.0))
+             for t in range(8)]
     hyper = dict(delta_scope="layer")
     a = Pair(lay, 8, seed=2, **hyper)
     for g in grads:
@@ -119,11 +122,15 @@ def test_checkpoint_resume_bitwise():
     for g in grads[:3]:
         b.gpu.step(g)
     state, lstate = b.gpu.get_state(), b.gpu.get_layer_state()
+    last = b.gpu.get_last_decision()
+    assert last[1].sum() > 0
     w2, m2 = b.w.clone(), b.m.clone()
     b.close()
     c = ags.AGS(lay.table(), w2, m2, 8, **b.hyper)
     c.set_state(*state)
     c.set_layer_state(lstate)
+    assert c.get_last_decision()[1].sum() == 0      # cleared by set_layer_state
+    c.set_last_decision(*last)
     for g in grads[3:]:
         c.step(g)
     torch.cuda.synchronize()

@@ -437,29 +437,52 @@ def test_two_handles_on_two_streams_interleaved():
         assert np.array_equal(a[3][0], b[3][0]) and a[3][1:] == b[3][1:]
 
 
+def _resume_grads(lay, K, n, seed, scale_from):
+    # fresh draws; from step scale_from + 1 on the gradients are doubled, so
+    # that step is sensitive (Delta = 3) and the next ones are not
+    return [to_device(synth.replica_grads(lay, K, t, seed) * np.float32(2.0 if t >= scale_from else 1.0))
+            for t in range(n)]
+
+
 def test_checkpoint_resume_bitwise():
+    """Resumed right after a sensitive step: with the last decision restored
+    too, the resumed run predicts (and rounds) as the original, bit for bit;
+    without it, the next step takes the other rounding path and agrees to
+    the parameter tolerance."""
     import torch
     lay = layouts.get_layout("resnet18_cifar")
-    grads = [to_device(synth.replica_grads(lay, 8, t, 2)) for t in range(10)]
+    grads = _resume_grads(lay, 8, 10, 2, 4)
     a = Pair(lay, 8, seed=2)
     for g in grads:
         a.gpu.step(g)
     b = Pair(lay, 8, seed=2)
     for g in grads[:5]:
         b.gpu.step(g)
-    state = b.gpu.get_state()
+    state, last = b.gpu.get_state(), b.gpu.get_last_decision()
+    assert last[0] == 1                    # step 5 was sensitive
     w2, m2 = b.w.clone(), b.m.clone()
+    w3, m3 = b.w.clone(), b.m.clone()
     b.close()
     c = ags.AGS(lay.table(), w2, m2, 8, **{k: v for k, v in b.hyper.items()})
     c.set_state(*state)
+    assert c.get_last_decision()[0] == 0   # cleared by set_state
+    c.set_last_decision(*last)
+    d = ags.AGS(lay.table(), w3, m3, 8, **{k: v for k, v in b.hyper.items()})
+    d.set_state(*state)
     for g in grads[5:]:
         c.step(g)
+        d.step(g)
     torch.cuda.synchronize()
     assert torch.equal(a.w, w2) and torch.equal(a.m, m2)
     sa, sc = a.gpu.get_state(), c.get_state()
     assert np.array_equal(sa[0], sc[0]) and sa[1:] == sc[1:]
+    assert a.gpu.get_last_decision()[0] == c.get_last_decision()[0] == 0
+    table = lay.table()
+    check_params(w3.cpu().numpy(), a.w.cpu().numpy().astype(np.float64), table, "resumed without the bit")
+    check_params(m3.cpu().numpy(), a.m.cpu().numpy().astype(np.float64), table, "resumed without the bit (m)")
     a.close()
     c.close()
+    d.close()
 
 
 def test_set_lr_and_profiling():
