@@ -14,7 +14,8 @@ Prints one JSON line (last line of stdout):
                  parameter per step (each replica read once, w and m read and
                  written once) over the measured step time
   roofline       the dominant kernel's algorithmic bytes per launch over its
-                 average duration (HIP events on the launch stream), against
+                 average duration (start and stop events of its own dispatch
+                 on the launch stream), against
                  the 8 TB/s HBM peak; traffic = HBM bytes per launch from
                  rocprofv3 FETCH_SIZE/WRITE_SIZE (committed summary), or null
                  when the kernels changed since it was taken; also as a
@@ -22,6 +23,11 @@ Prints one JSON line (last line of stdout):
                  package's hbm_probe (random data): a read-only stream, and
                  the step's own byte pattern with trivial arithmetic
   hbm_probe      those measured ceilings (and a copy), GB/s
+  cold_cache     single steps after a 1 GiB read evicts the caches
+  sensitive_phase_steps, mispredicted_steps
+                 steps whose decisions are all sensitive (predicted from the
+                 last decision, so corrected only once) and alternate (every
+                 step corrected: the worst case)
   cpu_baseline   the float64 oracle on the host on whole steps of the same
                  workload (a reported baseline, not a target)
 
