@@ -158,4 +158,17 @@ def test_layer_state_argument_errors():
             p.gpu.set_layer_state(bad)
         assert e.value.status == ags.AGS_E_ARG
     assert np.all(p.gpu.get_layer_state() == 0.0)
+    # the last decision: bits only, nothing changed on a refusal
+    for g, per in ((2, None), (0, [0, 3]), (-1, [0, 0])):
+        with pytest.raises(ags.AGSError) as e:
+            p.gpu.set_last_decision(g, per)
+        assert e.value.status == ags.AGS_E_ARG
+    g, per = p.gpu.get_last_decision()
+    assert g == 0 and list(per) == [0, 0]
+    p.gpu.set_last_decision(1, [1, 0])
+    g, per = p.gpu.get_last_decision()
+    assert g == 1 and list(per) == [1, 0]
+    p.gpu.set_last_decision(0)            # the layers' bits stay
+    g, per = p.gpu.get_last_decision()
+    assert g == 0 and list(per) == [1, 0]
     p.close()
