@@ -29,14 +29,22 @@ Prints one JSON line (last line of stdout):
                  last decision, so corrected only once) and alternate (every
                  step corrected: the worst case)
   cpu_baseline   the float64 oracle on the host on whole steps of the same
-                 workload (a reported baseline, not a target)
+                 workload (a reported baseline, not a target): on every host
+                 core (the layers split into one group per core, each group
+                 stepped by the unchanged single-threaded oracle on a thread
+                 of its own), and on one thread
+  configs        the other configurations in AGS mode (tiny CNN K=4 fp32,
+                 ResNet-18 CIFAR K=8 fp32, VGG-16 K=8 fp32, the ResNet-50
+                 sweep K=1..64 bf16): microseconds per step warm and cold,
+                 GB/s and fraction of peak for both, the kernel split
 
 With --elementwise the scale of Algorithm 1 is kept per parameter element
 (AGS mode): a step also reads the scales in force and writes the refreshed
 ones, (K*2 + 24) bytes per parameter.
 
 Usage: python bench.py [--gpus 1] [--steps 200] [--warmup 20]
-                       [--no-cpu-baseline] [--no-probe] [--copy-probe] [--elementwise]
+                       [--no-cpu-baseline] [--no-probe] [--no-configs] [--copy-probe]
+                       [--elementwise]
                        [--delta-scope global|layer] [--mode ags|sgd|lars|static]
 """
 from __future__ import annotations
@@ -177,6 +185,69 @@ def copy_probe(torch, nbytes=1 << 30, reps=20):
     return 2 * n * 4 / (ms * 1e-3) / 1e9
 
 
+def host_cores() -> int:
+    """Host cores this process may run on (its affinity mask)."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def split_layers(numels, parts):
+    """Layers into at most ``parts`` groups of nearly equal element counts
+    (largest first onto the lightest group); groups keep layer order."""
+    import heapq
+    parts = max(1, min(parts, len(numels)))
+    heap = [(0, i) for i in range(parts)]
+    groups = [[] for _ in range(parts)]
+    for l in sorted(range(len(numels)), key=lambda l: -int(numels[l])):
+        load, i = heapq.heappop(heap)
+        groups[i].append(l)
+        heapq.heappush(heap, (load + int(numels[l]), i))
+    return [sorted(g) for g in groups if g]
+
+
+def cpu_baseline_parallel(layout, w0, grads_np, cores, budget_s=15.0, max_steps=30):
+    """The float64 oracle as it stands, on all host cores: the layers are
+    split into ``cores`` groups of nearly equal size, each group is a model
+    of its own (its layers packed end to end, with its share of every
+    replica), and one thread per group runs the unchanged single-threaded
+    oracle on it; the oracle is C called through ctypes, which releases the
+    interpreter lock, so the groups' steps run in parallel.  A group takes
+    its own Delta and decision over its layers (O(layers) work); the
+    per-element work of a step is the whole model's.  Returns the median
+    wall time of a whole parallel step, the steps timed and the threads."""
+    import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
+    from oracle import OracleAGS
+    table = layout.table()
+    groups = split_layers([n for _, n, _ in table], cores)
+    oracles, gsub = [], []
+    for grp in groups:
+        sub, o = [], 0
+        for l in grp:
+            n = table[l][1]
+            sub.append((o, n, table[l][2]))
+            o += (n + 7) // 8 * 8
+        w_sub = np.zeros(o, np.float32)
+        g_sub = np.zeros((grads_np.shape[0], o), grads_np.dtype)
+        for (so, n, _), l in zip(sub, grp):
+            lo = table[l][0]
+            w_sub[so:so + n] = w0[lo:lo + n]
+            g_sub[:, so:so + n] = grads_np[:, lo:lo + n]
+        oracles.append(OracleAGS(sub, o, K, w_sub, grad_dtype="bf16" if E_G == 2 else "f32",
+                                 **HYPER))
+        gsub.append(g_sub)
+    times = []
+    with ThreadPoolExecutor(len(groups)) as ex:
+        t_start = time.time()
+        while len(times) < max_steps and (time.time() - t_start) < budget_s:
+            t0 = time.perf_counter()
+            list(ex.map(lambda i: oracles[i].step(gsub[i]), range(len(groups))))
+            times.append(time.perf_counter() - t0)
+    return sorted(times)[len(times) // 2], len(times), len(groups)
+
+
 def cpu_baseline(layout, w0, grads_np, budget_s=20.0, max_steps=30):
     """The float64 oracle as it stands, single-threaded, on whole steps."""
     from oracle import OracleAGS
@@ -190,6 +261,100 @@ def cpu_baseline(layout, w0, grads_np, budget_s=20.0, max_steps=30):
         times.append(time.perf_counter() - t0)
     sec = sorted(times)[len(times) // 2]
     return sec, len(times)
+
+
+def time_config(h, g, stream, torch, steps, warmup, flush, n_cold=20):
+    """Whole-step times of one handle: warm (back-to-back steps, mean over
+    ``steps``), cold (median of single steps, each after ``flush`` is read
+    with ordinary loads, which evicts the L2s and the Infinity Cache), and
+    each kernel's average duration from its own dispatch events."""
+    for _ in range(warmup):
+        h.step(g, stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        h.step(g, stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    warm = e0.elapsed_time(e1) / steps
+    h.set_profiling(True)
+    h.kernel_times()
+    for _ in range(steps):
+        h.step(g, stream)
+    torch.cuda.synchronize()
+    kms, ncalls = h.kernel_times()
+    h.set_profiling(False)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(n_cold)]
+    for a0, a1 in ev:
+        flush.sum()
+        a0.record(stream)
+        h.step(g, stream)
+        a1.record(stream)
+    torch.cuda.synchronize()
+    cold = sorted(a0.elapsed_time(a1) for a0, a1 in ev)[n_cold // 2]
+    from paper_2603_18112_amd import ags
+    return warm, cold, {n: round(kms[i] / ncalls * 1e3, 2) for i, n in enumerate(ags.KERNEL_NAMES)}
+
+
+def measure_configs(torch, np, stream, steps, warmup):
+    """Every configuration besides the headline, in AGS mode: the tiny CNN
+    (K = 4 fp32), ResNet-18 CIFAR (K = 8 fp32), VGG-16 (K = 8 fp32) and the
+    ResNet-50 batch-size sweep (K = 1..64 bf16; the first K replicas of one
+    K = 64 draw, which are the bytes a K-replica draw gives).  Per
+    configuration: whole-step microseconds warm and cold, algorithmic GB/s
+    and fraction of the 8 TB/s peak for both, steps/s, the per-kernel split;
+    for the sweep also the median over layers of >= 1000 elements of the
+    noise ratio V_l / G_l against its expectation c^2 (K-1) / (K + c^2)
+    under the generator (c = 0.5)."""
+    from paper_2603_18112_amd import ags, layouts, synth
+    flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    out = {}
+
+    def run(name, lay, k, gdt, g, noise_check=False):
+        w = torch.from_numpy(synth.init_weights(lay, 0)).cuda()
+        m = torch.zeros_like(w)
+        h = ags.AGS(lay.table(), w, m, k, grad_dtype=gdt, mode="ags",
+                    **{**HYPER, "elementwise": False, "delta_scope": "global"})
+        warm, cold, ksplit = time_config(h, g, stream, torch, steps, warmup, flush)
+        nbytes = lay.n_params * (k * (2 if gdt == "bf16" else 4) + 16)
+        rec = {"K": k, "grad_dtype": gdt, "params": lay.n_params, "bytes_per_step": nbytes,
+               "us_warm": round(warm * 1e3, 2), "us_cold": round(cold * 1e3, 2),
+               "GBps_warm": round(nbytes / (warm * 1e-3) / 1e9, 1),
+               "GBps_cold": round(nbytes / (cold * 1e-3) / 1e9, 1),
+               "peak_frac_warm": round(nbytes / (warm * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+               "peak_frac_cold": round(nbytes / (cold * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+               "steps_per_s": round(1e3 / warm, 1), "kernel_us": ksplit}
+        if noise_check:
+            big = np.array([n >= 1000 for _, n, _ in lay.table()])
+            rho = np.asarray(h.read_stats().layer["noise_ratio"])[big]
+            rec["noise_ratio_median"] = round(float(np.median(rho)), 6)
+            rec["noise_ratio_expected"] = round(0.25 * (k - 1) / (k + 0.25), 6)
+        h.close()
+        del w, m
+        out[name] = rec
+        log(f"config {name}: {rec['us_warm']} us warm, {rec['us_cold']} us cold "
+            f"({rec['peak_frac_warm']:.3f} / {rec['peak_frac_cold']:.3f} of peak)")
+
+    for name, lname, k, gdt in (("tiny_cnn_k4_f32", "tiny_cnn", 4, "f32"),
+                                ("resnet18_cifar_k8_f32", "resnet18_cifar", 8, "f32"),
+                                ("vgg16_k8_f32", "vgg16", 8, "f32")):
+        lay = layouts.get_layout(lname)
+        g_np = synth.replica_grads(lay, k, 0, 0, dtype=gdt, stride=layouts.replica_stride(lay))
+        g = torch.from_numpy(g_np).cuda()
+        del g_np
+        run(name, lay, k, gdt, g)
+        del g
+    lay = layouts.get_layout("resnet50")
+    g_np = synth.replica_grads(lay, max(PLAN_KS), 0, 0, dtype="bf16",
+                               stride=layouts.replica_stride(lay))
+    g_all = torch.from_numpy(g_np.view(np.int16)).cuda()
+    del g_np
+    for k in PLAN_KS:
+        run(f"resnet50_k{k}_bf16", lay, k, "bf16", g_all[:k], noise_check=True)
+    del g_all, flush
+    return out
 
 
 PLAN_KS = (1, 2, 4, 8, 16, 32, 64)
@@ -330,6 +495,9 @@ def main():
                     help="AGS with one scale per parameter element")
     ap.add_argument("--delta-scope", default="global", choices=["global", "layer"],
                     help="variability measure that decides a layer: global Delta or Delta_l")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the timing of the other configurations (tiny CNN, ResNet-18, "
+                         "VGG-16, the ResNet-50 K sweep) that the default run reports")
     ap.add_argument("--plan", action="store_true",
                     help="time the ResNet-50 bf16 step for K = 1..64 and fit the planner's "
                          "step-time model to it (full and partial search), then its knee")
@@ -501,14 +669,30 @@ def main():
     copy_bw = copy_probe(torch)
     log(f"device copy: {copy_bw:.1f} GB/s")
 
+    configs = None
+    if not args.no_configs and wkey == WORKLOAD and args.mode == "ags":
+        h.close()
+        h = None
+        configs = measure_configs(torch, np, stream, args.steps, args.warmup)
+
     cpu = None
     if not args.no_cpu_baseline:
-        log("cpu baseline: oracle on whole steps ...")
+        cores = host_cores()
+        log(f"cpu baseline: oracle on whole steps, {cores} threads ...")
+        psec, pn, threads = cpu_baseline_parallel(lay, w0, g_np, cores)
+        log(f"cpu baseline: {psec:.3f} s/step on {threads} threads; 1 thread ...")
         sec, n = cpu_baseline(lay, w0, g_np)
-        cpu = {"value": round(ab["whole_step"] / sec / 1e9, 3), "unit": "GB/s", "cores": 1,
-               "kind": "oracle", "sec_per_step": round(sec, 3),
-               "sample": f"median of {n} whole steps of {wkey}, float64, 1 thread"}
-        log(f"cpu baseline: {sec:.2f} s/step")
+        cpu = {"value": round(ab["whole_step"] / psec / 1e9, 3), "unit": "GB/s", "cores": threads,
+               "kind": "oracle", "sec_per_step": round(psec, 4),
+               "host_cores": cores,
+               "sample": (f"median of {pn} whole steps of {wkey}, float64, the layers split into "
+                          f"{threads} groups of nearly equal size, one thread per group running "
+                          f"the unchanged single-threaded oracle"),
+               "single_thread": {"value": round(ab["whole_step"] / sec / 1e9, 3), "unit": "GB/s",
+                                 "cores": 1, "sec_per_step": round(sec, 3),
+                                 "sample": f"median of {n} whole steps of {wkey}, float64, "
+                                           f"1 thread"}}
+        log(f"cpu baseline: {sec:.2f} s/step on 1 thread")
 
     headline = wkey == WORKLOAD and args.mode == "ags"
     mode_note = "" if args.mode == "ags" else f", {args.mode.upper()} mode"
@@ -526,6 +710,11 @@ def main():
         "ms_per_step": round(ms_step, 5),
         "steps_per_s": round(1e3 / ms_step, 1),
         "hbm_peak_frac": round(value / HBM_PEAK_GBPS, 4),
+        "hbm_peak_frac_cold": round(cold_value / HBM_PEAK_GBPS, 4),
+        "value_basis": ("warm: back-to-back steps reusing one gradient set, so w and m (16 B per "
+                        "parameter) can stay in the 256 MB Infinity Cache between steps; "
+                        "hbm_peak_frac_cold and cold_cache give the step after the caches are "
+                        "evicted, as after a forward and backward pass"),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -540,6 +729,7 @@ def main():
         "kernel_us": {n: round(v * 1e3, 2) for n, v in avg_ms.items()},
         "cold_cache": {"ms_per_step": round(cold_step, 5),
                        "value": round(cold_value, 1),
+                       "hbm_peak_frac": round(cold_value / HBM_PEAK_GBPS, 4),
                        "frac_of_measured_cold_step_pattern": (
                            round(cold_value / probe["step_pattern_cold_GBps"], 4)
                            if probe and "step_pattern_cold_GBps" in probe else None),
@@ -559,10 +749,12 @@ def main():
         "hbm_probe": probe,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "configs": configs,
         "last_step": {"delta": s.glob["delta"], "sensitive": s.glob["sensitive"],
                       "step": s.glob["step"]},
     }
-    h.close()
+    if h is not None:
+        h.close()
     print(json.dumps(out), flush=True)
 
 

@@ -63,6 +63,15 @@
  *    ags_get_last_decision, ags_set_last_decision,
  *    ags_get_elementwise_scale, ags_set_elementwise_scale and
  *    ags_get_kernel_times, which wait for the handle's last stream.
+ *  - Calls on one handle are ordered: the handle's workspace and state are
+ *    shared by all its steps, so a call on a stream other than the one the
+ *    handle last used first makes that stream wait (a HIP event) for the
+ *    work already queued on the handle's last stream.  Neither stream may
+ *    be capturing a graph then: a step captured into a graph must be
+ *    ordered after the handle's earlier work by the caller (for example by
+ *    capturing on the stream the handle last used, or after a synchronize).
+ *    The caller's own accesses to w, m and the gradients are ordered by the
+ *    caller, as for any kernel launched on hip_stream.
  *  - A handle is not thread-safe: one thread at a time.
  */
 #ifndef AGS_H
@@ -186,7 +195,13 @@ ags_status ags_init(const ags_config *cfg, float *d_w, float *d_m, void *hip_str
                     ags_handle **out);
 
 /* Statistics only: replica mean, per-layer and global statistics and the
- * coefficients a step would use now.  w, m and the AGS state are not
+ * coefficients a step would use now.  The replica mean is the large-batch
+ * gradient of synchronous data-parallel training (Eq. (1c)); W_l, G_l and
+ * S_l are the per-tensor norms of Algorithm 1 (UpdateGradScale); G and
+ * Delta are the whole-model norm and the variability metric of Eq. (5)
+ * (Sec. III-B); V_l, the spread of the replicas about their mean, measures
+ * the gap between small- and large-batch gradients that the noise term of
+ * Eq. (6) models (Sec. III-C).  w, m and the AGS state are not
  * changed.  d_grads: [K][replica_stride] elements of grad_dtype, caller-
  * owned; replica k starts at element k * replica_stride and uses the
  * layout of w; replica_stride >= n_flat, a multiple of AGS_ALIGN_ELEMS;
@@ -201,12 +216,20 @@ ags_status ags_step(ags_handle *h, const void *d_grads, int64_t replica_stride,
                     void *hip_stream);
 
 /* Copy the records of the last ags_stats / ags_step to host arrays
- * (out_layers [n_layers] may be NULL, out_global may be NULL). */
+ * (out_layers [n_layers] may be NULL, out_global may be NULL): the
+ * statistics of Eq. (5), Eq. (6) and Algorithm 1 listed with ags_stats, the
+ * decision of Algorithm 1 (sensitive iff not Delta < delta) and the
+ * coefficients and scale of the step.  Waits for the handle's last stream;
+ * AGS_E_STATE before the first ags_stats / ags_step. */
 ags_status ags_read_stats(ags_handle *h, ags_layer_stats *out_layers,
                           ags_global_stats *out_global);
 
-/* Learning rate for the steps launched after this call (host schedules).
- * A step captured in a HIP graph keeps the rate it was captured with. */
+/* Learning rate eta for the steps launched after this call.  The paper
+ * keeps eta a host-side schedule (the linear scaling with the batch and
+ * the warm-up and decay of the baselines, Sec. IV-B, IV-D); the update of
+ * Algorithm 1 and the wrapped momentum SGD read it per step.  lr must be
+ * finite and >= 0 (AGS_E_ARG).  A step captured in a HIP graph keeps the
+ * rate it was captured with. */
 ags_status ags_set_lr(ags_handle *h, double lr);
 
 /* Checkpoint / resume of the AGS state (w and m are the caller's).
@@ -216,7 +239,7 @@ ags_status ags_set_lr(ags_handle *h, double lr);
  * NULL and is not read): the element scales are restored with
  * ags_set_elementwise_scale.  ags_set_state clears the last step's
  * sensitive bit (see ags_set_last_decision). */
-ags_status ags_get_state(ags_handle *h, double *gradscale_L, double *g_sq_prev,
+ags_status ags_get_state(const ags_handle *h, double *gradscale_L, double *g_sq_prev,
                          int64_t *step);
 ags_status ags_set_state(ags_handle *h, const double *gradscale_L, double g_sq_prev,
                          int64_t step);

@@ -301,8 +301,10 @@ struct ags_handle {
     char* ws = nullptr;
     char* pinned = nullptr;
     hipStream_t last_stream = nullptr;
+    // Orders a call on another stream after the work queued on last_stream.
+    hipEvent_t order_ev = nullptr;
     bool has_stats = false;
-    std::string err;
+    mutable std::string err;
     bool profiling = false;
     // Per timed step: start and stop event of each kernel's dispatch.
     std::vector<std::array<hipEvent_t, 2 * AGS_N_KERNELS>> ev_pending, ev_free;
@@ -328,11 +330,11 @@ struct ags_handle {
     int32_t* last_sens_l() const { return reinterpret_cast<int32_t*>(ws + wl.last_sens_l); }
     DevState* state() const { return reinterpret_cast<DevState*>(ws + wl.state); }
 
-    ags_status fail(ags_status s, const std::string& why) {
+    ags_status fail(ags_status s, const std::string& why) const {
         err = why;
         return s;
     }
-    ags_status hip_fail(hipError_t e, const char* what) {
+    ags_status hip_fail(hipError_t e, const char* what) const {
         err = std::string(what) + ": " + hipGetErrorString(e);
         (void)hipGetLastError();
         return AGS_E_DEVICE;
@@ -347,6 +349,7 @@ void free_handle(ags_handle* h) {
         for (auto e : q) (void)hipEventDestroy(e);
     for (auto& q : h->ev_free)
         for (auto e : q) (void)hipEventDestroy(e);
+    if (h->order_ev) (void)hipEventDestroy(h->order_ev);
     if (h->ws) (void)hipFree(h->ws);
     if (h->pinned) (void)hipHostFree(h->pinned);
     delete h;
@@ -373,6 +376,17 @@ ags_status check_grads(ags_handle* h, const void* d_grads, int64_t stride) {
     return AGS_OK;
 }
 
+// Is s capturing a graph (an error of the query counts as capturing, so no
+// cross-stream wait is attempted then)?
+bool is_capturing(hipStream_t s) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess) {
+        (void)hipGetLastError();
+        return true;
+    }
+    return cs != hipStreamCaptureStatusNone;
+}
+
 ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipStream_t s,
                        bool commit) {
     int cur = -1;
@@ -380,17 +394,19 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         (void)hipGetLastError();
         return h->fail(AGS_E_DEVICE, "the current HIP device is not the handle's device");
     }
+    // Every step of a handle shares its workspace and state: a call on
+    // another stream waits for the work queued on the handle's last one
+    // (not during graph capture, whose ordering is the caller's).
+    if (s != h->last_stream && !is_capturing(s) && !is_capturing(h->last_stream)) {
+        hipError_t e = hipEventRecord(h->order_ev, h->last_stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s, h->order_ev, 0);
+        if (e != hipSuccess) return h->hip_fail(e, "ordering after the handle's last stream");
+    }
     constexpr int NE = 2 * AGS_N_KERNELS;
     std::array<hipEvent_t, NE> ev{};
     // Steps enqueued while the stream is being captured into a graph are not
     // timed: a graph replays them without the handle's bookkeeping.
-    bool capturing = false;
-    if (commit && h->profiling) {
-        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-        if (hipStreamIsCapturing(s, &cs) != hipSuccess) (void)hipGetLastError();
-        capturing = cs != hipStreamCaptureStatusNone;
-    }
-    const bool prof = commit && h->profiling && !capturing;
+    const bool prof = commit && h->profiling && !is_capturing(s);
     if (prof) {
         if (!h->ev_free.empty()) {
             ev = h->ev_free.back();
@@ -661,6 +677,14 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         free_handle(h);
         return AGS_E_NOMEM;
     }
+    e = hipEventCreateWithFlags(&h->order_ev, hipEventDisableTiming);
+    if (e != hipSuccess) {
+        h->order_ev = nullptr;
+        g_thread_error = std::string("hipEventCreateWithFlags: ") + hipGetErrorString(e);
+        (void)hipGetLastError();
+        free_handle(h);
+        return AGS_E_DEVICE;
+    }
 
     // Initial device state: tables, gradscale = 1, G_prev = 0, step = 0.
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
@@ -737,7 +761,7 @@ ags_status ags_set_lr(ags_handle* h, double lr) {
     return AGS_OK;
 }
 
-ags_status ags_get_state(ags_handle* h, double* gradscale_L, double* g_sq_prev, int64_t* step) {
+ags_status ags_get_state(const ags_handle* h, double* gradscale_L, double* g_sq_prev, int64_t* step) {
     if (!h) return AGS_E_ARG;
     if (!gradscale_L || !g_sq_prev || !step) return h->fail(AGS_E_ARG, "NULL output pointer");
     hipError_t e = hipMemcpyAsync(h->pinned, h->ws + h->wl.gradscale, h->wl.state_bytes,

@@ -203,20 +203,32 @@ class Pair:
 
 def run_steps(layout, K, steps, *, dtype="f32", mode="ags", seed=0, noise=0.5, check_each=True,
               label="", **hyper):
-    """Run ``steps`` fresh-gradient steps on both sides and check them."""
+    """Run ``steps`` fresh-gradient steps on both sides and check them.  The
+    next step's gradients are drawn on a helper thread while the current
+    step runs (the draw is keyed by the step, so the bytes are the same)."""
+    from concurrent.futures import ThreadPoolExecutor
     t0 = time.time()
     p = Pair(layout, K, dtype=dtype, mode=mode, seed=seed, **hyper)
     sig = synth.layer_sigmas(layout, seed)
     worst = (0.0, 0.0)
+
+    def draw(t):
+        return synth.replica_grads(layout, K, t, seed, noise=noise, dtype=dtype, sigmas=sig,
+                                   stride=p.stride)
+
     try:
-        for t in range(steps):
-            g = synth.replica_grads(layout, K, t, seed, noise=noise, dtype=dtype, sigmas=sig,
-                                    stride=p.stride)
-            p.step(g, what=f"{label} step {t + 1}")
-            if check_each or t == steps - 1:
-                r = p.check_state(f"{label} step {t + 1}")
-                worst = (max(worst[0], r[0]), max(worst[1], r[1]))
-            log(f"  {label}: step {t + 1}/{steps} ok ({time.time() - t0:.1f}s)")
+        with ThreadPoolExecutor(1) as ex:
+            nxt = ex.submit(draw, 0)
+            for t in range(steps):
+                g = nxt.result()
+                if t + 1 < steps:
+                    nxt = ex.submit(draw, t + 1)
+                p.step(g, what=f"{label} step {t + 1}")
+                del g
+                if check_each or t == steps - 1:
+                    r = p.check_state(f"{label} step {t + 1}")
+                    worst = (max(worst[0], r[0]), max(worst[1], r[1]))
+                log(f"  {label}: step {t + 1}/{steps} ok ({time.time() - t0:.1f}s)")
     finally:
         p.close()
     return worst

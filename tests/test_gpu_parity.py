@@ -65,8 +65,25 @@ def test_vgg16_k8_five_steps():
 
 @pytest.mark.parametrize("K", [1, 2, 4, 8, 32, 64])
 def test_resnet50_sweep_parity(K):
+    # The batch-size sweep at noise c = 0.5 for its configured 10 steps
+    # (K = 16 is the ten-step test above), at the benchmark's stride.
     lay = layouts.get_layout("resnet50")
-    run_steps(lay, K, 2, dtype="bf16", check_each=False, label=f"r50 K={K}")
+    run_steps(lay, K, 10, dtype="bf16", check_each=False, label=f"r50 K={K}",
+              stride=layouts.replica_stride(lay))
+
+
+@pytest.mark.parametrize("K,c,steps", [(2, 0.1, 10), (2, 2.0, 10), (64, 0.1, 4), (64, 2.0, 10)])
+def test_resnet50_sweep_noise_levels_against_oracle(K, c, steps):
+    """The sweep's other noise levels, c = 0.1 and 2.0 (per-replica noise std
+    in units of the layer's sigma), against the oracle: every statistic
+    (the noise ratio V_l / G_l among them) on every step and every element of
+    w and m after every step.  K = 64 with c = 2.0 is the hardest case for
+    the compiled replica loop's fp32 sums of g_k - g_0, each of which carries
+    replica 0's own deviation (Eq. (1c) averaged in that shifted form)."""
+    lay = layouts.get_layout("resnet50")
+    w = run_steps(lay, K, steps, dtype="bf16", noise=c, check_each=True,
+                  label=f"r50 K={K} c={c}", stride=layouts.replica_stride(lay))
+    log(f"  r50 K={K} c={c}: worst param error / tolerance scale: w {w[0]:.2e} m {w[1]:.2e}")
 
 
 def test_resnet50_sweep_noise_statistic_closed_form():
@@ -435,6 +452,44 @@ def test_two_handles_on_two_streams_interleaved():
         for f in ags.LAYER_STATS_FIELDS:
             assert np.array_equal(a[2][f], b[2][f]), f
         assert np.array_equal(a[3][0], b[3][0]) and a[3][1:] == b[3][1:]
+
+
+def test_one_handle_alternating_streams_is_ordered():
+    """Every call of a handle shares its workspace and state, so a call on
+    another stream than the handle's last one waits for the work queued
+    there: one handle whose steps and statistics calls alternate between
+    three streams, with no synchronisation between the calls, ends bitwise
+    where the same calls on one stream end (w, m, statistics, state)."""
+    import torch
+    lay = layouts.get_layout("resnet18_cifar")
+    K = 8
+    grads = [to_device(synth.replica_grads(lay, K, t, 11)) for t in range(6)]
+    w0 = synth.init_weights(lay, 11)
+    torch.cuda.synchronize()
+
+    def run(streams):
+        w = torch.from_numpy(w0.copy()).cuda()
+        h = ags.AGS(lay.table(), w, torch.zeros_like(w), K, grad_dtype="f32")
+        torch.cuda.synchronize()
+        recs = []
+        for t, g in enumerate(grads):
+            h.step(g, streams[t % len(streams)])
+            h.stats(grads[(t + 1) % len(grads)], streams[(t + 1) % len(streams)])
+            if t % 2 == 1:
+                # read_stats waits for the handle's last stream only
+                recs.append(h.read_stats().layer)
+        torch.cuda.synchronize()
+        out = (h.w.cpu().numpy(), h.m.cpu().numpy(), recs, h.get_state())
+        h.close()
+        return out
+
+    a = run([torch.cuda.current_stream()])
+    b = run([torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.current_stream()])
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    for ra, rb in zip(a[2], b[2]):
+        for f in ags.LAYER_STATS_FIELDS:
+            assert np.array_equal(ra[f], rb[f]), f
+    assert np.array_equal(a[3][0], b[3][0]) and a[3][1:] == b[3][1:]
 
 
 def _resume_grads(lay, K, n, seed, scale_from):
