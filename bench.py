@@ -93,7 +93,8 @@ def kernel_source_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(n_params: int, mode: str = "ags", elementwise: bool = False):
+def algorithmic_bytes(n_params: int, mode: str = "ags", elementwise: bool = False,
+                      reuse_w_norms: bool = True):
     """Per-launch algorithmic bytes of each kernel and of the whole step.
 
     A step reads every replica once and reads and writes w and m once:
@@ -103,14 +104,16 @@ def algorithmic_bytes(n_params: int, mode: str = "ags", elementwise: bool = Fals
     sensitive bit is predicted right.  A LARS step reads the replicas and w
     in the step kernel (and writes the replica mean when K * e_g > 8), then
     reads w, m and the mean (or the replicas again) and writes w, m in the
-    update pass.  Element scales add a 4-byte read of the scale in force and
+    update pass; with reuse_w_norms (the steps timed here) the first pass
+    takes the weight norms from the update pass before it and does not read
+    w.  Element scales add a 4-byte read of the scale in force and
     a 4-byte write of the refreshed one per parameter (refresh every step,
     scales applied: the steps timed here)."""
     step = n_params * (K * E_G + 16 + (8 if elementwise else 0))
     if mode != "lars":
         return {"step": step, "finalize": 0, "second_pass": 0, "whole_step": step}
     mat = K * E_G > 8
-    k0 = n_params * (K * E_G + 4 + (4 if mat else 0))
+    k0 = n_params * (K * E_G + (0 if reuse_w_norms else 4) + (4 if mat else 0))
     k2 = n_params * ((4 if mat else K * E_G) + 16)
     return {"step": k0, "finalize": 0, "second_pass": k2, "whole_step": step}
 
@@ -541,6 +544,8 @@ def main():
     layout_name, K, gdt, desc = WORKLOADS[args.workload]
     E_G = 2 if gdt == "bf16" else 4
     HYPER["elementwise"] = bool(args.elementwise)
+    if args.mode == "lars":
+        HYPER["reuse_w_norms"] = True   # the weight norms carried from the update pass
     HYPER["delta_scope"] = args.delta_scope
     wkey = workload_key(args.workload, args.elementwise, args.delta_scope, args.mode)
     lib = ags.load_library()

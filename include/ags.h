@@ -144,6 +144,9 @@ typedef struct {
     double static_scale;     /* s of AGS_MODE_STATIC (> 0)                 */
     int32_t elementwise;     /* 1: AGS scale per element (AGS mode only)    */
     int32_t delta_scope;     /* ags_delta_scope                            */
+    int32_t reuse_w_norms;   /* 1: LARS takes ||w_l||^2 from the last update
+                                pass instead of reading w (LARS mode only;
+                                see ags_invalidate_weight_norms)           */
 } ags_config;
 
 /* Per-layer record of the last ags_stats / ags_step.  var is V_l (the 1/K
@@ -238,11 +241,31 @@ ags_status ags_set_lr(ags_handle *h, double lr);
  * ags_set_state sets G_prev and the step count only (gradscale_L may be
  * NULL and is not read): the element scales are restored with
  * ags_set_elementwise_scale.  ags_set_state clears the last step's
- * sensitive bit (see ags_set_last_decision). */
+ * sensitive bit (see ags_set_last_decision) and drops LARS's carried
+ * weight norms (see ags_invalidate_weight_norms). */
 ags_status ags_get_state(const ags_handle *h, double *gradscale_L, double *g_sq_prev,
                          int64_t *step);
 ags_status ags_set_state(ags_handle *h, const double *gradscale_L, double g_sq_prev,
                          int64_t step);
+
+/* Weight norms carried from one LARS step to the next (cfg.reuse_w_norms).
+ * The LARS trust ratio of Sec. IV-D needs W_l = ||w_l||^2 before the
+ * update, so a LARS step is two passes: statistics, then the update.  With
+ * reuse_w_norms = 1 the update pass also sums the squares of the new w per
+ * tile, in exactly the order the statistics pass sums them, and the next
+ * ags_step or ags_stats takes W_l from those sums instead of reading w
+ * (4 bytes per parameter less; the statistics are bit for bit those of
+ * reading w, as long as w holds what the last update wrote).  The library
+ * cannot see writes to w made outside its calls: the sums are used only
+ * after a committed LARS ags_step of this handle, and are dropped by
+ * ags_set_state, a step whose launch fails (AGS_E_DEVICE), and this
+ * function, which a
+ * caller that writes w between calls (a checkpoint load, another
+ * optimizer's step, an in-place edit) must call before the next step.  A
+ * step captured into a HIP graph keeps the choice made at capture: capture
+ * after a step if the replays should use the sums.  AGS_E_STATE on a handle
+ * without reuse_w_norms. */
+ags_status ags_invalidate_weight_norms(ags_handle *h);
 
 /* Per-layer G_l,prev (the ||gbar_l||^2 of the last step), the state of
  * Delta_l: host [n_layers].  Get waits for the handle's last stream; set

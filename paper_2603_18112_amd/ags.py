@@ -53,7 +53,8 @@ class ags_config(ctypes.Structure):
                 ("eps", ctypes.c_double), ("s_max", ctypes.c_double),
                 ("trust_coef", ctypes.c_double), ("refresh_every", ctypes.c_int32),
                 ("small_replica", ctypes.c_int32), ("static_scale", ctypes.c_double),
-                ("elementwise", ctypes.c_int32), ("delta_scope", ctypes.c_int32)]
+                ("elementwise", ctypes.c_int32), ("delta_scope", ctypes.c_int32),
+                ("reuse_w_norms", ctypes.c_int32)]
 
 
 class ags_layer_stats(ctypes.Structure):
@@ -74,7 +75,7 @@ EXPORTS = ("ags_workspace_bytes", "ags_init", "ags_stats", "ags_step", "ags_read
            "ags_set_lr", "ags_get_state", "ags_set_state", "ags_get_layer_state",
            "ags_set_layer_state", "ags_get_last_decision", "ags_set_last_decision",
            "ags_get_elementwise_scale",
-           "ags_set_elementwise_scale", "ags_set_profiling",
+           "ags_set_elementwise_scale", "ags_invalidate_weight_norms", "ags_set_profiling",
            "ags_get_kernel_times", "ags_status_string", "ags_last_error", "ags_destroy")
 
 _lib = None
@@ -118,6 +119,7 @@ def load_library(path: str | None = None):
         "ags_set_lr": (c_int, [h, c_dbl]),
         "ags_get_state": (c_int, [h, vp, P(c_dbl), P(c_i64)]),
         "ags_set_state": (c_int, [h, vp, c_dbl, c_i64]),
+        "ags_invalidate_weight_norms": (c_int, [h]),
         "ags_get_layer_state": (c_int, [h, vp]),
         "ags_set_layer_state": (c_int, [h, vp]),
         "ags_get_last_decision": (c_int, [h, vp, vp]),
@@ -151,7 +153,7 @@ def _check(status: int, handle=None):
 def make_config(layers, n_flat, K, *, grad_dtype="f32", mode="ags", lr=0.1, momentum=0.9,
                 weight_decay=5e-4, delta=0.5, eps=1e-8, s_max=0.0, trust_coef=1e-3,
                 refresh_every=1, small_replica=0, static_scale=2.0, elementwise=False,
-                delta_scope="global"):
+                delta_scope="global", reuse_w_norms=False):
     """An ags_config (plus the layer array it points to, kept alive on it)."""
     arr = (ags_layer * max(len(layers), 1))()
     for i, (o, n, f) in enumerate(layers):
@@ -162,7 +164,8 @@ def make_config(layers, n_flat, K, *, grad_dtype="f32", mode="ags", lr=0.1, mome
                      delta=float(delta), eps=float(eps), s_max=float(s_max),
                      trust_coef=float(trust_coef), refresh_every=int(refresh_every),
                      small_replica=int(small_replica), static_scale=float(static_scale),
-                     elementwise=int(bool(elementwise)), delta_scope=DELTA_SCOPES[delta_scope])
+                     elementwise=int(bool(elementwise)), delta_scope=DELTA_SCOPES[delta_scope],
+                     reuse_w_norms=int(bool(reuse_w_norms)))
     cfg._layers_keepalive = arr
     return cfg
 
@@ -225,6 +228,10 @@ def ags_set_state(handle, gradscale, g_sq_prev: float, step: int):
         gs = np.ascontiguousarray(gradscale, dtype=np.float64)
         ptr = gs.ctypes.data
     _check(load_library().ags_set_state(handle, ptr, float(g_sq_prev), int(step)), handle)
+
+
+def ags_invalidate_weight_norms(handle):
+    _check(load_library().ags_invalidate_weight_norms(handle), handle)
 
 
 def ags_get_layer_state(handle, n_layers: int):
@@ -355,6 +362,9 @@ class AGS:
             if gradscale.size != self.n_layers:
                 raise ValueError(f"expected {self.n_layers} gradscale values, got {gradscale.size}")
         ags_set_state(self.handle, gradscale, g_sq_prev, step)
+
+    def invalidate_weight_norms(self):
+        ags_invalidate_weight_norms(self.handle)
 
     def get_layer_state(self):
         return ags_get_layer_state(self.handle, self.n_layers)

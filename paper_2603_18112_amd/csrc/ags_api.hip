@@ -34,6 +34,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct WsLayout {
     size_t gbar = 0, tiles = 0, partials = 0, ldev = 0, coef = 0, corr = 0, counters = 0;
     size_t ew_buf = 0, ew_partials = 0;  // element scales: two [n_flat] fp32 buffers
+    size_t w_norm = 0;                    // LARS: [n_tiles] fp32 sums of w^2 carried over
     size_t g_prev_l = 0;                  // [L] fp64 per-layer G_prev
     size_t last_sens_l = 0;               // [L] int32 per-layer last sensitive bit
     size_t chunks = 0, chunk_sums = 0, chunk_count = 0;
@@ -52,19 +53,23 @@ bool materialize_gbar(const ags_config& c) {
     return c.mode == AGS_MODE_LARS && (size_t)c.K * elem_bytes(c.grad_dtype) > 8;
 }
 
-WsLayout ws_layout(const ags_config& c, int64_t n_tiles, int64_t n_chunks) {
+// stats_only: the pieces a statistics-only call uses (no replica mean kept
+// between passes, no element scales, no carried weight norms).
+WsLayout ws_layout(const ags_config& c, int64_t n_tiles, int64_t n_chunks, bool stats_only = false) {
     WsLayout w;
     size_t p = 0;
     const size_t L = (size_t)c.n_layers;
     w.gbar = p;
-    if (materialize_gbar(c)) p = align_up(p + (size_t)c.n_flat * sizeof(float));
+    if (materialize_gbar(c) && !stats_only) p = align_up(p + (size_t)c.n_flat * sizeof(float));
     w.ew_buf = p;
     w.ew_partials = p;
-    if (c.elementwise) {
+    if (c.elementwise && !stats_only) {
         p = align_up(p + 2 * (size_t)c.n_flat * sizeof(float));
         w.ew_partials = p;
         p = align_up(p + (size_t)n_tiles * sizeof(float));
     }
+    w.w_norm = p;
+    if (c.reuse_w_norms && !stats_only) p = align_up(p + (size_t)n_tiles * sizeof(float));
     w.tiles = p;
     p = align_up(p + (size_t)n_tiles * sizeof(Tile));
     w.partials = p;
@@ -154,6 +159,14 @@ ags_status check_config(const ags_config* c, std::string& why) {
     }
     if (c->delta_scope != AGS_DELTA_GLOBAL && c->delta_scope != AGS_DELTA_LAYER) {
         why = "bad delta_scope";
+        return AGS_E_ARG;
+    }
+    if (c->reuse_w_norms != 0 && c->reuse_w_norms != 1) {
+        why = "reuse_w_norms must be 0 or 1";
+        return AGS_E_ARG;
+    }
+    if (c->reuse_w_norms && c->mode != AGS_MODE_LARS) {
+        why = "reuse_w_norms needs AGS_MODE_LARS";
         return AGS_E_ARG;
     }
     if (c->refresh_every < 0) { why = "refresh_every must be >= 0"; return AGS_E_ARG; }
@@ -304,6 +317,9 @@ struct ags_handle {
     // Orders a call on another stream after the work queued on last_stream.
     hipEvent_t order_ev = nullptr;
     bool has_stats = false;
+    // LARS: the last update pass left per-tile sums of w^2 that the next
+    // statistics pass may take instead of reading w.
+    bool w_norm_valid = false;
     mutable std::string err;
     bool profiling = false;
     // Per timed step: start and stop event of each kernel's dispatch.
@@ -323,6 +339,7 @@ struct ags_handle {
     unsigned* done_count() const { return reinterpret_cast<unsigned*>(ws + wl.counters); }
     int* corr_flag() const { return reinterpret_cast<int*>(done_count() + 1); }
     float* gbar() const { return materialize ? reinterpret_cast<float*>(ws + wl.gbar) : nullptr; }
+    float* w_norm() const { return cfg.reuse_w_norms ? reinterpret_cast<float*>(ws + wl.w_norm) : nullptr; }
     ags_layer_stats* lstats() const { return reinterpret_cast<ags_layer_stats*>(ws + wl.lstats); }
     ags_global_stats* gstats() const { return reinterpret_cast<ags_global_stats*>(ws + wl.gstats); }
     double* gradscale() const { return reinterpret_cast<double*>(ws + wl.gradscale); }
@@ -424,9 +441,11 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     auto kev = [&](int k) {
         return prof ? ags::KernelEvents{ev[2 * k], ev[2 * k + 1]} : ags::KernelEvents{};
     };
-    // A failed launch hands the step's events back to the pool.
+    // A failed launch hands the step's events back to the pool (and the
+    // carried weight norms are no longer trusted).
     auto launch_fail = [&](hipError_t err, const char* what) {
         if (prof) h->ev_free.push_back(ev);
+        h->w_norm_valid = false;
         return h->hip_fail(err, what);
     };
     const ags_config& c = h->cfg;
@@ -484,6 +503,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.ew_buf = h->ew_buf(0);
     sa.n_flat = c.n_flat;
     sa.ew_partials = h->ew_partials();
+    sa.w_norm_in = (!fused && h->w_norm_valid) ? h->w_norm() : nullptr;
     hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s, kev(0));
     if (e != hipSuccess) return launch_fail(e, "step kernel launch");
     e = ags::launch_finalize(sa, (int)h->n_chunks, s, kev(1));
@@ -509,11 +529,13 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         ua.corr_flag = h->corr_flag();
         ua.lr = (float)h->lr;
         ua.momentum = (float)c.momentum;
+        ua.w_norm_out = (c.mode == AGS_MODE_LARS) ? h->w_norm() : nullptr;
         e = (c.mode == AGS_MODE_LARS) ? ags::launch_update(ua, c.grad_dtype, s, kev(2))
                                       : ags::launch_correct(ua, c.grad_dtype, s, kev(2));
         if (e != hipSuccess) return launch_fail(e, "second-pass kernel launch");
     }
     if (prof) h->ev_pending.push_back(ev);
+    if (commit && c.mode == AGS_MODE_LARS) h->w_norm_valid = c.reuse_w_norms != 0;
     h->last_stream = s;
     h->has_stats = true;
     return AGS_OK;
@@ -792,6 +814,7 @@ ags_status ags_set_state(ags_handle* h, const double* gradscale_L, double g_sq_p
     // shared with them.
     hipError_t e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "waiting for the last stream");
+    h->w_norm_valid = false;  // a restored state comes with weights of its own
     // g_prev and step only: the element-scale buffer index stays.
     DevState ds{g_sq_prev, step, 0, 0};
     const size_t soff = h->wl.state - h->wl.gradscale;
@@ -804,6 +827,13 @@ ags_status ags_set_state(ags_handle* h, const double* gradscale_L, double g_sq_p
                             hipMemcpyHostToDevice, h->last_stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->last_stream);
     if (e != hipSuccess) return h->hip_fail(e, "writing state");
+    return AGS_OK;
+}
+
+ags_status ags_invalidate_weight_norms(ags_handle* h) {
+    if (!h) return AGS_E_ARG;
+    if (!h->cfg.reuse_w_norms) return h->fail(AGS_E_STATE, "the handle does not carry weight norms");
+    h->w_norm_valid = false;
     return AGS_OK;
 }
 

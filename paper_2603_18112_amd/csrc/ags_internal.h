@@ -58,7 +58,7 @@ constexpr int64_t kXcdMapMinTiles = 32768;
 constexpr int64_t kEwStreamMinBytes = 192ll << 20;
 
 // Elements per tile of a layer of numel elements.
-inline int64_t tile_elems_for(int64_t numel) {
+__host__ __device__ inline int64_t tile_elems_for(int64_t numel) {
     const int64_t per = (int64_t)kTileElems * kMaxTilesPerLayer;
     const int64_t mult = (numel + per - 1) / per;
     return (int64_t)kTileElems * (mult > 0 ? mult : 1);
@@ -152,6 +152,9 @@ struct StepArgs {
     float* ew_buf;           // [2][n_flat] the two scale buffers
     int64_t n_flat;
     float* ew_partials;      // [n_tiles] per-tile sums of the refreshed scales
+    // LARS: per-tile sums of w^2 written by the last update pass; when set,
+    // the statistics-only step kernel takes W from them and skips w.
+    const float* w_norm_in;
 };
 
 struct UpdateArgs {
@@ -173,6 +176,9 @@ struct UpdateArgs {
     const int* corr_flag;
     float lr;
     float momentum;
+    // LARS update: per-tile sums of the new w^2, summed as the statistics
+    // pass sums w^2 (or nullptr).
+    float* w_norm_out;
 };
 
 // Text for ags_last_error(NULL) on this thread (ags_api.hip).

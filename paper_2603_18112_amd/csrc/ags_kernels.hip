@@ -755,7 +755,9 @@ __device__ __forceinline__ float element_scale(float gsmall, double q, double in
 // EW: 0 = one scale per layer; 1 = element scales, ordinary accesses; 2 =
 // element scales with non-temporal scale loads and scale, w and m stores
 // (the host's choice for working sets the Infinity Cache cannot keep).
-template <typename GT, int KT, int RMODE, bool UPD, int EW, bool FULL>
+// WNC (statistics only): W of the tile comes from the last LARS update
+// pass, so w is not read.
+template <typename GT, int KT, int RMODE, bool UPD, int EW, bool FULL, bool WNC = false>
 __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restrict__ g,
                                            int64_t idx, int n0, int n1, int K, float ca,
                                            float cb, bool use_gs, bool scaled, bool refresh,
@@ -764,9 +766,10 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
                                            float& sg, float& sd, float& ss, float& sx) {
     constexpr int HS = Map<GT>::HS;
     constexpr bool NT = EW == 2;
+    static_assert(!(WNC && UPD), "the update reads w");
     float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
     double q[kVec];
-    load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
+    if (!WNC) load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
     if (UPD) load_f32<FULL, HS>(a.m + idx, n0, n1, mv);
     // Keep the w (and m) loads in front of the replica loads: without the
     // barrier the statistics-only variant issued them only after consuming
@@ -788,7 +791,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
     if (!UPD && a.gbar) store_f32<FULL, HS>(a.gbar + idx, n0, n1, gb);
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
-        sw = fmaf(wv[e], wv[e], sw);
+        if (!WNC) sw = fmaf(wv[e], wv[e], sw);
         sg = fmaf(gb[e], gb[e], sg);
         sd += dv[e];
         // (1/K) sum_k g_k^2 = gbar^2 + (1/K) sum_k (g_k - gbar)^2
@@ -847,7 +850,7 @@ __device__ __forceinline__ int tile_of_block(int b, int n, int xcd_map) {
     return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
 }
 
-template <typename GT, int KT, int RMODE, bool UPD, int EW>
+template <typename GT, int KT, int RMODE, bool UPD, int EW, bool WNC = false>
 __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
     __shared__ float red[5][kTileBlock / 64];
     const int ti = tile_of_block(blockIdx.x, gridDim.x, a.xcd_map);
@@ -888,7 +891,7 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
 
     float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f, sx = 0.0f;
     for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
-        step_group<GT, KT, RMODE, UPD, EW, decltype(full)::value>(
+        step_group<GT, KT, RMODE, UPD, EW, decltype(full)::value, WNC>(
             a, g, idx, n0, n1, K, ca, cb, use_gs, scaled, refresh, gs_old, gs_new, smax, sw, sg, sd,
             ss, sx);
     });
@@ -909,7 +912,7 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
     __syncthreads();
     if (threadIdx.x == 0) {
         Partial p;
-        p.w = tree_sum<kTileBlock / 64>(red[0]);
+        p.w = WNC ? a.w_norm_in[ti] : tree_sum<kTileBlock / 64>(red[0]);
         p.g = tree_sum<kTileBlock / 64>(red[1]);
         p.d = tree_sum<kTileBlock / 64>(red[2]);
         p.s = tree_sum<kTileBlock / 64>(red[3]);
@@ -1048,10 +1051,14 @@ __global__ __launch_bounds__(kTileBlock) void correct_kernel(UpdateArgs a) {
 // final coefficients.  gbar comes from the step kernel's buffer or, when
 // re-reading the replicas costs no more than that round trip, is
 // recomputed from them by the same code.
-template <typename GT, int KT, bool RECOMP, bool FULL>
+// WN: also add the squares of the new w to sw, element by element in the
+// order step_group adds the squares of w (a ragged end's missing elements
+// are 0 on both sides), so that the tile's sum has the bits the next
+// statistics pass would get from reading w.
+template <typename GT, int KT, bool RECOMP, bool FULL, bool WN>
 __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __restrict__ g,
                                              int64_t idx, int n0, int n1, int K, float ca,
-                                             float cb) {
+                                             float cb, float& sw) {
     float gb[kVec], wv[kVec], mv[kVec];
     load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
     load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
@@ -1070,17 +1077,32 @@ __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __re
     }
     store_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
     store_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
+    if (WN) {
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) sw = fmaf(wv[e], wv[e], sw);
+    }
 }
 
-template <typename GT, int KT, bool RECOMP>
+template <typename GT, int KT, bool RECOMP, bool WN>
 __global__ __launch_bounds__(kTileBlock) void update_kernel(UpdateArgs a) {
     const Tile t = a.tiles[blockIdx.x];
     const float2 ab = a.coef[t.layer];
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
+    float sw = 0.0f;
     for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
-        update_group<GT, KT, RECOMP, decltype(full)::value>(a, g, idx, n0, n1, K, ab.x, ab.y);
+        update_group<GT, KT, RECOMP, decltype(full)::value, WN>(a, g, idx, n0, n1, K, ab.x, ab.y,
+                                                                 sw);
     });
+    if (WN) {
+        // the step kernel's reduction: wave butterfly, then the waves in a
+        // fixed pairwise order
+        __shared__ float red[kTileBlock / 64];
+        sw = wave_sum(sw);
+        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sw;
+        __syncthreads();
+        if (threadIdx.x == 0) a.w_norm_out[blockIdx.x] = tree_sum<kTileBlock / 64>(red);
+    }
 }
 
 // ----------------------------------------------------------- dispatch ---
@@ -1101,6 +1123,8 @@ hipError_t launch(void (*k)(A), dim3 grid, dim3 block, hipStream_t s, const A& a
 template <typename GT, int KT, int RMODE>
 hipError_t step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s, KernelEvents ev) {
     const dim3 grid(n_tiles), block(kTileBlock);
+    if (!update && a.w_norm_in)
+        return launch(step_kernel<GT, KT, RMODE, false, 0, true>, grid, block, s, a, ev);
     if (!update) return launch(step_kernel<GT, KT, RMODE, false, 0>, grid, block, s, a, ev);
     if (a.ew == 2) return launch(step_kernel<GT, KT, RMODE, true, 2>, grid, block, s, a, ev);
     if (a.ew) return launch(step_kernel<GT, KT, RMODE, true, 1>, grid, block, s, a, ev);
@@ -1118,8 +1142,12 @@ hipError_t step_k(const StepArgs& a, int n_tiles, bool update, hipStream_t s, Ke
 template <typename GT, int KT>
 hipError_t update_k(const UpdateArgs& a, hipStream_t s, KernelEvents ev) {
     const dim3 grid(a.n_tiles), block(kTileBlock);
-    if (a.gbar) return launch(update_kernel<GT, KT, false>, grid, block, s, a, ev);
-    return launch(update_kernel<GT, KT, true>, grid, block, s, a, ev);
+    if (a.w_norm_out) {
+        if (a.gbar) return launch(update_kernel<GT, KT, false, true>, grid, block, s, a, ev);
+        return launch(update_kernel<GT, KT, true, true>, grid, block, s, a, ev);
+    }
+    if (a.gbar) return launch(update_kernel<GT, KT, false, false>, grid, block, s, a, ev);
+    return launch(update_kernel<GT, KT, true, false>, grid, block, s, a, ev);
 }
 
 template <typename GT, int KT>

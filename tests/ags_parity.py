@@ -159,8 +159,10 @@ class Pair:
         self.w = torch.from_numpy(self.w0.copy()).cuda()
         self.m = torch.zeros_like(self.w)
         self.gpu = ags.AGS(self.table, self.w, self.m, K, grad_dtype=dtype, mode=mode, **self.hyper)
+        # reuse_w_norms only chooses where the GPU takes W_l from
+        ora_hyper = {k: v for k, v in self.hyper.items() if k != "reuse_w_norms"}
         self.ora = OracleAGS(self.table, layout.n_flat, K, self.w0, mode=mode, grad_dtype=dtype,
-                             **self.hyper)
+                             **ora_hyper)
 
     def step(self, grads: np.ndarray, commit=True, check=True, what=""):
         g = to_device(grads)

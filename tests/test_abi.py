@@ -54,7 +54,9 @@ def test_struct_sizes_match_the_header():
     assert ctypes.sizeof(plan.ags_plan_model) == 4 + 4 + 4 * 8 + 4 + 4
     assert ctypes.sizeof(plan.ags_plan_candidate) == 16
     assert ctypes.sizeof(ags.ags_global_stats) == 40
-    assert ctypes.sizeof(ags.ags_config) == 4 + 4 + 8 + 8 + 4 + 4 + 4 + 4 + 7 * 8 + 4 + 4 + 8 + 4 + 4
+    # ... static_scale, elementwise, delta_scope, reuse_w_norms and the tail padding
+    assert ctypes.sizeof(ags.ags_config) == (4 + 4 + 8 + 8 + 4 + 4 + 4 + 4 + 7 * 8 + 4 + 4 + 8 + 4 + 4
+                                             + 4 + 4)
 
 
 def test_status_strings(lib):
@@ -91,6 +93,10 @@ def test_valid_config_workspace_size(lib):
     # ... unless re-reading the replicas is as cheap (K = 4 bf16: 8 bytes).
     cfg = ags.make_config(lay.table(), lay.n_flat, 4, grad_dtype="bf16", mode="lars")
     assert ags.ags_workspace_bytes(cfg) < 2_000_000
+    # Carried weight norms: one fp32 per tile of 2048 elements.
+    cfg2 = ags.make_config(lay.table(), lay.n_flat, 4, grad_dtype="bf16", mode="lars",
+                           reuse_w_norms=True)
+    assert 12_560 * 4 <= ags.ags_workspace_bytes(cfg2) - ags.ags_workspace_bytes(cfg) < 12_560 * 4 + 512
     # Element scales: two fp32 buffers of n_flat (the scales in force and the
     # refreshed ones) plus a per-tile sum.
     cfg = ags.make_config(lay.table(), lay.n_flat, 16, grad_dtype="bf16", elementwise=True)
@@ -127,6 +133,8 @@ def test_valid_config_workspace_size(lib):
     (dict(mode="sgd", elementwise=True), ags.AGS_E_ARG),     # element scales: AGS only
     (dict(mode="lars", elementwise=True), ags.AGS_E_ARG),
     (dict(mode="static", elementwise=True), ags.AGS_E_ARG),
+    (dict(mode="ags", reuse_w_norms=True), ags.AGS_E_ARG),    # carried weight norms: LARS only
+    (dict(mode="sgd", reuse_w_norms=True), ags.AGS_E_ARG),
 ])
 def test_config_validation(lib, kw, status):
     st, msg = _ws(**kw)
@@ -160,8 +168,8 @@ def test_bad_enum_values(lib):
 
 def test_bad_elementwise_and_delta_scope_fields(lib):
     for field, value in (("elementwise", 2), ("elementwise", -1), ("delta_scope", 2),
-                         ("delta_scope", -1)):
-        cfg = ags.make_config(_table(), 136, 4)
+                         ("delta_scope", -1), ("reuse_w_norms", 2), ("reuse_w_norms", -1)):
+        cfg = ags.make_config(_table(), 136, 4, mode="lars")
         setattr(cfg, field, value)
         with pytest.raises(ags.AGSError) as e:
             ags.ags_workspace_bytes(cfg)
@@ -214,6 +222,7 @@ def test_null_handle_calls_are_errors(lib):
     assert lib.ags_get_last_decision(None, None, None) == ags.AGS_E_ARG
     assert lib.ags_set_last_decision(None, 0, None) == ags.AGS_E_ARG
     assert lib.ags_set_elementwise_scale(None, None, 0) == ags.AGS_E_ARG
+    assert lib.ags_invalidate_weight_norms(None) == ags.AGS_E_ARG
     lib.ags_destroy(None)
 
 
@@ -230,3 +239,4 @@ def _load_fresh(path):
         return ags.load_library(path)
     finally:
         ags._lib = saved
+

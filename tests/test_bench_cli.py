@@ -33,12 +33,14 @@ def test_algorithmic_bytes_per_mode():
     ags = bench.algorithmic_bytes(n, "ags")
     assert ags == {"step": 48 * n, "finalize": 0, "second_pass": 0, "whole_step": 48 * n}
     assert bench.algorithmic_bytes(n, "ags", elementwise=True)["step"] == 56 * n
-    lars = bench.algorithmic_bytes(n, "lars")
+    lars = bench.algorithmic_bytes(n, "lars", reuse_w_norms=False)
     # first pass: replicas + w read, mean written; second: mean, w, m read, w, m written
     assert lars["step"] == (32 + 4 + 4) * n and lars["second_pass"] == (4 + 16) * n
     assert lars["whole_step"] == 48 * n
+    # with the weight norms carried from the update pass the first pass skips w
+    assert bench.algorithmic_bytes(n, "lars")["step"] == (32 + 4) * n
     bench.K, bench.E_G = 2, 2      # K e_g <= 8: the second pass re-reads the replicas
-    lars = bench.algorithmic_bytes(n, "lars")
+    lars = bench.algorithmic_bytes(n, "lars", reuse_w_norms=False)
     assert lars["step"] == (4 + 4) * n and lars["second_pass"] == (4 + 16) * n
     bench.K, bench.E_G = 16, 2
 

@@ -251,6 +251,110 @@ def test_resnet18_cifar_lars_two_steps():
     run_steps(lay, 8, 2, mode="lars", check_each=False, label="r18 lars")
 
 
+# ------------------------------- LARS with the weight norms carried over --
+
+
+@pytest.mark.parametrize("name,K,dtype,steps,extra", [
+    ("tiny_cnn", 4, "f32", 3, {}),
+    ("resnet18_cifar", 8, "f32", 3, {}),
+    ("resnet50", 16, "bf16", 3, {}),
+    ("ragged", 5, "bf16", 4, {"small_replica": 2}),
+    ("ragged", 16, "bf16", 4, {"small_replica": -1}),
+    ("ragged", 3, "f32", 4, {})])
+def test_lars_carried_weight_norms_match_oracle(name, K, dtype, steps, extra):
+    """LARS with reuse_w_norms: from the second step on, W_l comes from the
+    sums of w^2 the previous update pass wrote, and every statistic and
+    every element of w and m still match the oracle."""
+    if name == "ragged":
+        flags = [SD, SD, 0, layouts.LAYER_SCALE, layouts.LAYER_DECAY] * 3
+        lay = layouts.custom_layout(RAGGED, flags[:len(RAGGED)], pad=8)
+    else:
+        lay = layouts.get_layout(name)
+    stride = layouts.replica_stride(lay) if name == "resnet50" else None
+    run_steps(lay, K, steps, dtype=dtype, mode="lars", reuse_w_norms=True, stride=stride,
+              label=f"{name} lars carried K={K}", **extra)
+
+
+def test_lars_carried_weight_norms_are_bitwise_those_of_reading_w():
+    """The update pass sums the squares of the new w in the statistics
+    pass's order, so carrying them gives the bits of reading w: steps and
+    interleaved statistics calls with and without reuse_w_norms agree bit for
+    bit (w, m, every statistic)."""
+    import torch
+    lay = layouts.custom_layout(RAGGED, [SD, SD, 0, layouts.LAYER_SCALE, layouts.LAYER_DECAY] * 2
+                                + [SD] * 4, pad=8)
+    grads = [to_device(synth.replica_grads(lay, 16, t, 3, dtype="bf16")) for t in range(5)]
+    w0 = synth.init_weights(lay, 3)
+    torch.cuda.synchronize()
+
+    def run(reuse):
+        w = torch.from_numpy(w0.copy()).cuda()
+        h = ags.AGS(lay.table(), w, torch.zeros_like(w), 16, grad_dtype="bf16", mode="lars",
+                    reuse_w_norms=reuse)
+        recs = []
+        for t, g in enumerate(grads):
+            h.step(g)
+            recs.append(h.read_stats())
+            h.stats(grads[(t + 2) % len(grads)])
+            recs.append(h.read_stats())
+        torch.cuda.synchronize()
+        out = (h.w.cpu().numpy(), h.m.cpu().numpy(), recs)
+        h.close()
+        return out
+
+    a, b = run(False), run(True)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    for ra, rb in zip(a[2], b[2]):
+        for f in ags.LAYER_STATS_FIELDS:
+            assert np.array_equal(ra.layer[f], rb.layer[f]), f
+        assert ra.glob == rb.glob
+
+
+def test_lars_weight_norms_dropped_when_the_caller_writes_w():
+    """A caller that writes w between steps calls ags_invalidate_weight_norms
+    (or restores a state with ags_set_state, which drops them too): the next
+    step reads w again and matches the oracle run on the same new w."""
+    import torch
+    lay = layouts.get_layout("resnet18_cifar")
+    p = Pair(lay, 8, mode="lars", reuse_w_norms=True, seed=4)
+    sig = synth.layer_sigmas(lay, 4)
+    try:
+        t = 0
+
+        def one(what):
+            nonlocal t
+            g = synth.replica_grads(lay, 8, t, 4, sigmas=sig)
+            p.step(g, what=what)
+            p.check_state(what)
+            t += 1
+
+        one("before")
+        one("carried")
+        # an in-place edit of w by the caller (exact in both precisions)
+        p.w.mul_(0.5)
+        p.ora.w *= 0.5
+        torch.cuda.synchronize()
+        p.gpu.invalidate_weight_norms()
+        one("after invalidate")
+        one("carried again")
+        # a checkpoint restore with other weights
+        gs, gp, st = p.gpu.get_state()
+        p.w.mul_(2.0)
+        p.ora.w *= 2.0
+        torch.cuda.synchronize()
+        p.gpu.set_state(gs, gp, st)
+        one("after set_state")
+    finally:
+        p.close()
+    # a handle without carried norms has nothing to drop
+    w = torch.from_numpy(synth.init_weights(lay, 0)).cuda()
+    h = ags.AGS(lay.table(), w, torch.zeros_like(w), 8, mode="lars")
+    with pytest.raises(ags.AGSError) as e:
+        h.invalidate_weight_norms()
+    assert e.value.status == ags.AGS_E_STATE
+    h.close()
+
+
 def test_identical_replicas_zero_variance_exactly():
     lay = layouts.get_layout("tiny_cnn")
     x = synth.replica_grads(lay, 1, 0, 0)
