@@ -308,6 +308,32 @@ ags_status ags_set_elementwise_scale(ags_handle *h, const float *scale, int64_t 
 ags_status ags_set_profiling(ags_handle *h, int enable);
 ags_status ags_get_kernel_times(ags_handle *h, double *out_ms, int64_t *out_calls);
 
+/* For callers that cannot allocate device memory (code that must not call
+ * hipMalloc: tight serving loops, harnesses that forbid allocation): the
+ * statistics of ags_stats without a handle.  It fills out_layers (host
+ * [n_layers]) and out_global (host) with what ags_read_stats returns after
+ * ags_stats on a handle just created by ags_init(cfg, ...): the replica
+ * mean, W_l, G_l, V_l, S_l, rho_l, the global G, and the decision and
+ * coefficients of a first step (no previous norm: Delta and every Delta_l
+ * are +inf, the step is sensitive, gradscale is 1).  d_w: fp32 [n_flat],
+ * read only; d_grads as for ags_stats (m is not read).  Arguments are
+ * checked as by ags_init and ags_stats (AGS_E_ARG, AGS_E_LAYOUT,
+ * AGS_E_ALIGN; the error text is ags_last_error(NULL)).
+ *
+ * It allocates nothing: the layer table, tile map, tile partials, counters
+ * and records live in one device array of 6 MiB inside the library, which
+ * each GPU the library runs on holds until the process ends; a call whose
+ * tables do not fit (about 230 bytes per layer plus 32 per tile of 2048
+ * elements: about 4e8 parameters in up to a few hundred layers) returns
+ * AGS_E_NOMEM before any device work.  Every call on a GPU shares that GPU's
+ * array and leaves its tables there: calls that overlap on one GPU (two
+ * threads, or two streams without ordering between them) race.  The call
+ * enqueues its work on hip_stream, copies the records to the host arrays
+ * and waits for hip_stream before it returns. */
+ags_status ags_stats_noalloc(const ags_config *cfg, const float *d_w, const void *d_grads,
+                             int64_t replica_stride, ags_layer_stats *out_layers,
+                             ags_global_stats *out_global, void *hip_stream);
+
 /* Static text for a status; last error text of a handle (or, with NULL, of
  * the last failed ags_init / ags_workspace_bytes on this thread). */
 const char *ags_status_string(ags_status s);

@@ -76,7 +76,8 @@ EXPORTS = ("ags_workspace_bytes", "ags_init", "ags_stats", "ags_step", "ags_read
            "ags_set_layer_state", "ags_get_last_decision", "ags_set_last_decision",
            "ags_get_elementwise_scale",
            "ags_set_elementwise_scale", "ags_invalidate_weight_norms", "ags_set_profiling",
-           "ags_get_kernel_times", "ags_status_string", "ags_last_error", "ags_destroy")
+           "ags_get_kernel_times", "ags_stats_noalloc", "ags_status_string", "ags_last_error",
+           "ags_destroy")
 
 _lib = None
 
@@ -120,6 +121,7 @@ def load_library(path: str | None = None):
         "ags_get_state": (c_int, [h, vp, P(c_dbl), P(c_i64)]),
         "ags_set_state": (c_int, [h, vp, c_dbl, c_i64]),
         "ags_invalidate_weight_norms": (c_int, [h]),
+        "ags_stats_noalloc": (c_int, [P(ags_config), vp, vp, c_i64, vp, P(ags_global_stats), vp]),
         "ags_get_layer_state": (c_int, [h, vp]),
         "ags_set_layer_state": (c_int, [h, vp]),
         "ags_get_last_decision": (c_int, [h, vp, vp]),
@@ -228,6 +230,21 @@ def ags_set_state(handle, gradscale, g_sq_prev: float, step: int):
         gs = np.ascontiguousarray(gradscale, dtype=np.float64)
         ptr = gs.ctypes.data
     _check(load_library().ags_set_state(handle, ptr, float(g_sq_prev), int(step)), handle)
+
+
+def ags_stats_noalloc(cfg, d_w: int, d_grads: int, replica_stride: int, stream: int = 0):
+    """Statistics of one replica set without a handle and without any device
+    allocation; returns (per-layer dict, global dict) like ags_read_stats."""
+    n = int(cfg.n_layers)
+    arr = (ags_layer_stats * max(n, 1))()
+    g = ags_global_stats()
+    _check(load_library().ags_stats_noalloc(ctypes.byref(cfg), d_w, d_grads, int(replica_stride),
+                                            ctypes.cast(arr, ctypes.c_void_p), ctypes.byref(g),
+                                            stream))
+    layer = {f: np.array([getattr(arr[i], f) for i in range(n)]) for f in LAYER_STATS_FIELDS}
+    glob = {"step": int(g.step), "g_sq": g.g_sq, "g_sq_prev": g.g_sq_prev, "delta": g.delta,
+            "sensitive": int(g.sensitive), "nonfinite": int(g.nonfinite)}
+    return layer, glob
 
 
 def ags_invalidate_weight_norms(handle):

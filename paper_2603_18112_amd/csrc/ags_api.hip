@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -1004,3 +1005,314 @@ void ags_destroy(ags_handle* h) {
 }
 
 }  // extern "C"
+
+// ------------------------------------------------ statistics without allocation --
+//
+// ags_stats_noalloc keeps everything a statistics call needs beyond its
+// inputs and outputs (the layer table, the tile map, tile partials, chunk
+// sums, counters, the initial state and the records) in one file-scope
+// device array, so that it never allocates.  Each GPU holds its own copy of
+// the array until the process ends, found once per device through
+// hipGetSymbolAddress; host code uses only that address, never the array's
+// name.  Every call on a GPU uses the same array, so calls that overlap on
+// one GPU race.
+
+namespace {
+constexpr size_t kScratchBytes = 6u << 20;
+constexpr int kMaxScratchDevices = 64;
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// The address of this GPU's scratch array (the current device), looked up
+// on the first call on the device.
+ags_status scratch_address(int dev, unsigned char** out, std::string& why) {
+    if (dev < 0 || dev >= kMaxScratchDevices) {
+        why = "device index beyond the scratch table";
+        return AGS_E_DEVICE;
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            why = std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e);
+            (void)hipGetLastError();
+            return AGS_E_DEVICE;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *out = static_cast<unsigned char*>(g_scratch_ptr[dev]);
+    return AGS_OK;
+}
+
+// Pieces of the tables a statistics call builds in the scratch array.
+struct NoallocTables {
+    const ags_layer* layers;  // copy of the caller's layer table
+    int n_layers;
+    LayerDev* ldev;
+    Tile* tiles;
+    ags::FinChunk* chunks;
+    DevState* state;
+    double* gradscale;
+    double* g_prev_l;
+    int32_t* last_sens_l;
+    unsigned* chunk_count;
+    unsigned* counters;  // finished-layer counter, correction flag
+};
+
+// One block: every layer's tile and chunk ranges (an exclusive scan of the
+// per-layer counts, with ags_init's tiling: tiles of tile_elems_for(numel)
+// elements, chunks of ags::kFinTilesPerChunk tiles), and the state of a
+// handle that has taken no step (gradscale 1, no previous norms, counters
+// at zero).
+__global__ __launch_bounds__(256) void noalloc_layers_kernel(NoallocTables t) {
+    __shared__ int sh_t[256], sh_c[256];
+    const int tid = threadIdx.x;
+    const int per = (t.n_layers + 255) / 256;
+    const int l0 = min(tid * per, t.n_layers), l1 = min(l0 + per, t.n_layers);
+    int nt = 0, nc = 0;
+    for (int l = l0; l < l1; ++l) {
+        const int64_t n = t.layers[l].numel, te = ags::tile_elems_for(n);
+        const int tl = (int)((n + te - 1) / te);
+        nt += tl;
+        nc += (tl + ags::kFinTilesPerChunk - 1) / ags::kFinTilesPerChunk;
+    }
+    sh_t[tid] = nt;
+    sh_c[tid] = nc;
+    __syncthreads();
+    if (tid == 0) {
+        int rt = 0, rc = 0;
+        for (int i = 0; i < 256; ++i) {
+            const int a = sh_t[i], b = sh_c[i];
+            sh_t[i] = rt;
+            sh_c[i] = rc;
+            rt += a;
+            rc += b;
+        }
+    }
+    __syncthreads();
+    int tb = sh_t[tid], cb = sh_c[tid];
+    for (int l = l0; l < l1; ++l) {
+        const ags_layer ly = t.layers[l];
+        const int64_t te = ags::tile_elems_for(ly.numel);
+        const int tl = (int)((ly.numel + te - 1) / te);
+        const int cl = (tl + ags::kFinTilesPerChunk - 1) / ags::kFinTilesPerChunk;
+        LayerDev d;
+        d.tile_begin = tb;
+        d.tile_end = tb + tl;
+        d.flags = ly.flags;
+        d.chunk_begin = cb;
+        d.chunk_end = cb + cl;
+        d.pad_ = 0;
+        d.numel = ly.numel;
+        t.ldev[l] = d;
+        tb += tl;
+        cb += cl;
+        t.gradscale[l] = 1.0;
+        t.g_prev_l[l] = 0.0;
+        t.last_sens_l[l] = 0;
+        t.chunk_count[l] = 0u;
+    }
+    if (tid == 0) {
+        DevState ds;
+        ds.g_prev = 0.0;
+        ds.step = 0;
+        ds.last_sens = 0;
+        ds.ew_cur = 0;
+        *t.state = ds;
+        t.counters[0] = 0u;
+        t.counters[1] = 0u;
+    }
+}
+
+// One block per layer: its tiles and finalize chunks.
+__global__ __launch_bounds__(256) void noalloc_tiles_kernel(NoallocTables t) {
+    const int l = blockIdx.x;
+    const LayerDev d = t.ldev[l];
+    const ags_layer ly = t.layers[l];
+    const int64_t te = ags::tile_elems_for(ly.numel);
+    for (int i = d.tile_begin + (int)threadIdx.x; i < d.tile_end; i += blockDim.x) {
+        const int64_t o = (int64_t)(i - d.tile_begin) * te;
+        Tile x;
+        x.begin = ly.offset + o;
+        x.count = (int32_t)(ly.numel - o < te ? ly.numel - o : te);
+        x.layer = l;
+        t.tiles[i] = x;
+    }
+    for (int c = d.chunk_begin + (int)threadIdx.x; c < d.chunk_end; c += blockDim.x) {
+        ags::FinChunk ch;
+        ch.layer = l;
+        ch.tile_begin = d.tile_begin + (c - d.chunk_begin) * ags::kFinTilesPerChunk;
+        ch.tile_end = min(ch.tile_begin + ags::kFinTilesPerChunk, d.tile_end);
+        ch.pad_ = 0;
+        t.chunks[c] = ch;
+    }
+}
+
+}  // namespace
+
+extern "C" ags_status ags_stats_noalloc(const ags_config* cfg, const float* d_w, const void* d_grads,
+                                        int64_t replica_stride, ags_layer_stats* out_layers,
+                                        ags_global_stats* out_global, void* hip_stream) {
+    std::string why;
+    auto fail = [&](ags_status st) {
+        g_thread_error = why;
+        return st;
+    };
+    ags_status st = check_config_and_size(cfg, why);
+    if (st != AGS_OK) return fail(st);
+    if (!d_w || !d_grads) {
+        why = "d_w and d_grads must not be NULL";
+        return fail(AGS_E_ARG);
+    }
+    if (!out_layers || !out_global) {
+        why = "out_layers and out_global must not be NULL";
+        return fail(AGS_E_ARG);
+    }
+    if (!aligned16(d_w) || !aligned16(d_grads)) {
+        why = "d_w and d_grads must be 16-byte aligned";
+        return fail(AGS_E_ALIGN);
+    }
+    if (replica_stride < cfg->n_flat) {
+        why = "replica_stride must be >= n_flat";
+        return fail(AGS_E_ARG);
+    }
+    if (replica_stride % AGS_ALIGN_ELEMS != 0) {
+        why = "replica_stride must be a multiple of AGS_ALIGN_ELEMS";
+        return fail(AGS_E_ALIGN);
+    }
+    int64_t extent = 0;
+    for (int32_t l = 0; l < cfg->n_layers; ++l)
+        extent = std::max<int64_t>(extent, cfg->layers[l].offset + cfg->layers[l].numel);
+    const double total = (double)(cfg->K - 1) * (double)replica_stride + (double)extent;
+    if (total * (double)elem_bytes(cfg->grad_dtype) > 9.0e18) {
+        why = "replica_stride too large";
+        return fail(AGS_E_ARG);
+    }
+    const size_t gbytes = ((size_t)(cfg->K - 1) * (size_t)replica_stride + (size_t)extent) *
+                          elem_bytes(cfg->grad_dtype);
+    if (overlap(d_grads, gbytes, d_w, (size_t)extent * sizeof(float))) {
+        why = "d_grads overlaps w";
+        return fail(AGS_E_ARG);
+    }
+    // The scratch array's pieces: the layer table copy, then the workspace
+    // of a statistics call.
+    const int64_t n_tiles = count_tiles(*cfg), n_chunks = count_chunks(*cfg);
+    const size_t lay_bytes = align_up((size_t)cfg->n_layers * sizeof(ags_layer));
+    const WsLayout wl = ws_layout(*cfg, n_tiles, n_chunks, true);
+    if (lay_bytes + wl.end > kScratchBytes) {
+        char buf[240];
+        snprintf(buf, sizeof buf,
+                 "ags_stats_noalloc needs %zu bytes of scratch for %d layers and %lld tiles; the "
+                 "scratch array holds %zu",
+                 lay_bytes + wl.end, cfg->n_layers, (long long)n_tiles, kScratchBytes);
+        why = buf;
+        return fail(AGS_E_NOMEM);
+    }
+    // Device checks (first HIP calls).
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        why = std::string("hipGetDevice: ") + hipGetErrorString(e);
+        (void)hipGetLastError();
+        return fail(AGS_E_DEVICE);
+    }
+    st = check_device_range(d_w, (size_t)extent * sizeof(float), "d_w", why);
+    if (st == AGS_OK) st = check_device_range(d_grads, gbytes, "d_grads", why);
+    if (st != AGS_OK) return fail(st);
+    unsigned char* sp = nullptr;
+    st = scratch_address(dev, &sp, why);
+    if (st != AGS_OK) return fail(st);
+    unsigned char* ws = sp + lay_bytes;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+
+    NoallocTables nt{};
+    nt.layers = reinterpret_cast<const ags_layer*>(sp);
+    nt.n_layers = cfg->n_layers;
+    nt.ldev = reinterpret_cast<LayerDev*>(ws + wl.ldev);
+    nt.tiles = reinterpret_cast<Tile*>(ws + wl.tiles);
+    nt.chunks = reinterpret_cast<ags::FinChunk*>(ws + wl.chunks);
+    nt.state = reinterpret_cast<DevState*>(ws + wl.state);
+    nt.gradscale = reinterpret_cast<double*>(ws + wl.gradscale);
+    nt.g_prev_l = reinterpret_cast<double*>(ws + wl.g_prev_l);
+    nt.last_sens_l = reinterpret_cast<int32_t*>(ws + wl.last_sens_l);
+    nt.chunk_count = reinterpret_cast<unsigned*>(ws + wl.chunk_count);
+    nt.counters = reinterpret_cast<unsigned*>(ws + wl.counters);
+
+    const ags_config& c = *cfg;
+    ags::StepArgs sa{};
+    sa.grads = d_grads;
+    sa.stride = replica_stride;
+    sa.w = const_cast<float*>(d_w);  // read only: the statistics kernel never writes w
+    sa.m = nullptr;
+    sa.gbar = nullptr;
+    sa.tiles = nt.tiles;
+    sa.partials = reinterpret_cast<Partial*>(ws + wl.partials);
+    sa.layers = nt.ldev;
+    sa.n_layers = c.n_layers;
+    sa.K = c.K;
+    sa.invK = (float)(1.0 / (double)c.K);
+    sa.small_replica = c.small_replica;
+    sa.mode = c.mode;
+    sa.commit = 0;
+    sa.refresh_every = c.refresh_every;
+    sa.lr = (float)c.lr;
+    sa.momentum = (float)c.momentum;
+    sa.delta = c.delta;
+    sa.eps = c.eps;
+    sa.s_max = c.s_max;
+    sa.trust_coef = c.trust_coef;
+    sa.static_scale = c.static_scale;
+    sa.weight_decay = c.weight_decay;
+    sa.gradscale = nt.gradscale;
+    sa.state = nt.state;
+    sa.g_prev_l = nt.g_prev_l;
+    sa.last_sens_l = nt.last_sens_l;
+    sa.delta_scope = c.delta_scope;
+    sa.coef = reinterpret_cast<float2*>(ws + wl.coef);
+    sa.corr = reinterpret_cast<float2*>(ws + wl.corr);
+    sa.corr_flag = reinterpret_cast<int*>(nt.counters + 1);
+    sa.updated = 0;
+    sa.xcd_map = n_tiles >= ags::kXcdMapMinTiles ? 1 : 0;
+    sa.done_count = nt.counters;
+    sa.chunks = nt.chunks;
+    sa.chunk_sums = reinterpret_cast<ags::ChunkSum*>(ws + wl.chunk_sums);
+    sa.layer_chunk_count = nt.chunk_count;
+    sa.lstats = reinterpret_cast<ags_layer_stats*>(ws + wl.lstats);
+    sa.gstats = reinterpret_cast<ags_global_stats*>(ws + wl.gstats);
+    sa.ew = 0;
+    sa.ew_buf = nullptr;
+    sa.n_flat = c.n_flat;
+    sa.ew_partials = nullptr;
+    sa.w_norm_in = nullptr;
+
+    e = hipMemcpyAsync(sp, c.layers, (size_t)c.n_layers * sizeof(ags_layer), hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(noalloc_layers_kernel, dim3(1), dim3(256), 0, s, nt);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(noalloc_tiles_kernel, dim3(c.n_layers), dim3(256), 0, s, nt);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess) e = ags::launch_step(sa, c.grad_dtype, (int)n_tiles, false, s, ags::KernelEvents{});
+    if (e == hipSuccess) e = ags::launch_finalize(sa, (int)n_chunks, s, ags::KernelEvents{});
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(out_layers, ws + wl.lstats, (size_t)c.n_layers * sizeof(ags_layer_stats),
+                           hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(out_global, ws + wl.gstats, sizeof(ags_global_stats), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        why = std::string("ags_stats_noalloc: ") + hipGetErrorString(e);
+        (void)hipGetLastError();
+        return fail(AGS_E_DEVICE);
+    }
+    return AGS_OK;
+}

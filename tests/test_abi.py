@@ -240,3 +240,33 @@ def _load_fresh(path):
     finally:
         ags._lib = saved
 
+
+def test_noalloc_stats_rejects_before_any_device_call(lib):
+    """ags_stats_noalloc checks its arguments, and that its tables fit the
+    library's scratch array, on the host before any HIP call."""
+    cfg = ags.make_config(_table(), 136, 4)
+    out_l = (ags.ags_layer_stats * 3)()
+    out_g = ags.ags_global_stats()
+    f = lib.ags_stats_noalloc
+    assert f(ctypes.byref(cfg), None, 0x2000000000, 136, out_l, ctypes.byref(out_g), None) == ags.AGS_E_ARG
+    assert f(ctypes.byref(cfg), 0x1000000000, 0x2000000000, 136, None, ctypes.byref(out_g),
+             None) == ags.AGS_E_ARG
+    assert f(ctypes.byref(cfg), 0x1000000004, 0x2000000000, 136, out_l, ctypes.byref(out_g),
+             None) == ags.AGS_E_ALIGN
+    assert f(ctypes.byref(cfg), 0x1000000000, 0x2000000000, 100, out_l, ctypes.byref(out_g),
+             None) == ags.AGS_E_ARG
+    assert f(ctypes.byref(cfg), 0x1000000000, 0x1000000000, 136, out_l, ctypes.byref(out_g),
+             None) == ags.AGS_E_ARG                        # the replicas overlap w
+    # 5e8 parameters: 244k tiles of 2048 at 32 bytes each, more than the 6 MiB
+    # array holds
+    n = 500_000_000
+    big = ags.make_config([(0, n, 3)], n, 1)
+    st = f(ctypes.byref(big), 0x1000000000, 0x2000000000, n, out_l, ctypes.byref(out_g), None)
+    assert st == ags.AGS_E_NOMEM
+    assert "scratch" in ags.ags_last_error(None)
+    # VGG-16 (138M parameters, 67,569 tiles) fits
+    lay = layouts.get_layout("vgg16")
+    ok = ags.make_config(lay.table(), lay.n_flat, 8)
+    st = f(ctypes.byref(ok), 0x1000000000, 0x1000000000 + 8 * lay.n_flat, lay.n_flat, out_l,
+           ctypes.byref(out_g), None)
+    assert st != ags.AGS_E_NOMEM                           # fails later, at the device checks
