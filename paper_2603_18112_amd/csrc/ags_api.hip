@@ -321,6 +321,9 @@ struct ags_handle {
     // LARS: the last update pass left per-tile sums of w^2 that the next
     // statistics pass may take instead of reading w.
     bool w_norm_valid = false;
+    // Dynamic LDS of the fused step kernel's launches (0: none), capping the
+    // blocks per CU for layouts whose w and m outgrow the Infinity Cache.
+    int lds_pad = 0;
     mutable std::string err;
     bool profiling = false;
     // Per timed step: start and stop event of each kernel's dispatch.
@@ -505,6 +508,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.n_flat = c.n_flat;
     sa.ew_partials = h->ew_partials();
     sa.w_norm_in = (!fused && h->w_norm_valid) ? h->w_norm() : nullptr;
+    sa.lds_pad = ew ? 0 : h->lds_pad;
     hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s, kev(0));
     if (e != hipSuccess) return launch_fail(e, "step kernel launch");
     e = ags::launch_finalize(sa, (int)h->n_chunks, s, kev(1));
@@ -699,6 +703,22 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         g_thread_error = std::string("hipHostMalloc of the staging buffer failed: ") + hipGetErrorString(e);
         free_handle(h);
         return AGS_E_NOMEM;
+    }
+    // Occupancy cap of the fused step kernel: an LDS pad so that at most
+    // ags::kCappedBlocksPerCu blocks fit on a CU (left off if the device
+    // does not report its LDS sizes).
+    if (8 * cfg->n_flat > ags::kOccupancyCapMinBytes) {
+        int lds_cu = 0, lds_block = 0;
+        if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+                hipSuccess ||
+            hipDeviceGetAttribute(&lds_block, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+                hipSuccess) {
+            (void)hipGetLastError();
+            lds_cu = lds_block = 0;
+        }
+        const int pad = lds_cu / (ags::kCappedBlocksPerCu + 1) + 1024;
+        if (lds_cu > 0 && pad + 1024 <= lds_block && ags::kCappedBlocksPerCu * (pad + 1024) <= lds_cu)
+            h->lds_pad = pad;
     }
     e = hipEventCreateWithFlags(&h->order_ev, hipEventDisableTiming);
     if (e != hipSuccess) {

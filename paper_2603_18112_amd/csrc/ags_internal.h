@@ -56,6 +56,21 @@ constexpr int64_t kXcdMapMinTiles = 32768;
 // elements 157.8 / 157.1, 20M 195.7 / 186.2, ResNet-50 (25.6M) 272.2 /
 // 229.6, VGG-16 (138M) 1400 / 1358.
 constexpr int64_t kEwStreamMinBytes = 192ll << 20;
+// Once w and m (8 bytes per element) pass this size they cannot stay in the
+// Infinity Cache between steps, and every step streams them from HBM with
+// the replicas; the fused step kernel then runs best with two blocks per CU
+// (fewer concurrent streams, so fewer DRAM row conflicts), which the host
+// enforces with an LDS pad.  Measured on MI355X, whole step warm / cold,
+// blocks per CU 5 (the kernel's register limit), 4, 3, 2, 1: VGG-16 K = 8
+// fp32 1210 / 1177, 1187 / 1155, 1176 / 1147, 1164 / 1140, 1378 / 1375 us;
+// the layouts whose w and m fit lose from the cap (ResNet-50 K = 16 bf16
+// 193 -> 201 us, ResNet-18 K = 8 fp32 93 -> 100 us at 2 blocks per CU) or
+// barely gain (ResNet-50 K = 64 bf16 634 -> 631 us).
+#ifndef AGS_OCCUPANCY_CAP_MIN_BYTES
+#define AGS_OCCUPANCY_CAP_MIN_BYTES (256ll << 20)
+#endif
+constexpr int64_t kOccupancyCapMinBytes = AGS_OCCUPANCY_CAP_MIN_BYTES;
+constexpr int kCappedBlocksPerCu = 2;
 
 // Elements per tile of a layer of numel elements.
 __host__ __device__ inline int64_t tile_elems_for(int64_t numel) {
@@ -155,6 +170,9 @@ struct StepArgs {
     // LARS: per-tile sums of w^2 written by the last update pass; when set,
     // the statistics-only step kernel takes W from them and skips w.
     const float* w_norm_in;
+    // Bytes of dynamic LDS the fused per-layer-scale step kernel is launched
+    // with (it uses none): a pad that caps the blocks resident per CU.
+    int lds_pad;
 };
 
 struct UpdateArgs {

@@ -328,9 +328,21 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
                 acc(kb + j, v);
             }
         }
+    } else if constexpr (KT > 0) {
+        // The ragged end of a layer (one group per layer at most): one
+        // replica at a time, with the full groups' fp32 sums.  A kernel's
+        // register allocation is the largest any of its paths needs, so
+        // this rare path is kept smaller than the full groups' batches
+        // (it had taken the runtime-K loop's fp64 totals, which raised
+        // e.g. the fp32 K = 8 step kernel from 78 to 114 VGPRs).
+#pragma unroll 1
+        for (int k = 1; k < KT; ++k) {
+            float x[kVec];
+            load_tail<GT, Map<GT>::HS>(g + (int64_t)k * stride + idx, n0, n1, x);
+            acc(k, x);
+        }
     } else {
-        // Runtime K, and the ragged end of a layer (rare; unrolling it
-        // would raise the register count of the whole kernel).  The fp32
+        // Runtime K (full groups and the ragged end of a layer).  The fp32
         // sums of every four replicas are added to fp64 totals: each d_k
         // carries replica 0's own deviation, so one fp32 running sum would
         // drift by k times it and gather a rounding error growing like K
@@ -766,6 +778,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
                                            float& sg, float& sd, float& ss, float& sx) {
     constexpr int HS = Map<GT>::HS;
     constexpr bool NT = EW == 2;
+    constexpr bool ELEM = EW != 0;
     static_assert(!(WNC && UPD), "the update reads w");
     float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
     double q[kVec];
@@ -775,11 +788,11 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
     // barrier the statistics-only variant issued them only after consuming
     // every replica, a second round trip per block.
     if (!UPD) __builtin_amdgcn_sched_barrier(0);
-    constexpr int kb = EW ? RawGroup<GT>::kBatchEw : RawGroup<GT>::kBatch;
-    moments<GT, KT, RMODE, FULL, EW != 0, kb, !UPD>(g, a.stride, idx, n0, n1, K, a.small_replica,
+    constexpr int kb = ELEM ? RawGroup<GT>::kBatchEw : RawGroup<GT>::kBatch;
+    moments<GT, KT, RMODE, FULL, ELEM, kb, !UPD>(g, a.stride, idx, n0, n1, K, a.small_replica,
                                                a.invK, gb, dv, gr, q);
     float gsv[kVec];
-    if (EW) {
+    if (ELEM) {
         // Old scales: applied on scaled layers, carried over on the others.
         if (use_gs || (refresh && !scaled)) {
             load_f32_as<NT, FULL, HS>(gs_old + idx, n0, n1, gsv);
@@ -802,7 +815,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
         // d = a gbar + b w ; m <- mu m + d ; w <- w - eta m
 #pragma unroll
         for (int e = 0; e < kVec; ++e) {
-            const float ae = (EW && use_gs) ? gsv[e] : ca;
+            const float ae = (ELEM && use_gs) ? gsv[e] : ca;
             const float d = fmaf(ae, gb[e], cb * wv[e]);
             mv[e] = fmaf(a.momentum, mv[e], d);
             wv[e] = fmaf(-a.lr, mv[e], wv[e]);
@@ -810,7 +823,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
         store_f32_as<NT, FULL, HS>(a.w + idx, n0, n1, wv);
         store_f32_as<NT, FULL, HS>(a.m + idx, n0, n1, mv);
     }
-    if (EW && refresh) {
+    if (ELEM && refresh) {
         float sn[kVec];
         if (scaled) {
             const double invK = 1.0 / (double)K;
@@ -852,6 +865,7 @@ __device__ __forceinline__ int tile_of_block(int b, int n, int xcd_map) {
 
 template <typename GT, int KT, int RMODE, bool UPD, int EW, bool WNC = false>
 __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
+    constexpr bool ELEM = EW != 0;
     __shared__ float red[5][kTileBlock / 64];
     const int ti = tile_of_block(blockIdx.x, gridDim.x, a.xcd_map);
     const Tile t = a.tiles[ti];
@@ -873,7 +887,7 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
                               ? surely_sensitive(a.g_prev_l[l], step) || a.last_sens_l[l] != 0
                               : surely_sensitive(a.state->g_prev, step) || a.state->last_sens != 0;
         scaled = (f & AGS_LAYER_SCALE) != 0;
-        if (EW) {
+        if (ELEM) {
             // The buffer in force and the refresh, from the device state.
             const int cur = a.state->ew_cur;
             gs_old = a.ew_buf + (size_t)cur * (size_t)a.n_flat;
@@ -881,7 +895,7 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
             refresh = a.refresh_every > 0 && ((step + 1) % a.refresh_every) == 0;
         }
         if (scaled && !pred) {
-            if (EW) use_gs = true;
+            if (ELEM) use_gs = true;
             else if (a.mode == AGS_MODE_AGS) ca = (float)a.gradscale[l];
             else if (a.mode == AGS_MODE_STATIC) ca = (float)a.static_scale;
         }
@@ -901,7 +915,7 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
     sg = wave_sum(sg);
     sd = wave_sum(sd);
     ss = wave_sum(ss);
-    if (EW && refresh) sx = wave_sum(sx);
+    if (ELEM && refresh) sx = wave_sum(sx);
     if (lane == 0) {
         red[0][wid] = sw;
         red[1][wid] = sg;
@@ -917,7 +931,7 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
         p.d = tree_sum<kTileBlock / 64>(red[2]);
         p.s = tree_sum<kTileBlock / 64>(red[3]);
         a.partials[ti] = p;
-        if (EW && refresh) a.ew_partials[ti] = tree_sum<kTileBlock / 64>(red[4]);
+        if (ELEM && refresh) a.ew_partials[ti] = tree_sum<kTileBlock / 64>(red[4]);
     }
 }
 
@@ -1110,15 +1124,17 @@ __global__ __launch_bounds__(kTileBlock) void update_kernel(UpdateArgs a) {
 // One launch of a kernel whose single argument is a, with the dispatch's
 // own start and stop events when timing is on.
 template <typename A>
-hipError_t launch(void (*k)(A), dim3 grid, dim3 block, hipStream_t s, const A& a, KernelEvents ev) {
+hipError_t launch(void (*k)(A), dim3 grid, dim3 block, hipStream_t s, const A& a, KernelEvents ev,
+                  unsigned lds = 0) {
     if (!ev.start && !ev.stop) {
-        hipLaunchKernelGGL(k, grid, block, 0, s, a);
+        hipLaunchKernelGGL(k, grid, block, lds, s, a);
         return hipGetLastError();
     }
     void* args[] = {const_cast<A*>(&a)};
-    return hipExtLaunchKernel(reinterpret_cast<const void*>(k), grid, block, args, 0, s, ev.start,
+    return hipExtLaunchKernel(reinterpret_cast<const void*>(k), grid, block, args, lds, s, ev.start,
                               ev.stop, 0);
 }
+
 
 template <typename GT, int KT, int RMODE>
 hipError_t step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s, KernelEvents ev) {
@@ -1128,7 +1144,7 @@ hipError_t step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s, Ke
     if (!update) return launch(step_kernel<GT, KT, RMODE, false, 0>, grid, block, s, a, ev);
     if (a.ew == 2) return launch(step_kernel<GT, KT, RMODE, true, 2>, grid, block, s, a, ev);
     if (a.ew) return launch(step_kernel<GT, KT, RMODE, true, 1>, grid, block, s, a, ev);
-    return launch(step_kernel<GT, KT, RMODE, true, 0>, grid, block, s, a, ev);
+    return launch(step_kernel<GT, KT, RMODE, true, 0>, grid, block, s, a, ev, (unsigned)a.lds_pad);
 }
 
 template <typename GT, int KT>

@@ -15,6 +15,10 @@
 //         Infinity Cache).
 //         With "ew", the pattern of elementwise AGS: also the element scale
 //         in force read and the refreshed one written (8 more bytes).
+//         Both are timed with every number of blocks per CU from the
+//         register limit down to 2 (a dynamic LDS pad caps it), and the
+//         fastest counts: how many streams run at once decides how well
+//         the DRAM rows are used.
 // Usage: hbm_probe [K grad_dtype(bf16|f32) n_elements [ew]]; without
 // arguments the step pattern is the ResNet-50 layout's (K = 16, bf16,
 // 25,557,032).
@@ -187,11 +191,12 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
     *reinterpret_cast<float4*>(m + i1) = m1;
 }
 
-// Launch of the step pattern: element scales or not (ew: 0, 1 or 2).
+// Launch of the step pattern: element scales or not (ew: 0, 1 or 2), with
+// lds bytes of dynamic LDS (unused, a cap on the blocks per CU).
 void launch_step_pattern(bool bf16, int ew, int grid, const void* g, size_t stride, int K, float* w,
-                         float* m, const float* sc_in, float* sc_out) {
+                         float* m, const float* sc_in, float* sc_out, unsigned lds) {
 #define PROBE_LAUNCH(B, E) \
-    hipLaunchKernelGGL((probe_step<B, E>), dim3(grid), dim3(256), 0, 0, g, stride, K, w, m, sc_in, sc_out)
+    hipLaunchKernelGGL((probe_step<B, E>), dim3(grid), dim3(256), lds, 0, g, stride, K, w, m, sc_in, sc_out)
     if (bf16) {
         if (ew == 0) PROBE_LAUNCH(true, 0);
         else if (ew == 1) PROBE_LAUNCH(true, 1);
@@ -313,19 +318,37 @@ int main(int argc, char** argv) {
     float* sc_out = sc ? sc + ne + sc_gap : nullptr;
     CHECK(hipDeviceSynchronize());
     const int grid = (int)(ne / kTile);
+    // LDS pads that leave at most 4, 3 or 2 blocks on a CU (0: no cap).
+    int lds_cu = 0, lds_block = 0;
+    CHECK(hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, 0));
+    CHECK(hipDeviceGetAttribute(&lds_block, hipDeviceAttributeMaxSharedMemoryPerBlock, 0));
+    unsigned pads[4] = {0, 0, 0, 0};
+    int caps[4] = {0, 4, 3, 2};
+    int n_pads = 1;
+    for (int c = 4; c >= 2; --c) {
+        const int pad = lds_cu / (c + 1) + 1024;
+        if (lds_cu > 0 && pad + 1024 <= lds_block && c * (pad + 1024) <= lds_cu) {
+            pads[n_pads] = (unsigned)pad;
+            caps[n_pads] = c;
+            ++n_pads;
+        }
+    }
     // With element scales, the faster of ordinary and streaming accesses for
     // the scale streams (and the w and m stores) is the pattern's rate.
-    int best_ew = ew ? 1 : 0;
+    int best_ew = ew ? 1 : 0, best_pad = 0;
     double step_us = 0;
     for (int v = ew ? 1 : 0; v <= (ew ? 2 : 0); ++v) {
-        double us = 0;
-        const int rc = time_launches(
-            [&]() { launch_step_pattern(bf16, v, grid, g, stride, K, w, m, sc_in, sc_out); }, 50,
-            e0, e1, &us);
-        if (rc) return rc;
-        if (step_us == 0 || us < step_us) {
-            step_us = us;
-            best_ew = v;
+        for (int pi = 0; pi < n_pads; ++pi) {
+            double us = 0;
+            const int rc = time_launches(
+                [&]() { launch_step_pattern(bf16, v, grid, g, stride, K, w, m, sc_in, sc_out, pads[pi]); },
+                50, e0, e1, &us);
+            if (rc) return rc;
+            if (step_us == 0 || us < step_us) {
+                step_us = us;
+                best_ew = v;
+                best_pad = pi;
+            }
         }
     }
     // The same pattern cold: each launch timed on its own after a 1 GiB read
@@ -336,34 +359,45 @@ int main(int argc, char** argv) {
     if (fill(evict, evict_bytes, 6u, 1)) return 1;
     CHECK(hipDeviceSynchronize());
     constexpr int kCold = 21;
-    float cold_ms[kCold];
-    for (int r = 0; r < kCold; ++r) {
-        hipLaunchKernelGGL(evict_read, dim3(2048), dim3(256), 0, 0, evict, evict_bytes / 16, out);
-        CHECK(hipEventRecord(e0));
-        launch_step_pattern(bf16, best_ew, grid, g, stride, K, w, m, sc_in, sc_out);
-        CHECK(hipEventRecord(e1));
-        CHECK(hipEventSynchronize(e1));
-        CHECK(hipGetLastError());
-        CHECK(hipEventElapsedTime(&cold_ms[r], e0, e1));
-    }
-    for (int i = 1; i < kCold; ++i)  // insertion sort, then the median
-        for (int j = i; j > 0 && cold_ms[j] < cold_ms[j - 1]; --j) {
-            const float t = cold_ms[j];
-            cold_ms[j] = cold_ms[j - 1];
-            cold_ms[j - 1] = t;
+    double cold_us = 0;
+    int best_cold_pad = 0;
+    for (int pi = 0; pi < n_pads; ++pi) {
+        float cold_ms[kCold];
+        for (int r = 0; r < kCold; ++r) {
+            hipLaunchKernelGGL(evict_read, dim3(2048), dim3(256), 0, 0, evict, evict_bytes / 16, out);
+            CHECK(hipEventRecord(e0));
+            launch_step_pattern(bf16, best_ew, grid, g, stride, K, w, m, sc_in, sc_out, pads[pi]);
+            CHECK(hipEventRecord(e1));
+            CHECK(hipEventSynchronize(e1));
+            CHECK(hipGetLastError());
+            CHECK(hipEventElapsedTime(&cold_ms[r], e0, e1));
         }
-    const double cold_us = cold_ms[kCold / 2] * 1e3;
+        for (int i = 1; i < kCold; ++i)  // insertion sort, then the median
+            for (int j = i; j > 0 && cold_ms[j] < cold_ms[j - 1]; --j) {
+                const float t = cold_ms[j];
+                cold_ms[j] = cold_ms[j - 1];
+                cold_ms[j - 1] = t;
+            }
+        const double us = cold_ms[kCold / 2] * 1e3;
+        if (cold_us == 0 || us < cold_us) {
+            cold_us = us;
+            best_cold_pad = pi;
+        }
+    }
     CHECK(hipFree(evict));
     const size_t bpe = (size_t)K * es + 16 + (ew ? 8 : 0);
     const double step_bytes = (double)ne * (double)bpe;
     printf("{\"read_GBps\": %.1f, \"read_grid\": %d, \"copy_GBps\": %.1f, \"copy_grid\": %d, "
            "\"step_pattern_GBps\": %.1f, \"step_pattern_us\": %.2f, "
-           "\"step_pattern_cold_GBps\": %.1f, \"step_pattern_cold_us\": %.2f, \"step_pattern\": "
+           "\"step_pattern_cold_GBps\": %.1f, \"step_pattern_cold_us\": %.2f, "
+           "\"step_pattern_blocks_per_cu\": %d, \"step_pattern_cold_blocks_per_cu\": %d, "
+           "\"step_pattern\": "
            "{\"K\": %d, \"grad_dtype\": \"%s\", \"elements\": %zu, \"bytes_per_element\": %zu, "
            "\"element_scales\": %s}, "
            "\"bytes\": %zu, \"data\": \"random\"}\n",
            best[0], best_grid[0], best[1], best_grid[1], step_bytes / (step_us * 1e-6) / 1e9, step_us,
-           step_bytes / (cold_us * 1e-6) / 1e9, cold_us, K, bf16 ? "bf16" : "f32", ne, bpe,
+           step_bytes / (cold_us * 1e-6) / 1e9, cold_us, caps[best_pad], caps[best_cold_pad], K,
+           bf16 ? "bf16" : "f32", ne, bpe,
            !ew ? "null" : (best_ew == 2 ? "\"streaming\"" : "\"ordinary\""), bytes);
     if (sc) CHECK(hipFree(sc));
     CHECK(hipFree(g));
