@@ -263,6 +263,15 @@ template <> struct RawGroup<float> {
 // practice, for fp32 ones), from which an element scale's denominator
 // gbar + eps is formed without the cancellation of the fp32 sums.
 
+#ifndef AGS_PIPELINE
+#define AGS_PIPELINE 1
+#endif
+#ifndef AGS_STATS_SPLIT
+#define AGS_STATS_SPLIT 1
+#endif
+#ifndef AGS_STATS_WBARRIER
+#define AGS_STATS_WBARRIER 1
+#endif
 // SPLIT: keep each later batch in its packed form until the batch before
 // it is summed (a scheduling barrier after the batch's loads).  Without it
 // the statistics-only step kernel widened all K = 16 bf16 replicas as they
@@ -298,7 +307,55 @@ __device__ __forceinline__ void moments(const GT* __restrict__ g, int64_t stride
             if (EX) q[e] += (double)x[e];
         }
     };
-    if constexpr (KT > 0 && FULL) {
+    // bf16 replicas, K >= 16, no fp64 sums: two batches in registers (of 4
+    // replicas for K = 16, of 8 above), the next batch's loads in flight
+    // while the current one is summed, in the same replica order (so the
+    // same bits).  Measured on MI355X against one batch of 8 at a time:
+    // ResNet-50 K = 16 step 192.4 / 216.3 -> 192.0 / 213.0 us warm / cold,
+    // K = 32 343.7 -> 339.0, K = 64 637.4 -> 631.6, LARS K = 64 678.5 ->
+    // 671.5 us.
+    constexpr int PB = (sizeof(GT) == 2 && !EX && AGS_PIPELINE) ? (KT >= 32 ? 8 : 4) : 0;
+    if constexpr (KT >= 16 && FULL && PB > 0) {
+        constexpr int KB = PB;
+        static_assert(KT % (2 * KB) == 0, "K must be a multiple of two batches");
+        RawGroup<GT> a[KB], b[KB];
+#pragma unroll
+        for (int j = 1; j < KB; ++j) a[j].load(g + (int64_t)j * stride + idx);
+#pragma unroll
+        for (int j = 0; j < KB; ++j) b[j].load(g + (int64_t)(KB + j) * stride + idx);
+#pragma unroll
+        for (int j = 1; j < KB; ++j) {
+            float v[kVec];
+            a[j].widen(v);
+            acc(j, v);
+        }
+#pragma unroll 1
+        for (int kb = KB; kb < KT; kb += 2 * KB) {
+            // b holds replicas [kb, kb + KB); a takes the next batch, if any
+            const bool more = kb + KB < KT;
+            if (more) {
+#pragma unroll
+                for (int j = 0; j < KB; ++j) a[j].load(g + (int64_t)(kb + KB + j) * stride + idx);
+            }
+#pragma unroll
+            for (int j = 0; j < KB; ++j) {
+                float v[kVec];
+                b[j].widen(v);
+                acc(kb + j, v);
+            }
+            if (!more) break;
+            if (kb + 2 * KB < KT) {
+#pragma unroll
+                for (int j = 0; j < KB; ++j) b[j].load(g + (int64_t)(kb + 2 * KB + j) * stride + idx);
+            }
+#pragma unroll
+            for (int j = 0; j < KB; ++j) {
+                float v[kVec];
+                a[j].widen(v);
+                acc(kb + KB + j, v);
+            }
+        }
+    } else if constexpr (KT > 0 && FULL) {
         // Every load of a batch is issued before any of its values is used.
         // The first batch holds replicas 1..KB-1 (replica 0 is the shift);
         // later batches run as a loop, one batch in registers at a time.
@@ -768,8 +825,12 @@ __device__ __forceinline__ float element_scale(float gsmall, double q, double in
 // element scales with non-temporal scale loads and scale, w and m stores
 // (the host's choice for working sets the Infinity Cache cannot keep).
 // WNC (statistics only): W of the tile comes from the last LARS update
-// pass, so w is not read.
-template <typename GT, int KT, int RMODE, bool UPD, int EW, bool FULL, bool WNC = false>
+// pass, so w is not read.  GB (statistics only): store the replica mean
+// for the LARS update pass.  A compile-time choice: testing the pointer at
+// run time had made the K = 16 bf16 statistics kernel keep 183 VGPRs (two
+// waves per SIMD) against 95 with the store unconditional.
+template <typename GT, int KT, int RMODE, bool UPD, int EW, bool FULL, bool WNC = false,
+          bool GB = false>
 __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restrict__ g,
                                            int64_t idx, int n0, int n1, int K, float ca,
                                            float cb, bool use_gs, bool scaled, bool refresh,
@@ -780,6 +841,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
     constexpr bool NT = EW == 2;
     constexpr bool ELEM = EW != 0;
     static_assert(!(WNC && UPD), "the update reads w");
+    static_assert(!(GB && UPD), "the fused update keeps the mean in registers");
     float wv[kVec], mv[kVec], gb[kVec], dv[kVec], gr[kVec];
     double q[kVec];
     if (!WNC) load_f32<FULL, HS>(a.w + idx, n0, n1, wv);
@@ -787,9 +849,9 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
     // Keep the w (and m) loads in front of the replica loads: without the
     // barrier the statistics-only variant issued them only after consuming
     // every replica, a second round trip per block.
-    if (!UPD) __builtin_amdgcn_sched_barrier(0);
+    if (!UPD && AGS_STATS_WBARRIER) __builtin_amdgcn_sched_barrier(0);
     constexpr int kb = ELEM ? RawGroup<GT>::kBatchEw : RawGroup<GT>::kBatch;
-    moments<GT, KT, RMODE, FULL, ELEM, kb, !UPD>(g, a.stride, idx, n0, n1, K, a.small_replica,
+    moments<GT, KT, RMODE, FULL, ELEM, kb, !UPD && AGS_STATS_SPLIT>(g, a.stride, idx, n0, n1, K, a.small_replica,
                                                a.invK, gb, dv, gr, q);
     float gsv[kVec];
     if (ELEM) {
@@ -801,7 +863,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
             for (int e = 0; e < kVec; ++e) gsv[e] = 1.0f;
         }
     }
-    if (!UPD && a.gbar) store_f32<FULL, HS>(a.gbar + idx, n0, n1, gb);
+    if (GB) store_f32<FULL, HS>(a.gbar + idx, n0, n1, gb);
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
         if (!WNC) sw = fmaf(wv[e], wv[e], sw);
@@ -863,7 +925,7 @@ __device__ __forceinline__ int tile_of_block(int b, int n, int xcd_map) {
     return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
 }
 
-template <typename GT, int KT, int RMODE, bool UPD, int EW, bool WNC = false>
+template <typename GT, int KT, int RMODE, bool UPD, int EW, bool WNC = false, bool GB = false>
 __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
     constexpr bool ELEM = EW != 0;
     __shared__ float red[5][kTileBlock / 64];
@@ -905,7 +967,7 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
 
     float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f, sx = 0.0f;
     for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
-        step_group<GT, KT, RMODE, UPD, EW, decltype(full)::value, WNC>(
+        step_group<GT, KT, RMODE, UPD, EW, decltype(full)::value, WNC, GB>(
             a, g, idx, n0, n1, K, ca, cb, use_gs, scaled, refresh, gs_old, gs_new, smax, sw, sg, sd,
             ss, sx);
     });
@@ -1139,9 +1201,13 @@ hipError_t launch(void (*k)(A), dim3 grid, dim3 block, hipStream_t s, const A& a
 template <typename GT, int KT, int RMODE>
 hipError_t step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s, KernelEvents ev) {
     const dim3 grid(n_tiles), block(kTileBlock);
-    if (!update && a.w_norm_in)
-        return launch(step_kernel<GT, KT, RMODE, false, 0, true>, grid, block, s, a, ev);
-    if (!update) return launch(step_kernel<GT, KT, RMODE, false, 0>, grid, block, s, a, ev);
+    if (!update) {
+        if (a.gbar && a.w_norm_in)
+            return launch(step_kernel<GT, KT, RMODE, false, 0, true, true>, grid, block, s, a, ev);
+        if (a.gbar) return launch(step_kernel<GT, KT, RMODE, false, 0, false, true>, grid, block, s, a, ev);
+        if (a.w_norm_in) return launch(step_kernel<GT, KT, RMODE, false, 0, true>, grid, block, s, a, ev);
+        return launch(step_kernel<GT, KT, RMODE, false, 0>, grid, block, s, a, ev);
+    }
     if (a.ew == 2) return launch(step_kernel<GT, KT, RMODE, true, 2>, grid, block, s, a, ev);
     if (a.ew) return launch(step_kernel<GT, KT, RMODE, true, 1>, grid, block, s, a, ev);
     return launch(step_kernel<GT, KT, RMODE, true, 0>, grid, block, s, a, ev, (unsigned)a.lds_pad);
