@@ -68,7 +68,7 @@ def test_libags_host_code_under_asan_and_ubsan(tmp_path):
     if not (os.path.exists(HIPCC) and rts):
         pytest.skip("hipcc or the clang sanitizer runtime not available")
     lib = str(tmp_path / "libags_san_host.so")
-    cmd = [HIPCC, "--offload-arch=gfx950", "--offload-host-only", "-O1", "-g", "-std=c++17",
+    cmd = [HIPCC, "--offload-arch=gfx950", "-O1", "-g", "-std=c++17",
            "-fPIC", "-shared", "-shared-libasan",
            "-Xarch_host", "-fsanitize=address",
            "-Xarch_host", "-fsanitize=undefined",
