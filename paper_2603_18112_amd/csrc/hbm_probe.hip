@@ -16,9 +16,12 @@
 //         With "ew", the pattern of elementwise AGS: also the element scale
 //         in force read and the refreshed one written (8 more bytes).
 //         Both are timed with every number of blocks per CU from the
-//         register limit down to 2 (a dynamic LDS pad caps it), and the
-//         fastest counts: how many streams run at once decides how well
-//         the DRAM rows are used.
+//         register limit down to 2 (a dynamic LDS pad caps it), in both
+//         tile orders the step kernel uses (round-robin over the XCDs, and
+//         a contiguous range per XCD) and with load batches of 8 and 16
+//         (bf16 rows, or fp32 half rows), and the fastest counts: how many
+//         streams run at once, and where, decides how well the DRAM rows
+//         are used.
 // Usage: hbm_probe [K grad_dtype(bf16|f32) n_elements [ew]]; without
 // arguments the step pattern is the ResNet-50 layout's (K = 16, bf16,
 // 25,557,032).
@@ -98,20 +101,28 @@ __device__ __forceinline__ void add_bf16x8(const u32x4& v, float (&s)[8]) {
 // One block per tile of kTile elements; lane l of wave v owns, for bf16
 // rows, elements [512v + 8l, +8) (one 16-byte load per row), for fp32 rows
 // [512v + 4l, +4) and [512v + 256 + 4l, +4) (two 16-byte loads per row).
-// Rows are loaded in batches of B before any is used.  w and m: the same
+// Rows are loaded in batches of B (bf16: B rows; fp32: B / 2 rows, two
+// loads each) before any is used.  With xcd, block b
+// takes the tile that the step kernel's XCD-aware order gives it (each of
+// the 8 XCDs, which receive every 8th block, walks a contiguous range of
+// tiles) instead of tile b.  w and m: the same
 // elements, fp32, read and written.  EW (element scales): one more fp32
 // stream read (sc_in) and one written (sc_out) for the same elements, with
 // ordinary accesses (EW = 1) or streaming ones, w and m stores included
 // (EW = 2).  n is a multiple of kTile.
-template <bool BF16, int EW>
+template <bool BF16, int EW, int B>
 __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads, size_t stride,
                                                   int K, float* __restrict__ w,
                                                   float* __restrict__ m,
                                                   const float* __restrict__ sc_in,
-                                                  float* __restrict__ sc_out) {
-    constexpr int B = 8;
+                                                  float* __restrict__ sc_out, int xcd) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const size_t base = (size_t)blockIdx.x * kTile + (size_t)wave * 512;
+    int tile = blockIdx.x;
+    if (xcd) {
+        const int n = gridDim.x, q = n / 8, r = n % 8, x = tile % 8, i = tile / 8;
+        tile = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
+    }
+    const size_t base = (size_t)tile * kTile + (size_t)wave * 512;
     const size_t i0 = base + (BF16 ? 8 * lane : 4 * lane);
     const size_t i1 = BF16 ? i0 + 4 : i0 + 256;
     float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -192,11 +203,20 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
 }
 
 // Launch of the step pattern: element scales or not (ew: 0, 1 or 2), with
-// lds bytes of dynamic LDS (unused, a cap on the blocks per CU).
+// lds bytes of dynamic LDS (unused, a cap on the blocks per CU), in the
+// XCD-aware tile order or not, with load batches of 8 or (deep) 16.
 void launch_step_pattern(bool bf16, int ew, int grid, const void* g, size_t stride, int K, float* w,
-                         float* m, const float* sc_in, float* sc_out, unsigned lds) {
-#define PROBE_LAUNCH(B, E) \
-    hipLaunchKernelGGL((probe_step<B, E>), dim3(grid), dim3(256), lds, 0, g, stride, K, w, m, sc_in, sc_out)
+                         float* m, const float* sc_in, float* sc_out, unsigned lds, int xcd,
+                         int deep) {
+#define PROBE_LAUNCH(BF, E)                                                                      \
+    do {                                                                                         \
+        if (deep)                                                                                \
+            hipLaunchKernelGGL((probe_step<BF, E, 16>), dim3(grid), dim3(256), lds, 0, g, stride, K, \
+                               w, m, sc_in, sc_out, xcd);                                        \
+        else                                                                                     \
+            hipLaunchKernelGGL((probe_step<BF, E, 8>), dim3(grid), dim3(256), lds, 0, g, stride, K,  \
+                               w, m, sc_in, sc_out, xcd);                                        \
+    } while (0)
     if (bf16) {
         if (ew == 0) PROBE_LAUNCH(true, 0);
         else if (ew == 1) PROBE_LAUNCH(true, 1);
@@ -335,19 +355,25 @@ int main(int argc, char** argv) {
     }
     // With element scales, the faster of ordinary and streaming accesses for
     // the scale streams (and the w and m stores) is the pattern's rate.
-    int best_ew = ew ? 1 : 0, best_pad = 0;
+    int best_ew = ew ? 1 : 0, best_pad = 0, best_xcd = 0, best_deep = 0;
     double step_us = 0;
     for (int v = ew ? 1 : 0; v <= (ew ? 2 : 0); ++v) {
-        for (int pi = 0; pi < n_pads; ++pi) {
+        for (int c = 0; c < 4 * n_pads; ++c) {
+            const int pi = c % n_pads, xcd = (c / n_pads) & 1, deep = c / (2 * n_pads);
             double us = 0;
             const int rc = time_launches(
-                [&]() { launch_step_pattern(bf16, v, grid, g, stride, K, w, m, sc_in, sc_out, pads[pi]); },
+                [&]() {
+                    launch_step_pattern(bf16, v, grid, g, stride, K, w, m, sc_in, sc_out, pads[pi], xcd,
+                                        deep);
+                },
                 50, e0, e1, &us);
             if (rc) return rc;
             if (step_us == 0 || us < step_us) {
                 step_us = us;
                 best_ew = v;
                 best_pad = pi;
+                best_xcd = xcd;
+                best_deep = deep;
             }
         }
     }
@@ -360,13 +386,14 @@ int main(int argc, char** argv) {
     CHECK(hipDeviceSynchronize());
     constexpr int kCold = 21;
     double cold_us = 0;
-    int best_cold_pad = 0;
-    for (int pi = 0; pi < n_pads; ++pi) {
+    int best_cold_pad = 0, best_cold_xcd = 0, best_cold_deep = 0;
+    for (int ci = 0; ci < 4 * n_pads; ++ci) {
+        const int pi = ci % n_pads, xcd = (ci / n_pads) & 1, deep = ci / (2 * n_pads);
         float cold_ms[kCold];
         for (int r = 0; r < kCold; ++r) {
             hipLaunchKernelGGL(evict_read, dim3(2048), dim3(256), 0, 0, evict, evict_bytes / 16, out);
             CHECK(hipEventRecord(e0));
-            launch_step_pattern(bf16, best_ew, grid, g, stride, K, w, m, sc_in, sc_out, pads[pi]);
+            launch_step_pattern(bf16, best_ew, grid, g, stride, K, w, m, sc_in, sc_out, pads[pi], xcd, deep);
             CHECK(hipEventRecord(e1));
             CHECK(hipEventSynchronize(e1));
             CHECK(hipGetLastError());
@@ -382,6 +409,8 @@ int main(int argc, char** argv) {
         if (cold_us == 0 || us < cold_us) {
             cold_us = us;
             best_cold_pad = pi;
+            best_cold_xcd = xcd;
+            best_cold_deep = deep;
         }
     }
     CHECK(hipFree(evict));
@@ -391,12 +420,16 @@ int main(int argc, char** argv) {
            "\"step_pattern_GBps\": %.1f, \"step_pattern_us\": %.2f, "
            "\"step_pattern_cold_GBps\": %.1f, \"step_pattern_cold_us\": %.2f, "
            "\"step_pattern_blocks_per_cu\": %d, \"step_pattern_cold_blocks_per_cu\": %d, "
+           "\"step_pattern_xcd_order\": %s, \"step_pattern_cold_xcd_order\": %s, "
+           "\"step_pattern_load_batch\": %d, \"step_pattern_cold_load_batch\": %d, "
            "\"step_pattern\": "
            "{\"K\": %d, \"grad_dtype\": \"%s\", \"elements\": %zu, \"bytes_per_element\": %zu, "
            "\"element_scales\": %s}, "
            "\"bytes\": %zu, \"data\": \"random\"}\n",
            best[0], best_grid[0], best[1], best_grid[1], step_bytes / (step_us * 1e-6) / 1e9, step_us,
-           step_bytes / (cold_us * 1e-6) / 1e9, cold_us, caps[best_pad], caps[best_cold_pad], K,
+           step_bytes / (cold_us * 1e-6) / 1e9, cold_us, caps[best_pad], caps[best_cold_pad],
+           best_xcd ? "true" : "false", best_cold_xcd ? "true" : "false", best_deep ? 16 : 8,
+           best_cold_deep ? 16 : 8, K,
            bf16 ? "bf16" : "f32", ne, bpe,
            !ew ? "null" : (best_ew == 2 ? "\"streaming\"" : "\"ordinary\""), bytes);
     if (sc) CHECK(hipFree(sc));
