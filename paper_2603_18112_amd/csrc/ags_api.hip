@@ -321,9 +321,10 @@ struct ags_handle {
     // LARS: the last update pass left per-tile sums of w^2 that the next
     // statistics pass may take instead of reading w.
     bool w_norm_valid = false;
-    // Dynamic LDS of the fused step kernel's launches (0: none), capping the
+    // Dynamic LDS of the fused step kernel's launches, of the statistics-only
+    // step kernel's and of the LARS update kernel's (0: none), capping the
     // blocks per CU for layouts whose w and m outgrow the Infinity Cache.
-    int lds_pad = 0;
+    int lds_pad = 0, lds_pad_stats = 0, lds_pad_update = 0;
     mutable std::string err;
     bool profiling = false;
     // Per timed step: start and stop event of each kernel's dispatch.
@@ -508,7 +509,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.n_flat = c.n_flat;
     sa.ew_partials = h->ew_partials();
     sa.w_norm_in = (!fused && h->w_norm_valid) ? h->w_norm() : nullptr;
-    sa.lds_pad = ew ? 0 : h->lds_pad;
+    sa.lds_pad = ew ? 0 : (fused ? h->lds_pad : h->lds_pad_stats);
     hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s, kev(0));
     if (e != hipSuccess) return launch_fail(e, "step kernel launch");
     e = ags::launch_finalize(sa, (int)h->n_chunks, s, kev(1));
@@ -535,6 +536,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         ua.lr = (float)h->lr;
         ua.momentum = (float)c.momentum;
         ua.w_norm_out = (c.mode == AGS_MODE_LARS) ? h->w_norm() : nullptr;
+        ua.lds_pad = h->lds_pad_update;
         e = (c.mode == AGS_MODE_LARS) ? ags::launch_update(ua, c.grad_dtype, s, kev(2))
                                       : ags::launch_correct(ua, c.grad_dtype, s, kev(2));
         if (e != hipSuccess) return launch_fail(e, "second-pass kernel launch");
@@ -704,9 +706,10 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         free_handle(h);
         return AGS_E_NOMEM;
     }
-    // Occupancy cap of the fused step kernel: an LDS pad so that at most
-    // ags::kCappedBlocksPerCu blocks fit on a CU (left off if the device
-    // does not report its LDS sizes).
+    // Occupancy caps of the fused step kernel, the statistics-only step
+    // kernel and the LARS update kernel: LDS pads so that at most the given
+    // number of blocks fit on a CU (left off if the device does not report
+    // its LDS sizes).  The kernels use at most 1 KiB of static LDS.
     if (8 * cfg->n_flat > ags::kOccupancyCapMinBytes) {
         int lds_cu = 0, lds_block = 0;
         if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
@@ -716,9 +719,13 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
             (void)hipGetLastError();
             lds_cu = lds_block = 0;
         }
-        const int pad = lds_cu / (ags::kCappedBlocksPerCu + 1) + 1024;
-        if (lds_cu > 0 && pad + 1024 <= lds_block && ags::kCappedBlocksPerCu * (pad + 1024) <= lds_cu)
-            h->lds_pad = pad;
+        auto pad_for = [&](int blocks) {
+            const int pad = lds_cu / (blocks + 1) + 1024;
+            return lds_cu > 0 && pad + 1024 <= lds_block && blocks * (pad + 1024) <= lds_cu ? pad : 0;
+        };
+        h->lds_pad = pad_for(ags::kCappedBlocksPerCu);
+        h->lds_pad_stats = pad_for(ags::kCappedBlocksPerCuStats);
+        h->lds_pad_update = pad_for(ags::kCappedBlocksPerCuUpdate);
     }
     e = hipEventCreateWithFlags(&h->order_ev, hipEventDisableTiming);
     if (e != hipSuccess) {

@@ -65,12 +65,18 @@ constexpr int64_t kEwStreamMinBytes = 192ll << 20;
 // fp32 1210 / 1177, 1187 / 1155, 1176 / 1147, 1164 / 1140, 1378 / 1375 us;
 // the layouts whose w and m fit lose from the cap (ResNet-50 K = 16 bf16
 // 193 -> 201 us, ResNet-18 K = 8 fp32 93 -> 100 us at 2 blocks per CU) or
-// barely gain (ResNet-50 K = 64 bf16 634 -> 631 us).
+// barely gain (ResNet-50 K = 64 bf16 634 -> 631 us).  LARS's two passes on
+// the same layouts: the statistics-only step kernel runs best with three
+// blocks per CU (VGG-16 K = 8 fp32: 936 us uncapped, 901 at 3, 916 at 2),
+// the update kernel with two (525 -> 484 us); the whole LARS step 1471 ->
+// 1381 us.  ResNet-50's first pass loses from a cap (154 -> 160 us at 2).
 #ifndef AGS_OCCUPANCY_CAP_MIN_BYTES
 #define AGS_OCCUPANCY_CAP_MIN_BYTES (256ll << 20)
 #endif
 constexpr int64_t kOccupancyCapMinBytes = AGS_OCCUPANCY_CAP_MIN_BYTES;
 constexpr int kCappedBlocksPerCu = 2;
+constexpr int kCappedBlocksPerCuStats = 3;
+constexpr int kCappedBlocksPerCuUpdate = 2;
 
 // Elements per tile of a layer of numel elements.
 __host__ __device__ inline int64_t tile_elems_for(int64_t numel) {
@@ -170,8 +176,9 @@ struct StepArgs {
     // LARS: per-tile sums of w^2 written by the last update pass; when set,
     // the statistics-only step kernel takes W from them and skips w.
     const float* w_norm_in;
-    // Bytes of dynamic LDS the fused per-layer-scale step kernel is launched
-    // with (it uses none): a pad that caps the blocks resident per CU.
+    // Bytes of dynamic LDS the step kernel is launched with (it uses none):
+    // a pad that caps the blocks resident per CU.  Taken by the fused
+    // per-layer-scale variant and the statistics-only ones.
     int lds_pad;
 };
 
@@ -197,6 +204,9 @@ struct UpdateArgs {
     // LARS update: per-tile sums of the new w^2, summed as the statistics
     // pass sums w^2 (or nullptr).
     float* w_norm_out;
+    // Dynamic LDS of the LARS update launch (0: none), a cap on its blocks
+    // per CU.
+    int lds_pad;
 };
 
 // Text for ags_last_error(NULL) on this thread (ags_api.hip).

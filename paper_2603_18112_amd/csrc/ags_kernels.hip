@@ -1202,11 +1202,14 @@ template <typename GT, int KT, int RMODE>
 hipError_t step_r(const StepArgs& a, int n_tiles, bool update, hipStream_t s, KernelEvents ev) {
     const dim3 grid(n_tiles), block(kTileBlock);
     if (!update) {
+        const unsigned lds = (unsigned)a.lds_pad;
         if (a.gbar && a.w_norm_in)
-            return launch(step_kernel<GT, KT, RMODE, false, 0, true, true>, grid, block, s, a, ev);
-        if (a.gbar) return launch(step_kernel<GT, KT, RMODE, false, 0, false, true>, grid, block, s, a, ev);
-        if (a.w_norm_in) return launch(step_kernel<GT, KT, RMODE, false, 0, true>, grid, block, s, a, ev);
-        return launch(step_kernel<GT, KT, RMODE, false, 0>, grid, block, s, a, ev);
+            return launch(step_kernel<GT, KT, RMODE, false, 0, true, true>, grid, block, s, a, ev, lds);
+        if (a.gbar)
+            return launch(step_kernel<GT, KT, RMODE, false, 0, false, true>, grid, block, s, a, ev, lds);
+        if (a.w_norm_in)
+            return launch(step_kernel<GT, KT, RMODE, false, 0, true>, grid, block, s, a, ev, lds);
+        return launch(step_kernel<GT, KT, RMODE, false, 0>, grid, block, s, a, ev, lds);
     }
     if (a.ew == 2) return launch(step_kernel<GT, KT, RMODE, true, 2>, grid, block, s, a, ev);
     if (a.ew) return launch(step_kernel<GT, KT, RMODE, true, 1>, grid, block, s, a, ev);
@@ -1224,12 +1227,13 @@ hipError_t step_k(const StepArgs& a, int n_tiles, bool update, hipStream_t s, Ke
 template <typename GT, int KT>
 hipError_t update_k(const UpdateArgs& a, hipStream_t s, KernelEvents ev) {
     const dim3 grid(a.n_tiles), block(kTileBlock);
+    const unsigned lds = (unsigned)a.lds_pad;
     if (a.w_norm_out) {
-        if (a.gbar) return launch(update_kernel<GT, KT, false, true>, grid, block, s, a, ev);
-        return launch(update_kernel<GT, KT, true, true>, grid, block, s, a, ev);
+        if (a.gbar) return launch(update_kernel<GT, KT, false, true>, grid, block, s, a, ev, lds);
+        return launch(update_kernel<GT, KT, true, true>, grid, block, s, a, ev, lds);
     }
-    if (a.gbar) return launch(update_kernel<GT, KT, false, false>, grid, block, s, a, ev);
-    return launch(update_kernel<GT, KT, true, false>, grid, block, s, a, ev);
+    if (a.gbar) return launch(update_kernel<GT, KT, false, false>, grid, block, s, a, ev, lds);
+    return launch(update_kernel<GT, KT, true, false>, grid, block, s, a, ev, lds);
 }
 
 template <typename GT, int KT>
