@@ -501,6 +501,41 @@ def test_stats_call_does_not_mutate():
     p.close()
 
 
+def test_vgg16_capped_launches_against_oracle():
+    """Layouts whose w and m outgrow the Infinity Cache (VGG-16: 1.1 GB)
+    launch the statistics-only step kernel and the LARS update kernel with
+    an LDS pad that caps their blocks per CU.  Here every such launch runs
+    against the oracle: LARS steps (the first reads w, the next take the
+    carried weight norms), a LARS statistics call between them, and the
+    statistics call of an AGS handle; every statistic, and w and m after
+    the last step."""
+    lay = layouts.get_layout("vgg16")
+    K = 8
+    sig = synth.layer_sigmas(lay, 0)
+
+    def grads(t):
+        return synth.replica_grads(lay, K, t, 0, sigmas=sig)
+
+    p = Pair(lay, K, mode="lars", reuse_w_norms=True)
+    try:
+        p.step(grads(0), what="vgg16 lars step 1")
+        p.step(grads(1), commit=False, what="vgg16 lars stats call")
+        p.step(grads(2), what="vgg16 lars step 2")
+        p.step(grads(3), what="vgg16 lars step 3")
+        p.check_state("vgg16 lars step 3")
+    finally:
+        p.close()
+    log("  vgg16 lars ok")
+    p = Pair(lay, K)
+    try:
+        p.step(grads(0), commit=False, what="vgg16 ags stats call")
+        p.step(grads(1), what="vgg16 ags step 1")
+        p.step(grads(2), commit=False, what="vgg16 ags stats call after a step")
+        p.check_state("vgg16 ags step 1")
+    finally:
+        p.close()
+
+
 def test_bitwise_determinism():
     lay = layouts.get_layout("resnet18_cifar")
     grads = [to_device(synth.replica_grads(lay, 8, t, 1)) for t in range(3)]
