@@ -1,6 +1,7 @@
 // Launcher stubs for the sanitizer build of libags's host code (test
-// infrastructure): the host-only build has no kernels, and the host-side
-// tests it runs never reach a launch.
+// infrastructure): that build leaves out the file of the step, finalize,
+// correction and update kernels, and the host-side tests it runs never
+// reach a launch.
 #include "ags_internal.h"
 
 namespace ags {

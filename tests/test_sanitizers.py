@@ -3,7 +3,10 @@
 * the float64 oracle, built with gcc and both sanitizers, runs its pins;
 * libags's host code (argument validation, workspace layout, state and
   planner), built by hipcc with the sanitizers on the host pass only and
-  without device code, runs the C-ABI and planner tests.
+  without the step, finalize, correction and update kernels (launcher
+  stubs stand in for them; the two table kernels of the no-alloc entry
+  point, which live beside the host code, are compiled for the GPU without
+  sanitizers), runs the C-ABI and planner tests.
 
 Each run is a subprocess with the matching sanitizer runtime preloaded; a
 report makes it fail.  GPU code is never built with a sanitizer here.
