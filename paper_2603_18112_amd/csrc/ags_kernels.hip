@@ -52,11 +52,14 @@ namespace {
 // Batches of the element-scale kernels, which hold more per-element state
 // (the fp64 replica sums, the scales): with 8 bf16 replicas per batch the
 // refresh kernel needs 319 VGPRs (one wave per SIMD), with 4 it needs 121.
+// fp32: 4 replicas per batch keep more reads in flight than 2 (step kernel,
+// K = 8: ResNet-18 96.4 -> 95.0 us, the ResNet-50 layout 213.6 -> 210.5,
+// VGG-16 1357 -> 1348; 8 measured the same as 4).
 #ifndef AGS_BATCH_BF16_EW
 #define AGS_BATCH_BF16_EW 4
 #endif
 #ifndef AGS_BATCH_F32_EW
-#define AGS_BATCH_F32_EW 2
+#define AGS_BATCH_F32_EW 4
 #endif
 
 // bf16 gradients: a lane's two halves are adjacent (8 consecutive elements,
