@@ -19,7 +19,8 @@
 //         register limit down to 2 (a dynamic LDS pad caps it), in both
 //         tile orders the step kernel uses (round-robin over the XCDs, and
 //         a contiguous range per XCD) and with load batches of 8 and 16
-//         (bf16 rows, or fp32 half rows), and the fastest counts: how many
+//         (bf16 rows, or fp32 half rows) or, for bf16 rows, two batches of
+//         4 or 8 pipelined as the step kernel does, and the fastest counts: how many
 //         streams run at once, and where, decides how well the DRAM rows
 //         are used.
 // Usage: hbm_probe [K grad_dtype(bf16|f32) n_elements [ew]]; without
@@ -102,7 +103,9 @@ __device__ __forceinline__ void add_bf16x8(const u32x4& v, float (&s)[8]) {
 // rows, elements [512v + 8l, +8) (one 16-byte load per row), for fp32 rows
 // [512v + 4l, +4) and [512v + 256 + 4l, +4) (two 16-byte loads per row).
 // Rows are loaded in batches of B (bf16: B rows; fp32: B / 2 rows, two
-// loads each) before any is used.  With xcd, block b
+// loads each) before any is used.  B = -KB (bf16 only, K a multiple of
+// 2 KB): two batches of KB rows in registers, the next batch's loads in
+// flight while the current one is summed.  With xcd, block b
 // takes the tile that the step kernel's XCD-aware order gives it (each of
 // the 8 XCDs, which receive every 8th block, walks a contiguous range of
 // tiles) instead of tile b.  w and m: the same
@@ -138,6 +141,37 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
         c0 = make_float4(__uint_as_float(a.x), __uint_as_float(a.y), __uint_as_float(a.z), __uint_as_float(a.w));
         c1 = make_float4(__uint_as_float(b.x), __uint_as_float(b.y), __uint_as_float(b.z), __uint_as_float(b.w));
     }
+    if constexpr (BF16 && B < 0) {
+        constexpr int KB = -B;
+        const unsigned short* g = static_cast<const unsigned short*>(grads);
+        auto row = [&](int k) {
+            return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(g + (size_t)k * stride + i0));
+        };
+        u32x4 a[KB], b[KB];
+#pragma unroll
+        for (int j = 0; j < KB; ++j) a[j] = row(j);
+#pragma unroll
+        for (int j = 0; j < KB; ++j) b[j] = row(KB + j);
+#pragma unroll
+        for (int j = 0; j < KB; ++j) add_bf16x8(a[j], s);
+        for (int kb = KB; kb < K; kb += 2 * KB) {
+            // b holds rows [kb, kb + KB); a takes the next batch, if any
+            const bool more = kb + KB < K;
+            if (more) {
+#pragma unroll
+                for (int j = 0; j < KB; ++j) a[j] = row(kb + KB + j);
+            }
+#pragma unroll
+            for (int j = 0; j < KB; ++j) add_bf16x8(b[j], s);
+            if (!more) break;
+            if (kb + 2 * KB < K) {
+#pragma unroll
+                for (int j = 0; j < KB; ++j) b[j] = row(kb + 2 * KB + j);
+            }
+#pragma unroll
+            for (int j = 0; j < KB; ++j) add_bf16x8(a[j], s);
+        }
+    } else {
     for (int k0 = 0; k0 < K; k0 += B) {
         if (BF16) {
             const unsigned short* g = static_cast<const unsigned short*>(grads);
@@ -172,6 +206,7 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
             }
         }
     }
+    }
     m0.x = fmaf(0.9f, m0.x, c0.x * s[0]); m0.y = fmaf(0.9f, m0.y, c0.y * s[1]);
     m0.z = fmaf(0.9f, m0.z, c0.z * s[2]); m0.w = fmaf(0.9f, m0.w, c0.w * s[3]);
     m1.x = fmaf(0.9f, m1.x, c1.x * s[4]); m1.y = fmaf(0.9f, m1.y, c1.y * s[5]);
@@ -204,28 +239,42 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
 
 // Launch of the step pattern: element scales or not (ew: 0, 1 or 2), with
 // lds bytes of dynamic LDS (unused, a cap on the blocks per CU), in the
-// XCD-aware tile order or not, with load batches of 8 or (deep) 16.
+// XCD-aware tile order or not, with the load schedule `sched`: batches of
+// 8 (0) or 16 (1), or (bf16 only, see pipelined_ok) two pipelined batches
+// of 4 (2) or 8 (3).
+constexpr const char* kSchedName[4] = {"8", "16", "2x4 pipelined", "2x8 pipelined"};
+bool pipelined_ok(bool bf16, int K, int sched) {
+    const int kb = sched == 2 ? 4 : 8;
+    return sched < 2 || (bf16 && K % (2 * kb) == 0);
+}
 void launch_step_pattern(bool bf16, int ew, int grid, const void* g, size_t stride, int K, float* w,
                          float* m, const float* sc_in, float* sc_out, unsigned lds, int xcd,
-                         int deep) {
-#define PROBE_LAUNCH(BF, E)                                                                      \
-    do {                                                                                         \
-        if (deep)                                                                                \
-            hipLaunchKernelGGL((probe_step<BF, E, 16>), dim3(grid), dim3(256), lds, 0, g, stride, K, \
-                               w, m, sc_in, sc_out, xcd);                                        \
-        else                                                                                     \
-            hipLaunchKernelGGL((probe_step<BF, E, 8>), dim3(grid), dim3(256), lds, 0, g, stride, K,  \
-                               w, m, sc_in, sc_out, xcd);                                        \
+                         int sched) {
+#define PROBE_LAUNCH(BF, E, B)                                                                    \
+    hipLaunchKernelGGL((probe_step<BF, E, B>), dim3(grid), dim3(256), lds, 0, g, stride, K, w, m, \
+                       sc_in, sc_out, xcd)
+#define PROBE_SCHED(BF, E)                    \
+    do {                                      \
+        if (sched == 1) PROBE_LAUNCH(BF, E, 16); \
+        else PROBE_LAUNCH(BF, E, 8);          \
+    } while (0)
+#define PROBE_SCHED_PIPE(E)                         \
+    do {                                            \
+        if (sched == 3) PROBE_LAUNCH(true, E, -8);  \
+        else if (sched == 2) PROBE_LAUNCH(true, E, -4); \
+        else PROBE_SCHED(true, E);                  \
     } while (0)
     if (bf16) {
-        if (ew == 0) PROBE_LAUNCH(true, 0);
-        else if (ew == 1) PROBE_LAUNCH(true, 1);
-        else PROBE_LAUNCH(true, 2);
+        if (ew == 0) PROBE_SCHED_PIPE(0);
+        else if (ew == 1) PROBE_SCHED_PIPE(1);
+        else PROBE_SCHED_PIPE(2);
     } else {
-        if (ew == 0) PROBE_LAUNCH(false, 0);
-        else if (ew == 1) PROBE_LAUNCH(false, 1);
-        else PROBE_LAUNCH(false, 2);
+        if (ew == 0) PROBE_SCHED(false, 0);
+        else if (ew == 1) PROBE_SCHED(false, 1);
+        else PROBE_SCHED(false, 2);
     }
+#undef PROBE_SCHED_PIPE
+#undef PROBE_SCHED
 #undef PROBE_LAUNCH
 }
 
@@ -358,8 +407,9 @@ int main(int argc, char** argv) {
     int best_ew = ew ? 1 : 0, best_pad = 0, best_xcd = 0, best_deep = 0;
     double step_us = 0;
     for (int v = ew ? 1 : 0; v <= (ew ? 2 : 0); ++v) {
-        for (int c = 0; c < 4 * n_pads; ++c) {
+        for (int c = 0; c < 8 * n_pads; ++c) {
             const int pi = c % n_pads, xcd = (c / n_pads) & 1, deep = c / (2 * n_pads);
+            if (!pipelined_ok(bf16, K, deep)) continue;
             double us = 0;
             const int rc = time_launches(
                 [&]() {
@@ -387,8 +437,9 @@ int main(int argc, char** argv) {
     constexpr int kCold = 21;
     double cold_us = 0;
     int best_cold_pad = 0, best_cold_xcd = 0, best_cold_deep = 0;
-    for (int ci = 0; ci < 4 * n_pads; ++ci) {
+    for (int ci = 0; ci < 8 * n_pads; ++ci) {
         const int pi = ci % n_pads, xcd = (ci / n_pads) & 1, deep = ci / (2 * n_pads);
+        if (!pipelined_ok(bf16, K, deep)) continue;
         float cold_ms[kCold];
         for (int r = 0; r < kCold; ++r) {
             hipLaunchKernelGGL(evict_read, dim3(2048), dim3(256), 0, 0, evict, evict_bytes / 16, out);
@@ -421,15 +472,15 @@ int main(int argc, char** argv) {
            "\"step_pattern_cold_GBps\": %.1f, \"step_pattern_cold_us\": %.2f, "
            "\"step_pattern_blocks_per_cu\": %d, \"step_pattern_cold_blocks_per_cu\": %d, "
            "\"step_pattern_xcd_order\": %s, \"step_pattern_cold_xcd_order\": %s, "
-           "\"step_pattern_load_batch\": %d, \"step_pattern_cold_load_batch\": %d, "
+           "\"step_pattern_load_batch\": \"%s\", \"step_pattern_cold_load_batch\": \"%s\", "
            "\"step_pattern\": "
            "{\"K\": %d, \"grad_dtype\": \"%s\", \"elements\": %zu, \"bytes_per_element\": %zu, "
            "\"element_scales\": %s}, "
            "\"bytes\": %zu, \"data\": \"random\"}\n",
            best[0], best_grid[0], best[1], best_grid[1], step_bytes / (step_us * 1e-6) / 1e9, step_us,
            step_bytes / (cold_us * 1e-6) / 1e9, cold_us, caps[best_pad], caps[best_cold_pad],
-           best_xcd ? "true" : "false", best_cold_xcd ? "true" : "false", best_deep ? 16 : 8,
-           best_cold_deep ? 16 : 8, K,
+           best_xcd ? "true" : "false", best_cold_xcd ? "true" : "false", kSchedName[best_deep],
+           kSchedName[best_cold_deep], K,
            bf16 ? "bf16" : "f32", ne, bpe,
            !ew ? "null" : (best_ew == 2 ? "\"streaming\"" : "\"ordinary\""), bytes);
     if (sc) CHECK(hipFree(sc));
