@@ -20,7 +20,8 @@
 //         tile orders the step kernel uses (round-robin over the XCDs, and
 //         a contiguous range per XCD) and with load batches of 8 and 16
 //         (bf16 rows, or fp32 half rows) or, for bf16 rows, two batches of
-//         4 or 8 pipelined as the step kernel does, and the fastest counts: how many
+//         4 or 8 pipelined as the step kernel does, with w and m loaded
+//         before the replicas or after the first batch, and the fastest counts: how many
 //         streams run at once, and where, decides how well the DRAM rows
 //         are used.
 // Usage: hbm_probe [K grad_dtype(bf16|f32) n_elements [ew]]; without
@@ -112,8 +113,10 @@ __device__ __forceinline__ void add_bf16x8(const u32x4& v, float (&s)[8]) {
 // elements, fp32, read and written.  EW (element scales): one more fp32
 // stream read (sc_in) and one written (sc_out) for the same elements, with
 // ordinary accesses (EW = 1) or streaming ones, w and m stores included
-// (EW = 2).  n is a multiple of kTile.
-template <bool BF16, int EW, int B>
+// (EW = 2).  WL: w, m (and the scale in force) are loaded after the first
+// replica batch's loads are issued instead of before them.  n is a
+// multiple of kTile.
+template <bool BF16, int EW, int B, bool WL>
 __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads, size_t stride,
                                                   int K, float* __restrict__ w,
                                                   float* __restrict__ m,
@@ -129,18 +132,27 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
     const size_t i0 = base + (BF16 ? 8 * lane : 4 * lane);
     const size_t i1 = BF16 ? i0 + 4 : i0 + 256;
     float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    float4 w0 = *reinterpret_cast<const float4*>(w + i0), w1 = *reinterpret_cast<const float4*>(w + i1);
-    float4 m0 = *reinterpret_cast<const float4*>(m + i0), m1 = *reinterpret_cast<const float4*>(m + i1);
+    float4 w0, w1, m0, m1;
     float4 c0 = make_float4(1, 1, 1, 1), c1 = c0;
-    if (EW == 1) {
-        c0 = *reinterpret_cast<const float4*>(sc_in + i0);
-        c1 = *reinterpret_cast<const float4*>(sc_in + i1);
-    } else if (EW == 2) {
-        const u32x4 a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(sc_in + i0));
-        const u32x4 b = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(sc_in + i1));
-        c0 = make_float4(__uint_as_float(a.x), __uint_as_float(a.y), __uint_as_float(a.z), __uint_as_float(a.w));
-        c1 = make_float4(__uint_as_float(b.x), __uint_as_float(b.y), __uint_as_float(b.z), __uint_as_float(b.w));
-    }
+    // The compiler keeps the chosen order: scheduling barriers around it.
+    auto load_wm = [&]() {
+        __builtin_amdgcn_sched_barrier(0);
+        w0 = *reinterpret_cast<const float4*>(w + i0);
+        w1 = *reinterpret_cast<const float4*>(w + i1);
+        m0 = *reinterpret_cast<const float4*>(m + i0);
+        m1 = *reinterpret_cast<const float4*>(m + i1);
+        if (EW == 1) {
+            c0 = *reinterpret_cast<const float4*>(sc_in + i0);
+            c1 = *reinterpret_cast<const float4*>(sc_in + i1);
+        } else if (EW == 2) {
+            const u32x4 a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(sc_in + i0));
+            const u32x4 b = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(sc_in + i1));
+            c0 = make_float4(__uint_as_float(a.x), __uint_as_float(a.y), __uint_as_float(a.z), __uint_as_float(a.w));
+            c1 = make_float4(__uint_as_float(b.x), __uint_as_float(b.y), __uint_as_float(b.z), __uint_as_float(b.w));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    if (!WL) load_wm();
     if constexpr (BF16 && B < 0) {
         constexpr int KB = -B;
         const unsigned short* g = static_cast<const unsigned short*>(grads);
@@ -152,6 +164,7 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
         for (int j = 0; j < KB; ++j) a[j] = row(j);
 #pragma unroll
         for (int j = 0; j < KB; ++j) b[j] = row(KB + j);
+        if (WL) load_wm();
 #pragma unroll
         for (int j = 0; j < KB; ++j) add_bf16x8(a[j], s);
         for (int kb = KB; kb < K; kb += 2 * KB) {
@@ -183,6 +196,7 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
                 v[j] = in ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(r + i0))
                           : u32x4{0u, 0u, 0u, 0u};
             }
+            if (WL && k0 == 0) load_wm();
 #pragma unroll
             for (int j = 0; j < B; ++j) add_bf16x8(v[j], s);
         } else {
@@ -196,6 +210,7 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
                     a[j] = in ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(r + i0)) : u32x4{0u, 0u, 0u, 0u};
                     b[j] = in ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(r + i1)) : u32x4{0u, 0u, 0u, 0u};
                 }
+                if (WL && k0 == 0 && kk == 0) load_wm();
 #pragma unroll
                 for (int j = 0; j < B / 2; ++j) {
                     s[0] += __uint_as_float(a[j].x); s[1] += __uint_as_float(a[j].y);
@@ -241,27 +256,37 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
 // lds bytes of dynamic LDS (unused, a cap on the blocks per CU), in the
 // XCD-aware tile order or not, with the load schedule `sched`: batches of
 // 8 (0) or 16 (1), or (bf16 only, see pipelined_ok) two pipelined batches
-// of 4 (2) or 8 (3).
-constexpr const char* kSchedName[4] = {"8", "16", "2x4 pipelined", "2x8 pipelined"};
+// of 4 (2) or 8 (3); plus 4 for w and m after the first batch.
+constexpr int kScheds = 8;
+constexpr const char* kSchedName[kScheds] = {
+    "8", "16", "2x4 pipelined", "2x8 pipelined", "8, w and m after the first batch",
+    "16, w and m after the first batch", "2x4 pipelined, w and m after the first batch",
+    "2x8 pipelined, w and m after the first batch"};
 bool pipelined_ok(bool bf16, int K, int sched) {
-    const int kb = sched == 2 ? 4 : 8;
-    return sched < 2 || (bf16 && K % (2 * kb) == 0);
+    const int sc = sched & 3, kb = sc == 2 ? 4 : 8;
+    return sc < 2 || (bf16 && K % (2 * kb) == 0);
 }
 void launch_step_pattern(bool bf16, int ew, int grid, const void* g, size_t stride, int K, float* w,
                          float* m, const float* sc_in, float* sc_out, unsigned lds, int xcd,
                          int sched) {
-#define PROBE_LAUNCH(BF, E, B)                                                                    \
-    hipLaunchKernelGGL((probe_step<BF, E, B>), dim3(grid), dim3(256), lds, 0, g, stride, K, w, m, \
-                       sc_in, sc_out, xcd)
+#define PROBE_LAUNCH(BF, E, B)                                                                     \
+    do {                                                                                           \
+        if (sched >= 4)                                                                            \
+            hipLaunchKernelGGL((probe_step<BF, E, B, true>), dim3(grid), dim3(256), lds, 0, g, stride, \
+                               K, w, m, sc_in, sc_out, xcd);                                       \
+        else                                                                                       \
+            hipLaunchKernelGGL((probe_step<BF, E, B, false>), dim3(grid), dim3(256), lds, 0, g,       \
+                               stride, K, w, m, sc_in, sc_out, xcd);                               \
+    } while (0)
 #define PROBE_SCHED(BF, E)                    \
     do {                                      \
-        if (sched == 1) PROBE_LAUNCH(BF, E, 16); \
+        if ((sched & 3) == 1) PROBE_LAUNCH(BF, E, 16); \
         else PROBE_LAUNCH(BF, E, 8);          \
     } while (0)
 #define PROBE_SCHED_PIPE(E)                         \
     do {                                            \
-        if (sched == 3) PROBE_LAUNCH(true, E, -8);  \
-        else if (sched == 2) PROBE_LAUNCH(true, E, -4); \
+        if ((sched & 3) == 3) PROBE_LAUNCH(true, E, -8);  \
+        else if ((sched & 3) == 2) PROBE_LAUNCH(true, E, -4); \
         else PROBE_SCHED(true, E);                  \
     } while (0)
     if (bf16) {
@@ -407,7 +432,7 @@ int main(int argc, char** argv) {
     int best_ew = ew ? 1 : 0, best_pad = 0, best_xcd = 0, best_deep = 0;
     double step_us = 0;
     for (int v = ew ? 1 : 0; v <= (ew ? 2 : 0); ++v) {
-        for (int c = 0; c < 8 * n_pads; ++c) {
+        for (int c = 0; c < 2 * kScheds * n_pads; ++c) {
             const int pi = c % n_pads, xcd = (c / n_pads) & 1, deep = c / (2 * n_pads);
             if (!pipelined_ok(bf16, K, deep)) continue;
             double us = 0;
@@ -437,7 +462,7 @@ int main(int argc, char** argv) {
     constexpr int kCold = 21;
     double cold_us = 0;
     int best_cold_pad = 0, best_cold_xcd = 0, best_cold_deep = 0;
-    for (int ci = 0; ci < 8 * n_pads; ++ci) {
+    for (int ci = 0; ci < 2 * kScheds * n_pads; ++ci) {
         const int pi = ci % n_pads, xcd = (ci / n_pads) & 1, deep = ci / (2 * n_pads);
         if (!pipelined_ok(bf16, K, deep)) continue;
         float cold_ms[kCold];
