@@ -1,0 +1,123 @@
+"""Seeded random configurations against the oracle (marker gpu).
+
+Each case draws a ragged layout (1 to 40 layers of 1 to 150,000 elements,
+random scale / decay flags, offsets aligned to 8 or 64), a replica count
+from the compiled set and outside it, fp32 or bf16 replicas, a padded or
+tight replica stride, and every option of the step that combines with the
+others: mode (AGS, SGD, LARS, static), element scales (AGS), the per-layer
+Delta scope, carried LARS weight norms, the small-batch replica (0, the
+RMS over replicas, or another one), the refresh period and the noise
+level.  Five steps run on both sides, the third on gradients doubled (an
+exact scaling: Delta is about 3 there and 0.75 after it, so the decisions
+run not sensitive, sensitive, sensitive, not sensitive and the correction
+pass runs in both directions), with a statistics call between the second
+and third steps.  Every statistic is compared on every call and
+every element of w and m (and the element scales) after every step.
+
+Delta and Delta_l depend only on the gradient sequence, so a throwaway
+oracle run first picks a threshold delta that no Delta (and, with the
+per-layer scope, no scaled layer's Delta_l) comes close to: a decision
+taken at the threshold itself could go either way.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2603_18112_amd import layouts, synth
+from oracle import OracleAGS
+from ags_parity import Pair, log
+
+pytestmark = pytest.mark.gpu
+
+SD = layouts.LAYER_SCALE | layouts.LAYER_DECAY
+FLAGS = [0, layouts.LAYER_SCALE, layouts.LAYER_DECAY, SD]
+K_CHOICES = [1, 2, 3, 4, 5, 7, 8, 16, 17, 32, 64, 65]
+N_CASES = 24
+# replica elements per step (K * n_flat) above which a case is redrawn
+MAX_REPLICA_ELEMS = 12_000_000
+SCALES = [1.0, 1.0, 2.0, 1.0, 1.0]  # gradient factor per step
+
+
+def draw_case(seed):
+    rng = np.random.default_rng(seed)
+    K = int(rng.choice(K_CHOICES))
+    while True:
+        L = int(rng.integers(1, 41))
+        kind = rng.random(L)
+        sizes = np.where(kind < 0.25, rng.integers(1, 65, L),
+                         np.where(kind < 0.8, rng.integers(65, 12_000, L),
+                                  rng.integers(12_000, 150_001, L)))
+        flags = [FLAGS[int(i)] for i in rng.integers(0, 4, L)]
+        pad = int(rng.choice([8, 64]))
+        lay = layouts.custom_layout([int(s) for s in sizes], flags, pad=pad, name=f"random{seed}")
+        if K * lay.n_flat <= MAX_REPLICA_ELEMS:
+            break
+    dtype = str(rng.choice(["f32", "bf16"]))
+    mode = str(rng.choice(["ags", "sgd", "lars", "static"]))
+    hyper = dict(delta_scope=str(rng.choice(["global", "layer"])),
+                 refresh_every=int(rng.choice([1, 2, 3])))
+    if mode == "ags" and rng.random() < 0.5:
+        hyper["elementwise"] = True
+    if mode == "lars" and rng.random() < 0.5:
+        hyper["reuse_w_norms"] = True
+    if mode == "static":
+        hyper["static_scale"] = float(rng.choice([0.5, 2.0, 4.0]))
+    r = rng.random()
+    hyper["small_replica"] = 0 if (r < 0.4 or K == 1) else (-1 if r < 0.7 else int(rng.integers(1, K)))
+    stride = lay.n_flat + (0 if rng.random() < 0.5 else 8 * int(rng.integers(1, 600)))
+    noise = float(rng.choice([0.1, 0.5, 2.0]))
+    return lay, K, dtype, mode, hyper, stride, noise
+
+
+def doubled(g, dtype):
+    """g times 2, exactly: fp32 by multiplication, bf16 by one more in the
+    exponent field of every nonzero finite value."""
+    if dtype == "f32":
+        return g * np.float32(2.0)
+    exp = (g >> 7) & 0xFF
+    bump = (exp != 0) & (exp < 0xFE)
+    return np.where(bump, g + np.uint16(0x80), g).astype(np.uint16)
+
+
+def pick_delta(lay, K, dtype, grads, layer_scope):
+    """A threshold that every Delta (and with the per-layer scope every
+    scaled layer's Delta_l) of the sequence clears by at least 1%."""
+    table = lay.table()
+    o = OracleAGS(table, lay.n_flat, K, np.zeros(lay.n_flat, np.float32), mode="sgd",
+                  grad_dtype=dtype)
+    deltas = []
+    for g in grads:
+        layer, glob = o.step(g)
+        deltas.append(glob["delta"])
+        if layer_scope:
+            deltas += [d for d, (_, _, f) in zip(layer["delta"], table) if f & layouts.LAYER_SCALE]
+    finite = [d for d in deltas if math.isfinite(d)]
+    for cand in (0.5, 0.43, 0.61, 0.37, 0.77, 0.29, 0.93, 1.3, 0.21, 1.9):
+        if all(abs(d - cand) > 0.01 * cand for d in finite):
+            return cand
+    raise AssertionError("no clear threshold for this gradient sequence")
+
+
+@pytest.mark.parametrize("case", range(N_CASES))
+def test_random_configuration_against_oracle(case):
+    seed = 7000 + case
+    lay, K, dtype, mode, hyper, stride, noise = draw_case(seed)
+    desc = (f"case {case}: {len(lay.table())} layers, {lay.n_flat} elements, K={K} {dtype}, "
+            f"{mode}, {hyper}, stride {stride}, noise {noise}")
+    log(desc)
+    sig = synth.layer_sigmas(lay, seed)
+    grads = []
+    for t, f in enumerate(SCALES):
+        g = synth.replica_grads(lay, K, t, seed, noise=noise, dtype=dtype, sigmas=sig, stride=stride)
+        grads.append(doubled(g, dtype) if f == 2.0 else g)
+    hyper["delta"] = pick_delta(lay, K, dtype, grads, hyper["delta_scope"] == "layer")
+    p = Pair(lay, K, dtype=dtype, mode=mode, seed=seed, stride=stride, **hyper)
+    try:
+        for t, g in enumerate(grads):
+            if t == 2:
+                p.step(g, commit=False, what=f"{desc} stats call")
+            p.step(g, what=f"{desc} step {t + 1}")
+            p.check_state(f"{desc} step {t + 1}")
+    finally:
+        p.close()
