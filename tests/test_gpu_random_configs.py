@@ -33,7 +33,7 @@ pytestmark = pytest.mark.gpu
 SD = layouts.LAYER_SCALE | layouts.LAYER_DECAY
 FLAGS = [0, layouts.LAYER_SCALE, layouts.LAYER_DECAY, SD]
 K_CHOICES = [1, 2, 3, 4, 5, 7, 8, 16, 17, 32, 64, 65]
-N_CASES = 24
+N_CASES = 64
 # replica elements per step (K * n_flat) above which a case is redrawn
 MAX_REPLICA_ELEMS = 12_000_000
 SCALES = [1.0, 1.0, 2.0, 1.0, 1.0]  # gradient factor per step
