@@ -83,3 +83,45 @@ def test_noalloc_stats_match_ags_stats_call_after_call():
         # w is only read
         assert torch.equal(w, torch.from_numpy(w0).cuda())
         del g, w, m
+
+
+def test_noalloc_random_configs_match_ags_stats():
+    """Seeded random configurations (the generator of the random parity
+    sweep: ragged layouts, K from 2 to 65, fp32 or bf16, every mode, element
+    scales, both Delta scopes, every small-batch replica choice, padded
+    strides) in no particular order of size: every call bitwise equal to a
+    handle's ags_stats on the same bytes, and within tolerance of the
+    oracle's statistics of a first step."""
+    import torch
+    from test_gpu_random_configs import draw_case
+    stream = torch.cuda.current_stream()
+    for case in range(24):
+        seed = 9100 + case
+        lay, K, dt, mode, hyper, stride, noise = draw_case(seed)
+        hp = dict(lr=0.1, momentum=0.9, weight_decay=5e-4, delta=0.5, eps=1e-8, mode=mode,
+                  **{k: v for k, v in hyper.items() if k != "reuse_w_norms"})
+        w0 = synth.init_weights(lay, seed)
+        g_np = synth.replica_grads(lay, K, 0, seed, noise=noise, dtype=dt, stride=stride)
+        w = torch.from_numpy(w0.copy()).cuda()
+        m = torch.zeros_like(w)
+        g = to_device(g_np)
+        torch.cuda.synchronize()
+        what = f"no-alloc case {case}: {lay.n_flat} elements, K={K} {dt} {hp}"
+        log("  " + what)
+        cfg = ags.make_config(lay.table(), lay.n_flat, K, grad_dtype=dt, **hp)
+        nl, ng = ags.ags_stats_noalloc(cfg, w.data_ptr(), g.data_ptr(), stride, stream.cuda_stream)
+        h = ags.AGS(lay.table(), w, m, K, grad_dtype=dt, **hp)
+        h.stats(g)
+        s = h.read_stats()
+        h.close()
+        for f in ags.LAYER_STATS_FIELDS:
+            assert np.array_equal(nl[f], s.layer[f]), (what, f)
+        assert ng == s.glob, what
+        ora = {k: v for k, v in hp.items() if k != "mode"}
+        o = OracleAGS(lay.table(), lay.n_flat, K, w0, mode=mode, grad_dtype=dt, **ora)
+        ol, og = o.stats(g_np)
+        check_stats(nl, ng, ol, og, hp["delta"], what,
+                    layer_scope=hp.get("delta_scope") == "layer",
+                    scaled=[bool(f & layouts.LAYER_SCALE) for _, _, f in lay.table()])
+        assert torch.equal(w, torch.from_numpy(w0).cuda()), what
+        del g, w, m
