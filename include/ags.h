@@ -262,8 +262,10 @@ ags_status ags_set_state(ags_handle *h, const double *gradscale_L, double g_sq_p
  * function, which a
  * caller that writes w between calls (a checkpoint load, another
  * optimizer's step, an in-place edit) must call before the next step.  A
- * step captured into a HIP graph keeps the choice made at capture: capture
- * after a step if the replays should use the sums.  AGS_E_STATE on a handle
+ * step captured into a HIP graph always reads w (a replay cannot know
+ * whether w still holds what the last update wrote), and capturing leaves
+ * the handle's choice for its later eager calls as it was; a replayed
+ * update pass writes the sums like an eager one.  AGS_E_STATE on a handle
  * without reuse_w_norms. */
 ags_status ags_invalidate_weight_norms(ags_handle *h);
 

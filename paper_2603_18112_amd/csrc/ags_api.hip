@@ -428,7 +428,8 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     std::array<hipEvent_t, NE> ev{};
     // Steps enqueued while the stream is being captured into a graph are not
     // timed: a graph replays them without the handle's bookkeeping.
-    const bool prof = commit && h->profiling && !is_capturing(s);
+    const bool capturing = is_capturing(s);
+    const bool prof = commit && h->profiling && !capturing;
     if (prof) {
         if (!h->ev_free.empty()) {
             ev = h->ev_free.back();
@@ -508,7 +509,10 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.ew_buf = h->ew_buf(0);
     sa.n_flat = c.n_flat;
     sa.ew_partials = h->ew_partials();
-    sa.w_norm_in = (!fused && h->w_norm_valid) ? h->w_norm() : nullptr;
+    // A step captured into a graph reads w: a replay cannot see whether the
+    // carried weight norms still hold (the caller may have written w, or
+    // restored a state, since the capture).
+    sa.w_norm_in = (!fused && h->w_norm_valid && !capturing) ? h->w_norm() : nullptr;
     sa.lds_pad = ew ? 0 : (fused ? h->lds_pad : h->lds_pad_stats);
     hipError_t e = ags::launch_step(sa, c.grad_dtype, (int)h->n_tiles, fused, s, kev(0));
     if (e != hipSuccess) return launch_fail(e, "step kernel launch");
@@ -542,7 +546,10 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         if (e != hipSuccess) return launch_fail(e, "second-pass kernel launch");
     }
     if (prof) h->ev_pending.push_back(ev);
-    if (commit && c.mode == AGS_MODE_LARS) h->w_norm_valid = c.reuse_w_norms != 0;
+    // A captured step has not run: the norms are what the last executed
+    // update pass left (every update pass, replayed ones included, writes
+    // them for the w it writes).
+    if (commit && c.mode == AGS_MODE_LARS && !capturing) h->w_norm_valid = c.reuse_w_norms != 0;
     h->last_stream = s;
     h->has_stats = true;
     return AGS_OK;

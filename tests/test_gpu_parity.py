@@ -766,7 +766,9 @@ def test_bad_device_pointers_are_errors_not_faults():
     ("tiny_cnn", 4, "f32", {}), ("resnet18_cifar", 8, "f32", {}),
     ("tiny_cnn", 4, "bf16", {"elementwise": True}),
     ("resnet18_cifar", 8, "f32", {"elementwise": True, "refresh_every": 2}),
-    ("tiny_cnn", 4, "f32", {"delta_scope": "layer", "mode": "static"})])
+    ("tiny_cnn", 4, "f32", {"delta_scope": "layer", "mode": "static"}),
+    ("tiny_cnn", 4, "f32", {"mode": "sgd"}),
+    ("resnet18_cifar", 8, "bf16", {"mode": "lars"})])
 def test_hip_graph_capture_replays_match_eager(lay_name, K, dtype, hyper):
     """One ags_step captured in a HIP graph and replayed with fresh gradients
     copied into the captured buffer between replays (with eager work and a
@@ -809,6 +811,97 @@ def test_hip_graph_capture_replays_match_eager(lay_name, K, dtype, hyper):
             assert np.array_equal(eager.get_elementwise_scale(), graphed.get_elementwise_scale())
     eager.close()
     graphed.close()
+
+
+def test_lars_carried_norms_with_graph_capture():
+    """LARS with carried weight norms and HIP graphs: a captured step reads
+    w (a replay cannot know whether w still holds what the last update
+    wrote), and capturing leaves the handle's own choice alone, since the
+    captured step has not run.  (a) A fresh handle captures a step, then
+    steps eagerly (which must read w: no update pass has run), replays,
+    steps, replays.  (b) A handle steps, captures, replays, has w, m and its
+    state (global, last decision, per-layer) restored to an earlier point
+    (ags_set_state drops the sums), and replays again.  Both end bitwise where eager steps on the same
+    gradients end (the carried sums are bitwise those of reading w)."""
+    import torch
+    lay = layouts.get_layout("resnet18_cifar")
+    K = 8
+    hyper = dict(mode="lars", reuse_w_norms=True)
+    grads = [to_device(synth.replica_grads(lay, K, t, 6)) for t in range(4)]
+    w0 = torch.from_numpy(synth.init_weights(lay, 6)).cuda()
+
+    def handle():
+        w, m = w0.clone(), torch.zeros_like(w0)
+        return ags.AGS(lay.table(), w, m, K, **hyper), w, m
+
+    ref, wr, mr = handle()
+    ref_after = []
+    for g in grads:
+        ref.step(g)
+        torch.cuda.synchronize()
+        ref_after.append((wr.clone(), mr.clone(), ref.read_stats()))
+    ref.close()
+
+    def same(w, m, h, t, what):
+        rw, rm, rs = ref_after[t]
+        assert torch.equal(w, rw) and torch.equal(m, rm), f"{what}: w, m after step {t + 1}"
+        s = h.read_stats()
+        for f in ags.LAYER_STATS_FIELDS:
+            assert np.array_equal(s.layer[f], rs.layer[f]), (what, t, f)
+
+    def capture(h):
+        gbuf = torch.empty_like(grads[0])
+        s = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=s):
+            h.step(gbuf)
+        torch.cuda.synchronize()
+        return graph, gbuf
+
+    def replay(graph, gbuf, g):
+        gbuf.copy_(g)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+
+    # (a) capture first, then eager and replayed steps in turn
+    h, w, m = handle()
+    graph, gbuf = capture(h)
+    assert torch.equal(w, w0)
+    for t, g in enumerate(grads):
+        if t % 2 == 0:
+            h.step(g)
+            torch.cuda.synchronize()
+        else:
+            replay(graph, gbuf, g)
+        same(w, m, h, t, "capture first")
+    h.close()
+    del graph
+
+    # (b) step, capture, replay, restore an earlier point, replay again
+    h, w, m = handle()
+    h.step(grads[0])
+    torch.cuda.synchronize()
+    w1, m1 = w.clone(), m.clone()
+    state1, last1, layer1 = h.get_state(), h.get_last_decision(), h.get_layer_state()
+    graph, gbuf = capture(h)
+    replay(graph, gbuf, grads[1])
+    same(w, m, h, 1, "capture after a step")
+    replay(graph, gbuf, grads[2])
+    same(w, m, h, 2, "capture after a step")
+    w.copy_(w1)
+    m.copy_(m1)
+    torch.cuda.synchronize()
+    h.set_state(*state1)
+    h.set_last_decision(*last1)
+    h.set_layer_state(layer1)
+    replay(graph, gbuf, grads[1])
+    same(w, m, h, 1, "replay after a restore")
+    h.step(grads[2])
+    torch.cuda.synchronize()
+    same(w, m, h, 2, "eager step after the replays")
+    h.close()
 
 
 def test_matches_golden_oracle_fixture():
