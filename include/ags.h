@@ -71,9 +71,10 @@
  *    ordered after the handle's earlier work by the caller (for example by
  *    capturing on the stream the handle last used, or after a synchronize).
  *    The handle's last stream must still exist when a call comes on another
- *    stream (the wait is an event recorded on it then), and when the
- *    getters and setters above wait for it; a caller that destroys that
- *    stream first makes one call of the handle on a live stream.
+ *    stream (the wait is an event recorded on it then) and when the
+ *    functions above wait for it: destroy the stream a handle last used
+ *    only after the handle has made a call on another stream, or after
+ *    ags_destroy.
  *    The caller's own accesses to w, m and the gradients are ordered by the
  *    caller, as for any kernel launched on hip_stream.
  *  - A handle is not thread-safe: one thread at a time.
