@@ -301,7 +301,12 @@ ags_status ags_set_last_decision(ags_handle *h, int32_t sensitive, const int32_t
  * carried but never used.  Get waits for the handle's last stream.  Set
  * checks every value is finite and >= 0 (AGS_E_ARG, nothing changed),
  * waits for the last stream, copies the array and recomputes the layer
- * means in fp64. */
+ * means in fp64.  Those means only feed the reports (the coef_a and
+ * gradscale records, the means ags_get_state returns); the kernels form
+ * them from fp32 tile sums, so after a set they can differ from the
+ * original run's in the last bits (about 1e-7 relative) until the next
+ * refresh recomputes them.  The element scales themselves, and so w and m,
+ * resume bit for bit. */
 ags_status ags_get_elementwise_scale(ags_handle *h, float *scale, int64_t n);
 ags_status ags_set_elementwise_scale(ags_handle *h, const float *scale, int64_t n);
 

@@ -121,3 +121,77 @@ def test_random_configuration_against_oracle(case):
             p.check_state(f"{desc} step {t + 1}")
     finally:
         p.close()
+
+
+@pytest.mark.parametrize("case", range(32))
+def test_random_configuration_resume_bitwise(case):
+    """Checkpoint and resume on seeded random configurations: a handle
+    steps three times (the third on doubled gradients, so its decision is
+    sensitive); a second handle over copies of w and m takes the first's
+    state, last decision, per-layer state and element scales; then both
+    take three more steps (one more doubled) and stay bitwise equal in w,
+    m, the element scales, the decisions and every statistic after each.
+    The one exception is by design: with element scales the layer means of
+    the scales (the coef_a and gradscale records, and the means
+    ags_get_state reports) are recomputed on the host in fp64 by
+    ags_set_elementwise_scale, while the kernels form them from fp32 tile
+    sums; they agree to fp32 rounding until a refresh recomputes them on
+    the device."""
+    import torch
+    from paper_2603_18112_amd import ags
+    from ags_parity import to_device
+    seed = 8000 + case
+    lay, K, dtype, mode, hyper, stride, noise = draw_case(seed)
+    desc = f"resume case {case}: {lay.n_flat} elements, K={K} {dtype}, {mode}, {hyper}"
+    log(desc)
+    sig = synth.layer_sigmas(lay, seed)
+    scales = [1.0, 1.0, 2.0, 1.0, 2.0, 1.0]
+    grads_np = []
+    for t, f in enumerate(scales):
+        g = synth.replica_grads(lay, K, t, seed, noise=noise, dtype=dtype, sigmas=sig, stride=stride)
+        grads_np.append(doubled(g, dtype) if f == 2.0 else g)
+    hyper["delta"] = pick_delta(lay, K, dtype, grads_np, hyper["delta_scope"] == "layer")
+    grads = [to_device(g) for g in grads_np]
+    table = lay.table()
+    w0 = torch.from_numpy(synth.init_weights(lay, seed)).cuda()
+    wa, ma = w0.clone(), torch.zeros_like(w0)
+    a = ags.AGS(table, wa, ma, K, grad_dtype=dtype, mode=mode, **hyper)
+    for g in grads[:3]:
+        a.step(g)
+    torch.cuda.synchronize()
+    ew = bool(hyper.get("elementwise"))
+    state, last, layer = a.get_state(), a.get_last_decision(), a.get_layer_state()
+    scale = a.get_elementwise_scale() if ew else None
+    wb, mb = wa.clone(), ma.clone()
+    b = ags.AGS(table, wb, mb, K, grad_dtype=dtype, mode=mode, **hyper)
+    b.set_state(None if ew else state[0], state[1], state[2])
+    if ew:
+        b.set_elementwise_scale(scale)
+    b.set_layer_state(layer)
+    b.set_last_decision(*last)
+    try:
+        for t, g in enumerate(grads[3:], start=4):
+            a.step(g)
+            b.step(g)
+            torch.cuda.synchronize()
+            assert torch.equal(wa, wb) and torch.equal(ma, mb), f"{desc}: w, m after step {t}"
+            sa, sb = a.read_stats(), b.read_stats()
+            for f in ags.LAYER_STATS_FIELDS:
+                if ew and f in ("coef_a", "gradscale"):
+                    np.testing.assert_allclose(sa.layer[f], sb.layer[f], rtol=1e-6, err_msg=f"{desc} {t} {f}")
+                else:
+                    assert np.array_equal(sa.layer[f], sb.layer[f]), (desc, t, f)
+            assert sa.glob == sb.glob, (desc, t)
+            ga, gb = a.get_state(), b.get_state()
+            assert ga[1:] == gb[1:], (desc, t)
+            if ew:
+                np.testing.assert_allclose(ga[0], gb[0], rtol=1e-6, err_msg=f"{desc} {t} means")
+            else:
+                assert np.array_equal(ga[0], gb[0]), (desc, t)
+            la, lb = a.get_last_decision(), b.get_last_decision()
+            assert la[0] == lb[0] and np.array_equal(la[1], lb[1]), (desc, t)
+            if ew:
+                assert np.array_equal(a.get_elementwise_scale(), b.get_elementwise_scale()), (desc, t)
+    finally:
+        a.close()
+        b.close()
