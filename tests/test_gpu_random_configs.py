@@ -195,3 +195,59 @@ def test_random_configuration_resume_bitwise(case):
     finally:
         a.close()
         b.close()
+
+
+@pytest.mark.parametrize("case", range(16))
+def test_random_configuration_graph_replay_bitwise(case):
+    """A step captured into a HIP graph on seeded random configurations:
+    the graph, replayed with each step's gradients copied into the captured
+    buffer, and eager steps on another handle stay bitwise equal in w, m,
+    every statistic and the element scales, through the decision changes
+    of doubled gradients (the refresh, the scale buffer in force and the
+    sensitive bit are all taken on the device)."""
+    import torch
+    from paper_2603_18112_amd import ags
+    from ags_parity import to_device
+    seed = 8500 + case
+    lay, K, dtype, mode, hyper, stride, noise = draw_case(seed)
+    desc = f"graph case {case}: {lay.n_flat} elements, K={K} {dtype}, {mode}, {hyper}"
+    log(desc)
+    sig = synth.layer_sigmas(lay, seed)
+    grads_np = []
+    for t, f in enumerate(SCALES):
+        g = synth.replica_grads(lay, K, t, seed, noise=noise, dtype=dtype, sigmas=sig, stride=stride)
+        grads_np.append(doubled(g, dtype) if f == 2.0 else g)
+    hyper["delta"] = pick_delta(lay, K, dtype, grads_np, hyper["delta_scope"] == "layer")
+    grads = [to_device(g) for g in grads_np]
+    table = lay.table()
+    w0 = torch.from_numpy(synth.init_weights(lay, seed)).cuda()
+    we, me = w0.clone(), torch.zeros_like(w0)
+    wg, mg = w0.clone(), torch.zeros_like(w0)
+    eager = ags.AGS(table, we, me, K, grad_dtype=dtype, mode=mode, **hyper)
+    graphed = ags.AGS(table, wg, mg, K, grad_dtype=dtype, mode=mode, **hyper)
+    try:
+        gbuf = torch.empty_like(grads[0])
+        s = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=s):
+            graphed.step(gbuf)
+        torch.cuda.synchronize()
+        assert torch.equal(wg, w0), desc
+        for t, g in enumerate(grads):
+            eager.step(g)
+            gbuf.copy_(g)
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(we, wg) and torch.equal(me, mg), f"{desc}: replay {t + 1}"
+            se, sg = eager.read_stats(), graphed.read_stats()
+            for f in ags.LAYER_STATS_FIELDS:
+                assert np.array_equal(se.layer[f], sg.layer[f]), (desc, t, f)
+            assert se.glob == sg.glob, (desc, t)
+            if hyper.get("elementwise"):
+                assert np.array_equal(eager.get_elementwise_scale(), graphed.get_elementwise_scale()), (desc, t)
+        del graph
+    finally:
+        eager.close()
+        graphed.close()
