@@ -236,8 +236,13 @@ ags_status ags_read_stats(ags_handle *h, ags_layer_stats *out_layers,
  * keeps eta a host-side schedule (the linear scaling with the batch and
  * the warm-up and decay of the baselines, Sec. IV-B, IV-D); the update of
  * Algorithm 1 and the wrapped momentum SGD read it per step.  lr must be
- * finite and >= 0 (AGS_E_ARG).  A step captured in a HIP graph keeps the
- * rate it was captured with. */
+ * finite and >= 0 (AGS_E_ARG).  The rate is kept in the device state and
+ * written (as fp32, by a one-thread kernel) on the handle's last stream,
+ * after the work queued there: every step that runs after it uses it,
+ * eager steps and steps replayed from a HIP graph captured earlier alike
+ * (a replay on another stream is ordered after this call by the caller).
+ * Called while that stream captures a graph, the write becomes part of the
+ * graph. */
 ags_status ags_set_lr(ags_handle *h, double lr);
 
 /* Checkpoint / resume of the AGS state (w and m are the caller's).

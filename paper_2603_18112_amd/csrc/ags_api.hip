@@ -306,7 +306,6 @@ struct ags_handle {
     float* d_w = nullptr;
     float* d_m = nullptr;
     int device = 0;
-    double lr = 0;
     int64_t n_tiles = 0;
     int64_t n_chunks = 0;
     int64_t grad_extent = 0;  // elements of one replica that are read
@@ -481,7 +480,6 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.mode = c.mode;
     sa.commit = commit ? 1 : 0;
     sa.refresh_every = c.refresh_every;
-    sa.lr = (float)h->lr;
     sa.momentum = (float)c.momentum;
     sa.delta = c.delta;
     sa.eps = c.eps;
@@ -537,7 +535,6 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         ua.state = h->state();
         ua.refresh_every = c.refresh_every;
         ua.corr_flag = h->corr_flag();
-        ua.lr = (float)h->lr;
         ua.momentum = (float)c.momentum;
         ua.w_norm_out = (c.mode == AGS_MODE_LARS) ? h->w_norm() : nullptr;
         ua.lds_pad = h->lds_pad_update;
@@ -690,7 +687,6 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
     h->d_w = d_w;
     h->d_m = d_m;
     h->device = dev;
-    h->lr = cfg->lr;
     h->n_tiles = n_tiles;
     h->n_chunks = (int64_t)chunks.size();
     h->grad_extent = extent;
@@ -743,10 +739,11 @@ ags_status ags_init(const ags_config* cfg, float* d_w, float* d_m, void* hip_str
         return AGS_E_DEVICE;
     }
 
-    // Initial device state: tables, gradscale = 1, G_prev = 0, step = 0.
+    // Initial device state: tables, gradscale = 1, G_prev = 0, step = 0,
+    // the configured learning rate.
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     std::vector<double> ones(cfg->n_layers, 1.0);
-    DevState ds{0.0, 0, 0, 0};
+    DevState ds{0.0, 0, 0, 0, (float)cfg->lr, 0};
     const struct {
         size_t off;
         const void* src;
@@ -814,7 +811,11 @@ ags_status ags_read_stats(ags_handle* h, ags_layer_stats* out_layers, ags_global
 ags_status ags_set_lr(ags_handle* h, double lr) {
     if (!h) return AGS_E_ARG;
     if (!std::isfinite(lr) || lr < 0) return h->fail(AGS_E_ARG, "lr must be finite and >= 0");
-    h->lr = lr;
+    // The rate lives in the device state, written in stream order after the
+    // handle's queued work, so that every later step reads it: eager ones
+    // and those replayed from a graph captured before.
+    const hipError_t e = ags::launch_set_lr(h->state(), (float)lr, h->last_stream);
+    if (e != hipSuccess) return h->hip_fail(e, "setting the learning rate");
     return AGS_OK;
 }
 
@@ -851,7 +852,7 @@ ags_status ags_set_state(ags_handle* h, const double* gradscale_L, double g_sq_p
     if (e != hipSuccess) return h->hip_fail(e, "waiting for the last stream");
     h->w_norm_valid = false;  // a restored state comes with weights of its own
     // g_prev and step only: the element-scale buffer index stays.
-    DevState ds{g_sq_prev, step, 0, 0};
+    DevState ds{g_sq_prev, step, 0, 0, 0.0f, 0};
     const size_t soff = h->wl.state - h->wl.gradscale;
     const size_t head = offsetof(DevState, ew_cur);
     std::memcpy(h->pinned + soff, &ds, head);
@@ -1159,6 +1160,8 @@ __global__ __launch_bounds__(256) void noalloc_layers_kernel(NoallocTables t) {
         ds.step = 0;
         ds.last_sens = 0;
         ds.ew_cur = 0;
+        ds.lr = 0.0f;  // a statistics call updates nothing
+        ds.pad_ = 0;
         *t.state = ds;
         t.counters[0] = 0u;
         t.counters[1] = 0u;
@@ -1296,7 +1299,6 @@ extern "C" ags_status ags_stats_noalloc(const ags_config* cfg, const float* d_w,
     sa.mode = c.mode;
     sa.commit = 0;
     sa.refresh_every = c.refresh_every;
-    sa.lr = (float)c.lr;
     sa.momentum = (float)c.momentum;
     sa.delta = c.delta;
     sa.eps = c.eps;

@@ -120,6 +120,9 @@ struct DevState {
     int64_t step;       // steps completed
     int32_t last_sens;  // the sensitive bit of the last committed step
     int32_t ew_cur;     // element scales: which of the two buffers is in force
+    float lr;           // learning rate in force (ags_set_lr writes it on the handle's
+                        // stream, so a step replayed from a graph uses the current one)
+    int32_t pad_;
 };
 
 // Per-tile fp32 partial sums: W (sum w^2), G (sum gbar^2), D (sum over
@@ -148,7 +151,7 @@ struct StepArgs {
     int mode;                // ags_mode
     int commit;              // 1: a step (state advances), 0: statistics only
     int refresh_every;
-    float lr, momentum;      // used when the kernel updates w and m
+    float momentum;          // used when the kernel updates w and m (lr: state->lr)
     double delta, eps, s_max, trust_coef, weight_decay, static_scale;
     double* gradscale;       // [n_layers]; with element scales, their layer means
     DevState* state;
@@ -199,8 +202,7 @@ struct UpdateArgs {
     const DevState* state;  // after the step: the buffer in force and the step count
     int refresh_every;
     const int* corr_flag;
-    float lr;
-    float momentum;
+    float momentum;          // lr: state->lr
     // LARS update: per-tile sums of the new w^2, summed as the statistics
     // pass sums w^2 (or nullptr).
     float* w_norm_out;
@@ -227,5 +229,7 @@ hipError_t launch_step(const StepArgs& a, ags_dtype dt, int n_tiles, bool update
 hipError_t launch_finalize(const StepArgs& a, int n_chunks, hipStream_t s, KernelEvents ev);
 hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s, KernelEvents ev);
 hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s, KernelEvents ev);
+// Writes the learning rate in force into the device state (one thread).
+hipError_t launch_set_lr(DevState* state, float lr, hipStream_t s);
 
 }  // namespace ags

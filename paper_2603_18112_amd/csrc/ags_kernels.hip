@@ -836,7 +836,7 @@ template <typename GT, int KT, int RMODE, bool UPD, int EW, bool FULL, bool WNC 
           bool GB = false>
 __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restrict__ g,
                                            int64_t idx, int n0, int n1, int K, float ca,
-                                           float cb, bool use_gs, bool scaled, bool refresh,
+                                           float cb, float lr, bool use_gs, bool scaled, bool refresh,
                                            const float* __restrict__ gs_old,
                                            float* __restrict__ gs_new, float smax, float& sw,
                                            float& sg, float& sd, float& ss, float& sx) {
@@ -883,7 +883,7 @@ __device__ __forceinline__ void step_group(const StepArgs& a, const GT* __restri
             const float ae = (ELEM && use_gs) ? gsv[e] : ca;
             const float d = fmaf(ae, gb[e], cb * wv[e]);
             mv[e] = fmaf(a.momentum, mv[e], d);
-            wv[e] = fmaf(-a.lr, mv[e], wv[e]);
+            wv[e] = fmaf(-lr, mv[e], wv[e]);
         }
         store_f32_as<NT, FULL, HS>(a.w + idx, n0, n1, wv);
         store_f32_as<NT, FULL, HS>(a.m + idx, n0, n1, mv);
@@ -941,11 +941,12 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
     // Coefficients predicted before the step: the unscaled ones when the
     // step is surely sensitive (Delta infinite by definition) or the last
     // committed step was sensitive, otherwise the scaled ones.
-    float ca = 1.0f, cb = 0.0f;
+    float ca = 1.0f, cb = 0.0f, lr = 0.0f;
     bool use_gs = false, scaled = false, refresh = false;
     const float* gs_old = nullptr;
     float* gs_new = nullptr;
     if (UPD) {
+        lr = a.state->lr;
         const uint32_t f = a.layers[l].flags;
         const long long step = a.state->step;
         const bool pred = a.delta_scope
@@ -971,8 +972,8 @@ __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
     float sw = 0.0f, sg = 0.0f, sd = 0.0f, ss = 0.0f, sx = 0.0f;
     for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
         step_group<GT, KT, RMODE, UPD, EW, decltype(full)::value, WNC, GB>(
-            a, g, idx, n0, n1, K, ca, cb, use_gs, scaled, refresh, gs_old, gs_new, smax, sw, sg, sd,
-            ss, sx);
+            a, g, idx, n0, n1, K, ca, cb, lr, use_gs, scaled, refresh, gs_old, gs_new, smax, sw, sg,
+            sd, ss, sx);
     });
 
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -1068,7 +1069,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(StepArgs a) {
 template <typename GT, int KT, bool PE, bool FULL>
 __device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __restrict__ g,
                                               int64_t idx, int n0, int n1, int K, float2 c,
-                                              const float* __restrict__ gs_old) {
+                                              float lr, const float* __restrict__ gs_old) {
     constexpr int HS = Map<GT>::HS;
     float gb[kVec], dv[kVec], gr[kVec], wv[kVec], mv[kVec], cv[kVec];
     double q[kVec];
@@ -1089,7 +1090,7 @@ __device__ __forceinline__ void correct_group(const UpdateArgs& a, const GT* __r
 #pragma unroll
     for (int e = 0; e < kVec; ++e) {
         mv[e] = fmaf(cv[e], gb[e], mv[e]);
-        wv[e] = fmaf(-a.lr * cv[e], gb[e], wv[e]);
+        wv[e] = fmaf(-lr * cv[e], gb[e], wv[e]);
     }
     store_f32<FULL, HS>(a.w + idx, n0, n1, wv);
     store_f32<FULL, HS>(a.m + idx, n0, n1, mv);
@@ -1100,6 +1101,7 @@ __global__ __launch_bounds__(kTileBlock) void correct_kernel(UpdateArgs a) {
     if (*a.corr_flag == 0) return;
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
+    const float lr = a.state->lr;
     // Element scales in force before the step: the other buffer if the
     // step (already counted) refreshed them.
     const float* gs_old = nullptr;
@@ -1116,11 +1118,11 @@ __global__ __launch_bounds__(kTileBlock) void correct_kernel(UpdateArgs a) {
         if (c.x == 0.0f && c.y == 0.0f) continue;
         if (c.y == 0.0f) {
             for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
-                correct_group<GT, KT, false, decltype(full)::value>(a, g, idx, n0, n1, K, c, gs_old);
+                correct_group<GT, KT, false, decltype(full)::value>(a, g, idx, n0, n1, K, c, lr, gs_old);
             });
         } else {
             for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
-                correct_group<GT, KT, true, decltype(full)::value>(a, g, idx, n0, n1, K, c, gs_old);
+                correct_group<GT, KT, true, decltype(full)::value>(a, g, idx, n0, n1, K, c, lr, gs_old);
             });
         }
     }
@@ -1137,7 +1139,7 @@ __global__ __launch_bounds__(kTileBlock) void correct_kernel(UpdateArgs a) {
 template <typename GT, int KT, bool RECOMP, bool FULL, bool WN>
 __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __restrict__ g,
                                              int64_t idx, int n0, int n1, int K, float ca,
-                                             float cb, float& sw) {
+                                             float cb, float lr, float& sw) {
     float gb[kVec], wv[kVec], mv[kVec];
     load_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
     load_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
@@ -1152,7 +1154,7 @@ __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __re
     for (int e = 0; e < kVec; ++e) {
         const float d = fmaf(ca, gb[e], cb * wv[e]);
         mv[e] = fmaf(a.momentum, mv[e], d);
-        wv[e] = fmaf(-a.lr, mv[e], wv[e]);
+        wv[e] = fmaf(-lr, mv[e], wv[e]);
     }
     store_f32<FULL, Map<GT>::HS>(a.w + idx, n0, n1, wv);
     store_f32<FULL, Map<GT>::HS>(a.m + idx, n0, n1, mv);
@@ -1168,10 +1170,11 @@ __global__ __launch_bounds__(kTileBlock) void update_kernel(UpdateArgs a) {
     const float2 ab = a.coef[t.layer];
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
+    const float lr = a.state->lr;
     float sw = 0.0f;
     for_each_group<Map<GT>::HS>(t.begin, t.count, [&](int64_t idx, int n0, int n1, auto full) {
         update_group<GT, KT, RECOMP, decltype(full)::value, WN>(a, g, idx, n0, n1, K, ab.x, ab.y,
-                                                                 sw);
+                                                                 lr, sw);
     });
     if (WN) {
         // the step kernel's reduction: wave butterfly, then the waves in a
@@ -1182,6 +1185,13 @@ __global__ __launch_bounds__(kTileBlock) void update_kernel(UpdateArgs a) {
         __syncthreads();
         if (threadIdx.x == 0) a.w_norm_out[blockIdx.x] = tree_sum<kTileBlock / 64>(red);
     }
+}
+
+// The learning rate in force, written by one lane (a kernel rather than a
+// copy, so that a call made while the stream captures a graph becomes a
+// kernel node that sets the same rate on every replay).
+__global__ __launch_bounds__(64) void set_lr_kernel(DevState* state, float lr) {
+    if (threadIdx.x == 0) state->lr = lr;
 }
 
 // ----------------------------------------------------------- dispatch ---
@@ -1288,6 +1298,11 @@ hipError_t launch_update(const UpdateArgs& a, ags_dtype dt, hipStream_t s, Kerne
 
 hipError_t launch_correct(const UpdateArgs& a, ags_dtype dt, hipStream_t s, KernelEvents ev) {
     return dt == AGS_BF16 ? correct_t<uint16_t>(a, s, ev) : correct_t<float>(a, s, ev);
+}
+
+hipError_t launch_set_lr(DevState* state, float lr, hipStream_t s) {
+    hipLaunchKernelGGL(set_lr_kernel, dim3(1), dim3(64), 0, s, state, lr);
+    return hipGetLastError();
 }
 
 }  // namespace ags

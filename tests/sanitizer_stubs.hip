@@ -18,5 +18,8 @@ hipError_t launch_update(const UpdateArgs&, ags_dtype, hipStream_t, KernelEvents
 hipError_t launch_correct(const UpdateArgs&, ags_dtype, hipStream_t, KernelEvents) {
     return hipErrorInvalidDeviceFunction;
 }
+hipError_t launch_set_lr(DevState*, float, hipStream_t) {
+    return hipErrorInvalidDeviceFunction;
+}
 
 }  // namespace ags

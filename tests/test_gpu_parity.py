@@ -813,6 +813,53 @@ def test_hip_graph_capture_replays_match_eager(lay_name, K, dtype, hyper):
     graphed.close()
 
 
+@pytest.mark.parametrize("lay_name,K,dtype,hyper", [
+    ("resnet18_cifar", 8, "f32", {}),
+    ("tiny_cnn", 4, "bf16", {"elementwise": True}),
+    ("resnet18_cifar", 8, "f32", {"mode": "lars", "reuse_w_norms": True})])
+def test_set_lr_reaches_graph_replays(lay_name, K, dtype, hyper):
+    """The learning rate lives in the device state: one step captured into a
+    HIP graph, replayed under a schedule set with ags_set_lr between the
+    replays (warm-up, decay, a zero rate), stays bitwise equal to eager
+    steps under the same schedule, and both to the oracle at the last step
+    (the update pass of LARS and the correction pass read it too)."""
+    import torch
+    lay = layouts.get_layout(lay_name)
+    schedule = [0.1, 0.05, 0.2, 0.0, 0.08, 0.1]
+    grads_np = [synth.replica_grads(lay, K, t, 9, dtype=dtype) * (2 if t == 3 else 1)
+                if dtype == "f32" else synth.replica_grads(lay, K, t, 9, dtype=dtype)
+                for t in range(len(schedule))]
+    grads = [to_device(g) for g in grads_np]
+    p = Pair(lay, K, dtype=dtype, seed=9, **hyper)  # "mode" goes to Pair's own argument
+    wg, mg = torch.from_numpy(p.w0.copy()).cuda(), torch.zeros_like(p.w)
+    graphed = ags.AGS(lay.table(), wg, mg, K, grad_dtype=dtype, mode=hyper.get("mode", "ags"),
+                      **p.hyper)
+    try:
+        gbuf = torch.empty_like(grads[0])
+        s = torch.cuda.Stream()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=s):
+            graphed.step(gbuf)
+        torch.cuda.synchronize()
+        for t, (lr, g, g_np) in enumerate(zip(schedule, grads, grads_np)):
+            p.gpu.set_lr(lr)
+            p.gpu.step(g)
+            p.prev_w, p.prev_m = p.ora.w.copy(), p.ora.m.copy()
+            p.ora.step(g_np, lr=lr)
+            graphed.set_lr(lr)
+            gbuf.copy_(g)
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(p.w, wg) and torch.equal(p.m, mg), f"lr {lr}, step {t + 1}"
+        p.check_state(f"{lay_name} lr schedule")
+        del graph
+    finally:
+        graphed.close()
+        p.close()
+
+
 def test_lars_carried_norms_with_graph_capture():
     """LARS with carried weight norms and HIP graphs: a captured step reads
     w (a replay cannot know whether w still holds what the last update
