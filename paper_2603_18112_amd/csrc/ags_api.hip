@@ -538,6 +538,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         ua.momentum = (float)c.momentum;
         ua.w_norm_out = (c.mode == AGS_MODE_LARS) ? h->w_norm() : nullptr;
         ua.lds_pad = h->lds_pad_update;
+        ua.reverse = (8 * c.n_flat <= ags::kOccupancyCapMinBytes) ? 1 : 0;
         e = (c.mode == AGS_MODE_LARS) ? ags::launch_update(ua, c.grad_dtype, s, kev(2))
                                       : ags::launch_correct(ua, c.grad_dtype, s, kev(2));
         if (e != hipSuccess) return launch_fail(e, "second-pass kernel launch");

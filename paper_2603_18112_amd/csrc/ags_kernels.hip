@@ -1166,7 +1166,8 @@ __device__ __forceinline__ void update_group(const UpdateArgs& a, const GT* __re
 
 template <typename GT, int KT, bool RECOMP, bool WN>
 __global__ __launch_bounds__(kTileBlock) void update_kernel(UpdateArgs a) {
-    const Tile t = a.tiles[blockIdx.x];
+    const int ti = a.reverse ? a.n_tiles - 1 - (int)blockIdx.x : (int)blockIdx.x;
+    const Tile t = a.tiles[ti];
     const float2 ab = a.coef[t.layer];
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);
     const int K = KT > 0 ? KT : a.K;
@@ -1183,7 +1184,7 @@ __global__ __launch_bounds__(kTileBlock) void update_kernel(UpdateArgs a) {
         sw = wave_sum(sw);
         if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sw;
         __syncthreads();
-        if (threadIdx.x == 0) a.w_norm_out[blockIdx.x] = tree_sum<kTileBlock / 64>(red);
+        if (threadIdx.x == 0) a.w_norm_out[ti] = tree_sum<kTileBlock / 64>(red);
     }
 }
 
