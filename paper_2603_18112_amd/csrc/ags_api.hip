@@ -308,6 +308,9 @@ struct ags_handle {
     int device = 0;
     int64_t n_tiles = 0;
     int64_t n_chunks = 0;
+    // Fused steps launched outside graph capture: their parity sets the
+    // step kernel's tile direction for layouts that outgrow the cache.
+    int64_t n_fused = 0;
     int64_t grad_extent = 0;  // elements of one replica that are read
     bool materialize = false;
     WsLayout wl;
@@ -497,6 +500,10 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
     sa.corr_flag = h->corr_flag();
     sa.updated = fused ? 1 : 0;
     sa.xcd_map = h->n_tiles >= ags::kXcdMapMinTiles ? 1 : 0;
+    // A captured step keeps the forward direction (its replays cannot
+    // alternate); the results are the same either way, only the order of
+    // the tiles differs.
+    sa.reverse = (fused && !capturing && 8 * c.n_flat > ags::kOccupancyCapMinBytes && (h->n_fused & 1)) ? 1 : 0;
     sa.done_count = h->done_count();
     sa.chunks = reinterpret_cast<const ags::FinChunk*>(h->ws + h->wl.chunks);
     sa.chunk_sums = reinterpret_cast<ags::ChunkSum*>(h->ws + h->wl.chunk_sums);
@@ -544,6 +551,7 @@ ags_status launch_step(ags_handle* h, const void* d_grads, int64_t stride, hipSt
         if (e != hipSuccess) return launch_fail(e, "second-pass kernel launch");
     }
     if (prof) h->ev_pending.push_back(ev);
+    if (fused && !capturing) ++h->n_fused;
     // A captured step has not run: the norms are what the last executed
     // update pass left (every update pass, replayed ones included, writes
     // them for the w it writes).

@@ -932,7 +932,8 @@ template <typename GT, int KT, int RMODE, bool UPD, int EW, bool WNC = false, bo
 __global__ __launch_bounds__(kTileBlock) void step_kernel(StepArgs a) {
     constexpr bool ELEM = EW != 0;
     __shared__ float red[5][kTileBlock / 64];
-    const int ti = tile_of_block(blockIdx.x, gridDim.x, a.xcd_map);
+    const int tb = tile_of_block(blockIdx.x, gridDim.x, a.xcd_map);
+    const int ti = a.reverse ? (int)gridDim.x - 1 - tb : tb;
     const Tile t = a.tiles[ti];
     const int l = t.layer;
     const GT* __restrict__ g = static_cast<const GT*>(a.grads);

@@ -21,7 +21,9 @@
 //         a contiguous range per XCD) and with load batches of 8 and 16
 //         (bf16 rows, or fp32 half rows) or, for bf16 rows, two batches of
 //         4 or 8 pipelined as the step kernel does, with w and m loaded
-//         before the replicas or after the first batch, and the fastest counts: how many
+//         before the replicas or after the first batch, and (warm) with the
+//         tile direction alternating from launch to launch as the step
+//         kernel's does for large layouts, and the fastest counts: how many
 //         streams run at once, and where, decides how well the DRAM rows
 //         are used.
 // Usage: hbm_probe [K grad_dtype(bf16|f32) n_elements [ew]]; without
@@ -109,7 +111,7 @@ __device__ __forceinline__ void add_bf16x8(const u32x4& v, float (&s)[8]) {
 // flight while the current one is summed.  With xcd, block b
 // takes the tile that the step kernel's XCD-aware order gives it (each of
 // the 8 XCDs, which receive every 8th block, walks a contiguous range of
-// tiles) instead of tile b.  w and m: the same
+// tiles) instead of tile b; with xcd & 2 the tiles run in reverse order.  w and m: the same
 // elements, fp32, read and written.  EW (element scales): one more fp32
 // stream read (sc_in) and one written (sc_out) for the same elements, with
 // ordinary accesses (EW = 1) or streaming ones, w and m stores included
@@ -124,10 +126,11 @@ __global__ __launch_bounds__(256) void probe_step(const void* __restrict__ grads
                                                   float* __restrict__ sc_out, int xcd) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int tile = blockIdx.x;
-    if (xcd) {
+    if (xcd & 1) {
         const int n = gridDim.x, q = n / 8, r = n % 8, x = tile % 8, i = tile / 8;
         tile = (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
     }
+    if (xcd & 2) tile = (int)gridDim.x - 1 - tile;  // reverse direction
     const size_t base = (size_t)tile * kTile + (size_t)wave * 512;
     const size_t i0 = base + (BF16 ? 8 * lane : 4 * lane);
     const size_t i1 = BF16 ? i0 + 4 : i0 + 256;
@@ -429,17 +432,23 @@ int main(int argc, char** argv) {
     }
     // With element scales, the faster of ordinary and streaming accesses for
     // the scale streams (and the w and m stores) is the pattern's rate.
-    int best_ew = ew ? 1 : 0, best_pad = 0, best_xcd = 0, best_deep = 0;
+    // Warm launches also run with the direction alternating from launch to
+    // launch (zig), as the step kernel does once w and m outgrow the
+    // Infinity Cache.
+    int best_ew = ew ? 1 : 0, best_pad = 0, best_xcd = 0, best_deep = 0, best_zig = 0;
     double step_us = 0;
     for (int v = ew ? 1 : 0; v <= (ew ? 2 : 0); ++v) {
-        for (int c = 0; c < 2 * kScheds * n_pads; ++c) {
-            const int pi = c % n_pads, xcd = (c / n_pads) & 1, deep = c / (2 * n_pads);
+        for (int c = 0; c < 4 * kScheds * n_pads; ++c) {
+            const int pi = c % n_pads, xcd = (c / n_pads) & 1, deep = (c / (2 * n_pads)) % kScheds,
+                      zig = c / (2 * kScheds * n_pads);
             if (!pipelined_ok(bf16, K, deep)) continue;
             double us = 0;
+            int calls = 0;
             const int rc = time_launches(
                 [&]() {
-                    launch_step_pattern(bf16, v, grid, g, stride, K, w, m, sc_in, sc_out, pads[pi], xcd,
-                                        deep);
+                    const int dir = (zig && (calls++ & 1)) ? 2 : 0;
+                    launch_step_pattern(bf16, v, grid, g, stride, K, w, m, sc_in, sc_out, pads[pi],
+                                        xcd | dir, deep);
                 },
                 50, e0, e1, &us);
             if (rc) return rc;
@@ -449,6 +458,7 @@ int main(int argc, char** argv) {
                 best_pad = pi;
                 best_xcd = xcd;
                 best_deep = deep;
+                best_zig = zig;
             }
         }
     }
@@ -497,6 +507,7 @@ int main(int argc, char** argv) {
            "\"step_pattern_cold_GBps\": %.1f, \"step_pattern_cold_us\": %.2f, "
            "\"step_pattern_blocks_per_cu\": %d, \"step_pattern_cold_blocks_per_cu\": %d, "
            "\"step_pattern_xcd_order\": %s, \"step_pattern_cold_xcd_order\": %s, "
+           "\"step_pattern_alternating\": %s, "
            "\"step_pattern_load_batch\": \"%s\", \"step_pattern_cold_load_batch\": \"%s\", "
            "\"step_pattern\": "
            "{\"K\": %d, \"grad_dtype\": \"%s\", \"elements\": %zu, \"bytes_per_element\": %zu, "
@@ -504,7 +515,8 @@ int main(int argc, char** argv) {
            "\"bytes\": %zu, \"data\": \"random\"}\n",
            best[0], best_grid[0], best[1], best_grid[1], step_bytes / (step_us * 1e-6) / 1e9, step_us,
            step_bytes / (cold_us * 1e-6) / 1e9, cold_us, caps[best_pad], caps[best_cold_pad],
-           best_xcd ? "true" : "false", best_cold_xcd ? "true" : "false", kSchedName[best_deep],
+           best_xcd ? "true" : "false", best_cold_xcd ? "true" : "false", best_zig ? "true" : "false",
+           kSchedName[best_deep],
            kSchedName[best_cold_deep], K,
            bf16 ? "bf16" : "f32", ne, bpe,
            !ew ? "null" : (best_ew == 2 ? "\"streaming\"" : "\"ordinary\""), bytes);
